@@ -1,0 +1,461 @@
+"""ResKV oracle: a plain, slow, fp64 statement of what the hot path computes.
+
+This module is TEST INFRASTRUCTURE. Only the test suite, the package smoke
+check and the CPU-baseline leg of the benchmark may import it. The product
+path (the HIP library and its Python binding) never calls it and shares no
+code with it: no kernels, headers, helpers, tables or pre/post-processing.
+Inputs come from the seeded generators, which hold none of the method's
+arithmetic; everything below is written from the paper's definitions.
+
+Every floating-point step runs in float64. Inputs stored in bf16 or fp32 are
+exactly representable in float64, so they are upcast without loss.
+
+Paper map (section / equation / algorithm):
+  full attention ............ Sec. 3.1, attention equation
+  eviction attention ........ Sec. 3.2, eviction equation
+  Z / N statistics .......... Sec. 4.2, (Z, N) definition; App. A.1 decomposition
+  main selection ............ Sec. 5.2, main-selection equation
+  observation-window scores . App. B.2.2 (SnapKV rule: observation window,
+                              average pooling with kernel 5, recent protection)
+  residual partition ........ Sec. 5.3, key-space partition objective, solved
+                              with Lloyd iterations seeded from the
+                              highest-scored evicted tokens (App. B.3)
+  residual summary .......... Sec. 5.3, summary equation (mean key, mean value,
+                              count); App. B.3 (count exponent beta)
+  shared-softmax decode ..... Sec. 5.4, residual-logit, denominator, numerator
+                              and output equations; App. D, Algorithm 2
+  dynamic gate .............. Sec. 5.5.2, gate equation; App. A.3
+
+Readings taken where the paper is silent (each also listed in the design
+notes of the repository):
+  R1  window scores use causal masking inside the observation window and each
+      window row is normalised over every key it can see;
+  R2  scores of the query heads that share a KV head are summed;
+  R3  pooling is a centred 5-tap sum with zero padding over the scored range;
+  R4  the protected recent window is |P| = min(recent_window, m) last tokens and
+      only the positions before it are scored;
+  R6  score ties are broken by the lower position;
+  R7  Lloyd seeds are the evicted tokens of rank k_top .. k_top+r-1 in the
+      selection order; centre j is the j-th seed by ascending position;
+      assignment ties go to the lower centre index;
+  R8  one Lloyd iteration is one assignment plus one update; the entries come
+      from the T-th assignment;
+  R9  an empty cluster keeps its centre; a final count of 0 marks the entry
+      empty (log-count -inf, value 0) and it contributes nothing at decode;
+  R10 mean key and mean value are stored in the cache dtype, rounded once to
+      nearest-even; log-counts are fp32;
+  R12 single-token residual entries reproduce full attention only with the
+      gate held at 1 (g_min = 1);
+  R13 p_max covers every main slot, including tokens appended during decode.
+"""
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "round_to_dtype", "full_attention", "evict_attention", "zn_stats",
+    "window_raw_scores", "pool5", "scored_length", "select_main",
+    "lloyd", "lloyd_objective", "assign_nearest", "residual_entries",
+    "build_head", "build_cache", "gate_value", "decode_head", "decode",
+]
+
+_F64 = np.float64
+
+
+# --------------------------------------------------------------------------
+# storage rounding of the oracle's own outputs (R10)
+# --------------------------------------------------------------------------
+
+def _round_bf16(x):
+    """Round float64 values to the nearest bf16 value, ties to even.
+
+    bf16 keeps 8 significant bits; the quantum of a value with binary exponent
+    e (x = f * 2**e, 0.5 <= |f| < 1) is 2**(e-8), floored at the subnormal
+    quantum 2**-133. Dividing by a power of two is exact in float64, and
+    np.rint rounds halves to even.
+    """
+    x = np.asarray(x, dtype=_F64)
+    out = np.zeros_like(x)
+    nz = (x != 0) & np.isfinite(x)
+    _, e = np.frexp(x[nz])
+    q = np.maximum(e - 8, -133).astype(_F64)
+    scale = np.exp2(q)
+    out[nz] = np.rint(x[nz] / scale) * scale
+    out[~np.isfinite(x)] = x[~np.isfinite(x)]
+    big = np.abs(out) > 3.3895313892515355e38  # largest finite bf16
+    out[big] = np.sign(out[big]) * np.inf
+    return out
+
+
+def round_to_dtype(x, dtype):
+    """Value of float64 `x` after storage in `dtype` ('bf16' or 'f32')."""
+    if dtype == "bf16":
+        return _round_bf16(x)
+    if dtype == "f32":
+        return np.asarray(x, dtype=_F64).astype(np.float32).astype(_F64)
+    raise ValueError(dtype)
+
+
+# --------------------------------------------------------------------------
+# plain attention definitions (Sec. 3.1, Sec. 3.2, Sec. 4.2)
+# --------------------------------------------------------------------------
+
+def _logits(q, K):
+    d = K.shape[-1]
+    return (np.asarray(K, _F64) @ np.asarray(q, _F64)) / math.sqrt(d)
+
+
+def full_attention(q, K, V):
+    """o = softmax(q K^T / sqrt(d)) V  (Sec. 3.1, attention equation)."""
+    a = _logits(q, K)
+    w = np.exp(a - a.max())
+    return (w @ np.asarray(V, _F64)) / w.sum()
+
+
+def evict_attention(q, K, V, kept):
+    """Attention over the kept rows only (Sec. 3.2, eviction equation)."""
+    kept = np.asarray(kept, dtype=np.int64)
+    return full_attention(q, np.asarray(K)[kept], np.asarray(V)[kept])
+
+
+def zn_stats(q, K, V, subset):
+    """(log Z_T, N_T / Z_T-free form) for a token subset T (Sec. 4.2).
+
+    Returns (Z, N) with Z = sum_{p in T} e^{a_p}, N = sum_{p in T} e^{a_p} v_p,
+    both scaled by e^{-c} for the shift c returned as the third item, so that
+    Z * e^c and N * e^c are the paper's statistics without overflow.
+    """
+    subset = np.asarray(subset, dtype=np.int64)
+    a = _logits(q, np.asarray(K)[subset])
+    c = a.max() if a.size else 0.0
+    w = np.exp(a - c)
+    return w.sum(), w @ np.asarray(V, _F64)[subset], c
+
+
+# --------------------------------------------------------------------------
+# observation-window scoring (App. B.2.2, SnapKV rule; readings R1-R4)
+# --------------------------------------------------------------------------
+
+def scored_length(s, m, recent_window):
+    """Number of scored positions: everything before the protected window."""
+    p = min(recent_window, m, s)
+    return s - p
+
+
+def window_raw_scores(K, Qw):
+    """Per-key attention mass from the observation window.
+
+    K  : [s, d] prefill keys of one KV head.
+    Qw : [G, w, d] window queries of the G query heads sharing that KV head;
+         row i of each head sits at position s - w + i.
+    Returns raw[s]: raw[p] = sum over window rows t that can see p (p <= pos(t))
+    of softmax_t[p], where softmax_t normalises over every key row t can see
+    (R1), summed over the G heads of the group (R2).
+    """
+    K = np.asarray(K, _F64)
+    Qw = np.asarray(Qw, _F64)
+    s, d = K.shape
+    G, w, _ = Qw.shape
+    raw = np.zeros(s, dtype=_F64)
+    for h in range(G):
+        a = (Qw[h] @ K.T) / math.sqrt(d)              # [w, s]
+        pos = s - w + np.arange(w)
+        visible = np.arange(s)[None, :] <= pos[:, None]
+        a = np.where(visible, a, -np.inf)
+        a = a - a.max(axis=1, keepdims=True)
+        e = np.exp(a)
+        soft = e / e.sum(axis=1, keepdims=True)
+        raw += soft.sum(axis=0)
+    return raw
+
+
+def pool5(raw):
+    """Centred 5-tap sum with zero padding (R3): out[p] = sum_{i=-2..2} raw[p+i]."""
+    raw = np.asarray(raw, _F64)
+    n = raw.shape[0]
+    out = np.zeros(n, dtype=_F64)
+    for off in range(-2, 3):
+        lo = max(0, -off)
+        hi = min(n, n - off)
+        out[lo:hi] += raw[lo + off:hi + off]
+    return out
+
+
+# --------------------------------------------------------------------------
+# main selection (Sec. 5.2, main-selection equation; R4, R6, R7)
+# --------------------------------------------------------------------------
+
+def select_main(scores, s, m, recent_window, r):
+    """M = P  U  Top_{m-|P|}(s),  E = S \\ M, plus the Lloyd seeds.
+
+    scores : [n] pooled scores of positions 0..n-1, n = scored_length(...).
+    Returns (main_idx ascending, evicted ascending, seeds ascending).
+    When s <= m every token is kept and nothing is evicted.
+    """
+    if s <= m:
+        return np.arange(s), np.zeros(0, np.int64), np.zeros(0, np.int64)
+    p = min(recent_window, m, s)
+    n = s - p
+    k_top = m - p
+    scores = np.asarray(scores, _F64)
+    assert scores.shape[0] == n
+    # order: score descending, then position ascending
+    order = np.lexsort((np.arange(n), -scores))
+    top = order[:k_top]
+    main = np.sort(np.concatenate([top, np.arange(n, s)]))
+    evicted = np.sort(order[k_top:])
+    seeds = np.sort(order[k_top:k_top + r])
+    return main, evicted, seeds
+
+
+# --------------------------------------------------------------------------
+# residual partition by Lloyd iterations (Sec. 5.3; App. B.3; R7-R9)
+# --------------------------------------------------------------------------
+
+def assign_nearest(KE, centers):
+    """argmin_j ||k_p - mu_j||^2 in direct-difference form; ties -> lowest j.
+
+    Returns (assignment [n], squared distances [n, r]).
+    """
+    KE = np.asarray(KE, _F64)
+    centers = np.asarray(centers, _F64)
+    n = KE.shape[0]
+    r = centers.shape[0]
+    dist = np.empty((n, r), dtype=_F64)
+    step = max(1, (1 << 22) // max(1, r * KE.shape[1]))
+    for lo in range(0, n, step):
+        diff = KE[lo:lo + step, None, :] - centers[None, :, :]
+        dist[lo:lo + step] = np.einsum("prd,prd->pr", diff, diff)
+    return np.argmin(dist, axis=1), dist
+
+
+def lloyd_objective(KE, assign, r):
+    """sum_j sum_{p in C_j} ||k_p - kbar_j||^2 (Sec. 5.3, partition objective)."""
+    KE = np.asarray(KE, _F64)
+    tot = 0.0
+    for j in range(r):
+        mem = KE[assign == j]
+        if mem.shape[0]:
+            tot += float(((mem - mem.mean(axis=0)) ** 2).sum())
+    return tot
+
+
+def lloyd(KE, init_centers, iters):
+    """`iters` rounds of (assign, update) from the given centres (R8, R9).
+
+    Returns (final assignment, final centres, per-iteration history of
+    (assignment, centres before that assignment)).
+    """
+    mu = np.array(init_centers, dtype=_F64, copy=True)
+    KE = np.asarray(KE, _F64)
+    history = []
+    assign = np.zeros(KE.shape[0], dtype=np.int64)
+    for _ in range(iters):
+        prev = mu.copy()
+        assign, _ = assign_nearest(KE, mu)
+        for j in range(mu.shape[0]):
+            mem = KE[assign == j]
+            if mem.shape[0]:
+                mu[j] = mem.mean(axis=0)
+        history.append((assign.copy(), prev))
+    return assign, mu, history
+
+
+def residual_entries(KE, VE, assign, centers, r, d):
+    """Mean key, mean value and count per group (Sec. 5.3, summary equation).
+
+    Entries j >= number of centres, and groups with no member, are empty:
+    count 0, mean value 0, mean key = the centre (or 0), log-count -inf (R9).
+    """
+    kbar = np.zeros((r, d), _F64)
+    vbar = np.zeros((r, d), _F64)
+    cnt = np.zeros(r, dtype=np.int64)
+    KE = np.asarray(KE, _F64)
+    VE = np.asarray(VE, _F64)
+    for j in range(len(centers)):
+        kbar[j] = centers[j]
+        mem = assign == j
+        c = int(mem.sum())
+        cnt[j] = c
+        if c:
+            vbar[j] = VE[mem].mean(axis=0)
+    with np.errstate(divide="ignore"):
+        logc = np.where(cnt > 0, np.log(np.maximum(cnt, 1).astype(_F64)), -np.inf)
+    return kbar, vbar, cnt, logc
+
+
+# --------------------------------------------------------------------------
+# construction of one (layer, KV head) (App. D, Algorithm 1 with r given)
+# --------------------------------------------------------------------------
+
+def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16"):
+    """Construct the main + residual layout for one (layer, KV head).
+
+    K, V : [s, d] prefill keys/values (values already in the storage dtype).
+    Qw   : [G, w, d] window queries.
+    Returns a dict with the scores, selection, Lloyd record and the cache
+    rows in slot order: residual entries in slots [0, r), main tokens in
+    slots [r, r + main_len).
+    """
+    K = np.asarray(K, _F64)
+    V = np.asarray(V, _F64)
+    s = K.shape[0]
+    out = {}
+    if s <= m:
+        main = np.arange(s)
+        evicted = np.zeros(0, np.int64)
+        seeds = np.zeros(0, np.int64)
+        out["scores"] = np.zeros(0)
+    else:
+        n = scored_length(s, m, recent_window)
+        raw = window_raw_scores(K, Qw)
+        out["raw"] = raw
+        scores = pool5(raw[:n])
+        out["scores"] = scores
+        main, evicted, seeds = select_main(scores, s, m, recent_window, r)
+    out["main_idx"], out["evicted"], out["seeds"] = main, evicted, seeds
+    KE, VE = K[evicted], V[evicted]
+    centers0 = K[seeds]
+    if r > 0 and evicted.size > 0:
+        assign, mu, hist = lloyd(KE, centers0, lloyd_iters)
+    else:
+        assign, mu, hist = np.zeros(evicted.size, np.int64), centers0, []
+    out["assign"], out["centers"], out["lloyd_history"] = assign, mu, hist
+    kbar, vbar, cnt, logc = residual_entries(KE, VE, assign, mu, r, K.shape[1])
+    out["counts"], out["logc"] = cnt, logc
+    out["kbar64"], out["vbar64"] = kbar, vbar
+    kres = round_to_dtype(kbar, dtype)
+    vres = round_to_dtype(vbar, dtype)
+    out["kc"] = np.concatenate([kres, K[main]], axis=0)
+    out["vc"] = np.concatenate([vres, V[main]], axis=0)
+    out["res_len"] = r
+    out["main_len"] = main.size
+    return out
+
+
+def build_cache(K, V, Qobs, seq_len, budget, res_count, recent_window,
+                lloyd_iters, dtype, slot_cap, res_cap, heads=None):
+    """Run build_head over (batch, KV head) and lay the result out as the
+    library's cache tensors.
+
+    K, V     : [B, Hkv, S, d]; Qobs : [B, Hq, w, d]; seq_len, budget : [B];
+    res_count : [B, Hkv]. `heads` optionally restricts to a list of
+    (b, kvh) pairs; other rows stay zero.
+    Returns kc, vc [B, Hkv, C, d], logc [B, Hkv, Rcap], main_idx [B, Hkv, C],
+    res_len, main_len [B, Hkv], plus per-head records.
+    """
+    K = np.asarray(K)
+    B, Hkv, S, d = K.shape
+    Hq = Qobs.shape[1]
+    G = Hq // Hkv
+    kc = np.zeros((B, Hkv, slot_cap, d))
+    vc = np.zeros((B, Hkv, slot_cap, d))
+    logc = np.full((B, Hkv, res_cap), -np.inf)
+    main_idx = np.full((B, Hkv, slot_cap), -1, dtype=np.int64)
+    res_len = np.zeros((B, Hkv), np.int64)
+    main_len = np.zeros((B, Hkv), np.int64)
+    recs = {}
+    todo = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hkv)]
+    for b, h in todo:
+        s = int(seq_len[b])
+        r = int(res_count[b][h])
+        m = int(budget[b]) - r
+        rec = build_head(K[b, h, :s], V[b, h, :s], Qobs[b, h * G:(h + 1) * G],
+                         m, r, recent_window, lloyd_iters, dtype)
+        n = rec["kc"].shape[0]
+        kc[b, h, :n] = rec["kc"]
+        vc[b, h, :n] = rec["vc"]
+        logc[b, h, :r] = rec["logc"]
+        main_idx[b, h, :rec["main_len"]] = rec["main_idx"]
+        res_len[b, h] = r
+        main_len[b, h] = rec["main_len"]
+        recs[(b, h)] = rec
+    return dict(kc=kc, vc=vc, logc=logc, main_idx=main_idx, res_len=res_len,
+                main_len=main_len, records=recs)
+
+
+# --------------------------------------------------------------------------
+# shared-softmax decode with the dynamic gate (Sec. 5.4, Sec. 5.5.2, Alg. 2)
+# --------------------------------------------------------------------------
+
+def gate_value(p_max, tau, alpha, g_min):
+    """g = max(g_min, sigmoid((tau - p_max) / T_g)) with T_g = 1/alpha."""
+    x = (tau - p_max) * alpha
+    with np.errstate(over="ignore"):
+        sig = 1.0 / (1.0 + math.exp(-x)) if x > -700 else 0.0
+    return max(g_min, sig)
+
+
+def decode_head(q, Kmain, Vmain, Kres, Vres, logc, tau, alpha, g_min, beta):
+    """One query against one KV head's cache, in Algorithm 2's order.
+
+    Returns (output [d], debug dict with lse_main, lse_res, gate, p_max).
+    lse_res is log sum_j exp(<q, kbar_j>/sqrt(d) + beta*log c_j) before the
+    gate shift (-inf when no entry is populated).
+    """
+    q = np.asarray(q, _F64)
+    d = q.shape[0]
+    Kmain = np.asarray(Kmain, _F64)
+    Vmain = np.asarray(Vmain, _F64)
+    # main logits a_p = <q, k_p>/sqrt(d)
+    a = (Kmain @ q) / math.sqrt(d)
+    amax = a.max()
+    wm = np.exp(a - amax)
+    # p_max = max_p e^{a_p} / sum_p' e^{a_p'}
+    p_max = float(wm.max() / wm.sum())
+    g = gate_value(p_max, tau, alpha, g_min)
+    log_g = math.log(g) if g > 0 else -np.inf
+    # residual logits: <q, kbar_j>/sqrt(d) + beta*log c_j + log g; empty
+    # entries (log c = -inf) are left out entirely.
+    logc = np.asarray(logc, _F64)
+    live = np.isfinite(logc)
+    Kres = np.asarray(Kres, _F64)[live]
+    Vres = np.asarray(Vres, _F64)[live]
+    ares_nogate = (Kres @ q) / math.sqrt(d) + beta * logc[live]
+    ares = ares_nogate + log_g
+    # one shared softmax over main logits and residual logits
+    all_a = np.concatenate([a, ares])
+    top = all_a.max()
+    w = np.exp(all_a - top)
+    num = w[:a.size] @ Vmain + (w[a.size:] @ Vres if Kres.shape[0] else 0.0)
+    den = w.sum()
+    out = num / den
+    lse_main = amax + math.log(wm.sum())
+    if ares_nogate.size:
+        t = ares_nogate.max()
+        lse_res = t + math.log(np.exp(ares_nogate - t).sum())
+    else:
+        lse_res = -np.inf
+    return out, dict(lse_main=lse_main, lse_res=lse_res, gate=g, p_max=p_max)
+
+
+def decode(q, kc, vc, logc, res_len, main_len, tau, alpha, g_min, beta, heads=None):
+    """Decode one step for every (batch, query head).
+
+    q : [B, Hq, d]; kc, vc : [B, Hkv, C, d]; logc : [B, Hkv, Rcap];
+    res_len, main_len : [B, Hkv]; tau : scalar or [B, Hq].
+    Returns out [B, Hq, d], lse_main, lse_res, gate [B, Hq].
+    """
+    q = np.asarray(q, _F64)
+    B, Hq, d = q.shape
+    Hkv = kc.shape[1]
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, d))
+    lse_m = np.zeros((B, Hq))
+    lse_r = np.zeros((B, Hq))
+    gate = np.zeros((B, Hq))
+    tau = np.broadcast_to(np.asarray(tau, _F64), (B, Hq))
+    todo = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hq)]
+    for b, h in todo:
+        kv = h // G
+        r = int(res_len[b, kv])
+        n = int(main_len[b, kv])
+        o, dbg = decode_head(q[b, h], kc[b, kv, r:r + n], vc[b, kv, r:r + n],
+                             kc[b, kv, :r], vc[b, kv, :r], logc[b, kv, :r],
+                             float(tau[b, h]), alpha, g_min, beta)
+        out[b, h] = o
+        lse_m[b, h] = dbg["lse_main"]
+        lse_r[b, h] = dbg["lse_res"]
+        gate[b, h] = dbg["gate"]
+    return out, lse_m, lse_r, gate
