@@ -1,0 +1,197 @@
+/*
+ * reskv.h - C ABI of the ResKV hot path on AMD Instinct MI355X (gfx950).
+ *
+ * ResKV keeps, per (layer, KV head), a fixed budget of b = m + r cache slots:
+ * m exact "main" tokens and r "residual" entries that summarise the evicted
+ * tokens by a mean key, a mean value and a population count (Sec. 5.1-5.3 of
+ * the paper). At decode, main tokens and residual entries share one softmax;
+ * the residual logits carry log-count and a per-query dynamic gate (Sec. 5.4,
+ * Sec. 5.5.2; App. D, Algorithm 2).
+ *
+ * One call handles one layer. All tensors are caller-owned device buffers
+ * (row-major, innermost dimension last) unless a name ends in _host. The
+ * library allocates nothing, keeps no pointer after a call returns, and
+ * enqueues its kernels on the caller's HIP stream (passed as void*, i.e. a
+ * hipStream_t; NULL is the null stream). Calls are asynchronous: argument
+ * errors are reported by the return value before anything is launched;
+ * faults inside a kernel surface at the caller's next synchronisation.
+ *
+ * Shapes: B = batch, Hq / Hkv = query / KV heads with Hq % Hkv == 0 and
+ * G = Hq / Hkv <= 16 (grouped-query attention: query head h reads KV head
+ * h / G, and the G heads of a group share its main indices and residual
+ * entries, Sec. 6.1 and App. B), d = head_dim in {64, 128}, S = row stride
+ * of the prefill K/V, C = slot capacity per (sequence, KV head), Rcap =
+ * residual capacity.
+ *
+ * Cache layout per (b, kv head): slots [0, r) hold residual entries (mean
+ * key / mean value, log-count in logc[0..r)); slots [r, r + main_len) hold
+ * main tokens in ascending source position, followed by tokens appended
+ * during decode. res_len[b*Hkv + h] = r, main_len[b*Hkv + h] = main slots.
+ */
+#ifndef RESKV_H
+#define RESKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RESKV_OK = 0,
+  RESKV_ERR_INVALID_ARG = 1,  /* shape, pointer or parameter out of range */
+  RESKV_ERR_UNSUPPORTED = 2,  /* valid but not implemented (d, G, dtype) */
+  RESKV_ERR_WORKSPACE = 3,    /* workspace missing or too small */
+  RESKV_ERR_HIP = 4           /* a HIP runtime call failed at launch */
+} reskv_status_t;
+
+typedef enum { RESKV_F32 = 0, RESKV_BF16 = 1 } reskv_dtype_t;
+
+typedef struct {
+  int32_t batch;         /* B >= 1 */
+  int32_t num_q_heads;   /* Hq, multiple of Hkv, Hq / Hkv <= 16 */
+  int32_t num_kv_heads;  /* Hkv >= 1 */
+  int32_t head_dim;      /* d: 64 or 128 */
+  int32_t dtype;         /* reskv_dtype_t of every K/V/q tensor */
+  int32_t slot_cap;      /* C: slots per (b, kv head) of kc, vc, main_idx */
+  int32_t res_cap;       /* Rcap >= 1: entries per (b, kv head) of logc */
+} reskv_shape_t;
+
+typedef struct {
+  int32_t max_seq_len;   /* S: row stride (in rows) of k and v */
+  int32_t obs_window;    /* w: observation-window queries per q head, 1..S */
+  int32_t recent_window; /* |P| before clamping to m: protected last tokens */
+  int32_t lloyd_iters;   /* T >= 1: (assign, update) rounds, App. B.3 uses 4 */
+} reskv_build_params_t;
+
+typedef struct {
+  const float* tau;      /* device [B*Hq] per-query threshold, or NULL */
+  float tau_scalar;      /* threshold when tau == NULL (App. B.3: 0.25) */
+  float alpha;           /* sigmoid slope 1/T_g (App. B.3: 12) */
+  float g_min;           /* gate floor in [0, 1] (App. B.3: 0) */
+  float beta;            /* log-count exponent (App. B.3: 1) */
+} reskv_gate_t;
+
+/*
+ * reskv_build_cache - construct the main + residual cache of one layer from
+ * its prefill K/V (App. D, Algorithm 1 with r given per (b, kv head)).
+ *
+ * Steps, per (b, kv head): observation-window scores (App. B.2.2: window
+ * queries at positions s-w..s-1 attend causally, softmax per row, summed
+ * over the G query heads, 5-tap zero-padded pooling over the positions
+ * before the protected window); main selection M = P u Top_{m-|P|}(scores)
+ * with ties to the lower position (Sec. 5.2, main-selection equation);
+ * Lloyd partition of the evicted set E = S \ M into r groups, seeded by the
+ * evicted tokens ranked k_top..k_top+r-1 (Sec. 5.3, partition objective;
+ * App. B.3); entries = (mean key, mean value, count) of the final groups
+ * (Sec. 5.3, summary equation).
+ *
+ *   k, v            [B, Hkv, S, d]   prefill keys/values (rows >= s unused)
+ *   seq_len_host    [B]              s per sequence, w <= s <= S
+ *   q_obs           [B, Hq, w, d]    window queries (row i at position s-w+i)
+ *   budget_host     [B]              b per KV head of sequence b, b <= C
+ *   res_count_host  [B*Hkv]          r, 0 <= r < b, r <= Rcap
+ *   kc, vc          [B, Hkv, C, d]   out: slots [0,r) residual, [r,r+m') main
+ *   logc            [B, Hkv, Rcap]   out fp32: log c_j, -inf if group empty
+ *   main_idx        [B, Hkv, C]      out int32: source positions of main
+ *                                    slots, ascending; m' = min(m, s) valid
+ *   res_len         [B*Hkv]          out int32: r
+ *   main_len        [B*Hkv]          out int32: m' = min(b - r, s)
+ *   dbg_scores      [B, Hkv, S]      optional (NULL): pooled scores, fp32
+ *   dbg_assign      [T, B, Hkv, S]   optional (NULL): per Lloyd round, the
+ *                                    group of each evicted position (-1 for
+ *                                    main positions and rows >= s)
+ *   workspace       device scratch of reskv_build_workspace_size() bytes
+ *
+ * When s <= m every token is main and the r residual entries are empty.
+ * Returns RESKV_OK or an error code before launching anything.
+ */
+reskv_status_t reskv_build_cache(const reskv_shape_t* shape,
+                                 const reskv_build_params_t* params,
+                                 const void* k, const void* v,
+                                 const int32_t* seq_len_host,
+                                 const void* q_obs,
+                                 const int32_t* budget_host,
+                                 const int32_t* res_count_host,
+                                 void* kc, void* vc, float* logc,
+                                 int32_t* main_idx,
+                                 int32_t* res_len, int32_t* main_len,
+                                 float* dbg_scores, int32_t* dbg_assign,
+                                 void* workspace, size_t workspace_bytes,
+                                 void* stream);
+
+/* Bytes of device workspace reskv_build_cache needs for these arguments
+ * (0 if the arguments are invalid). */
+size_t reskv_build_workspace_size(const reskv_shape_t* shape,
+                                  const reskv_build_params_t* params,
+                                  const int32_t* seq_len_host,
+                                  const int32_t* budget_host,
+                                  const int32_t* res_count_host);
+
+/*
+ * reskv_decode_attn - one decode step of shared-softmax attention for one
+ * layer (Sec. 5.4: residual-logit, denominator, numerator and output
+ * equations; Sec. 5.5.2: gate; App. D, Algorithm 2).
+ *
+ * For query head h of sequence b (KV head kv = h / G, r = res_len, n =
+ * main_len):
+ *   a_p   = <q, k_p> / sqrt(d)                           main slots
+ *   p_max = max_p e^{a_p} / sum_p e^{a_p}
+ *   g     = max(g_min, sigmoid((tau - p_max) * alpha))
+ *   at_j  = <q, kbar_j> / sqrt(d) + beta * logc_j + log g  residual slots
+ *   out   = (sum e^{a_p} v_p + sum e^{at_j} vbar_j) / (sum e^{a_p} + sum e^{at_j})
+ * Entries with logc = -inf contribute nothing. main_len must be >= 1.
+ *
+ *   q               [B, Hq, d]       this step's queries
+ *   kc, vc, logc    cache as written by reskv_build_cache / reskv_append_kv
+ *   res_len, main_len  [B*Hkv] int32, read on the device
+ *   out             [B, Hq, d] fp32
+ *   dbg_lse_main    [B*Hq] optional: log sum_p e^{a_p}
+ *   dbg_lse_res     [B*Hq] optional: log sum_j e^{<q,kbar_j>/sqrt(d) + beta logc_j}
+ *   dbg_gate        [B*Hq] optional: g
+ *   workspace       device scratch of reskv_decode_workspace_size() bytes
+ *
+ * Lengths read on the device are clamped to the capacities, so corrupt
+ * lengths cannot make the kernels read outside the cache.
+ */
+reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
+                                 const reskv_gate_t* gate,
+                                 const void* q,
+                                 const void* kc, const void* vc,
+                                 const float* logc,
+                                 const int32_t* res_len,
+                                 const int32_t* main_len,
+                                 float* out,
+                                 float* dbg_lse_main, float* dbg_lse_res,
+                                 float* dbg_gate,
+                                 void* workspace, size_t workspace_bytes,
+                                 void* stream);
+
+/* Bytes of device workspace reskv_decode_attn needs (0 if invalid). */
+size_t reskv_decode_workspace_size(const reskv_shape_t* shape);
+
+/*
+ * reskv_append_kv - append one decode token per (b, kv head) as a main slot
+ * (Sec. 3.1: each decode step appends the new token's key and value).
+ * Writes k_new/v_new [B, Hkv, d] into slot res_len + main_len and increments
+ * main_len, on the device. A (b, kv head) whose cache is full (res_len +
+ * main_len == C) is left unchanged.
+ */
+reskv_status_t reskv_append_kv(const reskv_shape_t* shape,
+                               const void* k_new, const void* v_new,
+                               void* kc, void* vc,
+                               const int32_t* res_len, int32_t* main_len,
+                               void* stream);
+
+/* Static description of a status code. */
+const char* reskv_status_string(reskv_status_t status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* reskv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RESKV_H */

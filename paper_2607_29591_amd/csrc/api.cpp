@@ -1,0 +1,173 @@
+// C ABI of the ResKV hot path: argument validation, workspace sizing and
+// launch on the caller's stream. Every check runs on the host before any
+// kernel is enqueued.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "internal.h"
+
+using namespace reskv;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+reskv_status_t fail(reskv_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+reskv_status_t fail(reskv_status_t st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+reskv_status_t ok() {
+  g_last_error[0] = '\0';
+  return RESKV_OK;
+}
+
+reskv_status_t check_shape(const reskv_shape_t* s) {
+  if (!s) return fail(RESKV_ERR_INVALID_ARG, "shape is NULL");
+  if (s->batch < 1) return fail(RESKV_ERR_INVALID_ARG, "batch must be >= 1 (got %d)", s->batch);
+  if (s->num_kv_heads < 1 || s->num_q_heads < 1)
+    return fail(RESKV_ERR_INVALID_ARG, "head counts must be >= 1 (Hq=%d, Hkv=%d)", s->num_q_heads, s->num_kv_heads);
+  if (s->num_q_heads % s->num_kv_heads != 0)
+    return fail(RESKV_ERR_INVALID_ARG, "Hq (%d) must be a multiple of Hkv (%d)", s->num_q_heads, s->num_kv_heads);
+  if (s->num_q_heads / s->num_kv_heads > 16)
+    return fail(RESKV_ERR_UNSUPPORTED, "group size Hq/Hkv = %d > 16", s->num_q_heads / s->num_kv_heads);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(RESKV_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", s->head_dim);
+  if (s->dtype != RESKV_F32 && s->dtype != RESKV_BF16)
+    return fail(RESKV_ERR_UNSUPPORTED, "dtype %d not in {F32, BF16}", s->dtype);
+  if (s->slot_cap < 1) return fail(RESKV_ERR_INVALID_ARG, "slot_cap must be >= 1 (got %d)", s->slot_cap);
+  if (s->res_cap < 1) return fail(RESKV_ERR_INVALID_ARG, "res_cap must be >= 1 (got %d)", s->res_cap);
+  const double cells = (double)s->batch * s->num_kv_heads * s->slot_cap * s->head_dim;
+  if (cells > 4.0e12) return fail(RESKV_ERR_INVALID_ARG, "cache of %.3g elements is too large", cells);
+  return RESKV_OK;
+}
+
+reskv_status_t check_gate(const reskv_gate_t* g) {
+  if (!g) return fail(RESKV_ERR_INVALID_ARG, "gate is NULL");
+  if (!(g->g_min >= 0.f && g->g_min <= 1.f)) return fail(RESKV_ERR_INVALID_ARG, "g_min %g outside [0, 1]", g->g_min);
+  if (!isfinite(g->alpha) || !isfinite(g->beta) || !isfinite(g->tau_scalar))
+    return fail(RESKV_ERR_INVALID_ARG, "gate parameters must be finite");
+  if (g->beta < 0.f) return fail(RESKV_ERR_INVALID_ARG, "beta %g must be >= 0", g->beta);
+  return RESKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* reskv_status_string(reskv_status_t st) {
+  switch (st) {
+    case RESKV_OK: return "ok";
+    case RESKV_ERR_INVALID_ARG: return "invalid argument";
+    case RESKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RESKV_ERR_WORKSPACE: return "workspace missing or too small";
+    case RESKV_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* reskv_last_error(void) { return g_last_error; }
+
+size_t reskv_decode_workspace_size(const reskv_shape_t* shape) {
+  if (check_shape(shape) != RESKV_OK) return 0;
+  return make_decode_plan(*shape).bytes;
+}
+
+reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
+                                 const void* kc, const void* vc, const float* logc,
+                                 const int32_t* res_len, const int32_t* main_len, float* out,
+                                 float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if ((st = check_gate(gate)) != RESKV_OK) return st;
+  if (!q || !kc || !vc || !logc || !res_len || !main_len || !out)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  const DecodePlan plan = make_decode_plan(*shape);
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(RESKV_ERR_WORKSPACE, "decode needs %zu workspace bytes, got %zu", plan.bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  hipError_t e = launch_decode(*shape, *gate, plan, q, kc, vc, logc, res_len, main_len, out, dbg_lse_main,
+                               dbg_lse_res, dbg_gate, workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+reskv_status_t reskv_append_kv(const reskv_shape_t* shape, const void* k_new, const void* v_new, void* kc,
+                               void* vc, const int32_t* res_len, int32_t* main_len, void* stream) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if (!k_new || !v_new || !kc || !vc || !res_len || !main_len)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  hipError_t e = launch_append(*shape, k_new, v_new, kc, vc, res_len, main_len, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "append launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+static reskv_status_t check_build(const reskv_shape_t* shape, const reskv_build_params_t* p,
+                                  const int32_t* seq_len, const int32_t* budget, const int32_t* res_count) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if (!p) return fail(RESKV_ERR_INVALID_ARG, "params is NULL");
+  if (!seq_len || !budget || !res_count) return fail(RESKV_ERR_INVALID_ARG, "a host length array is NULL");
+  if (p->max_seq_len < 1) return fail(RESKV_ERR_INVALID_ARG, "max_seq_len must be >= 1");
+  if (p->obs_window < 1 || p->obs_window > p->max_seq_len)
+    return fail(RESKV_ERR_INVALID_ARG, "obs_window %d outside [1, %d]", p->obs_window, p->max_seq_len);
+  if (p->recent_window < 0) return fail(RESKV_ERR_INVALID_ARG, "recent_window must be >= 0");
+  if (p->lloyd_iters < 1 || p->lloyd_iters > 64) return fail(RESKV_ERR_INVALID_ARG, "lloyd_iters %d outside [1, 64]", p->lloyd_iters);
+  const int Hkv = shape->num_kv_heads;
+  for (int b = 0; b < shape->batch; ++b) {
+    const int s = seq_len[b];
+    if (s < p->obs_window || s > p->max_seq_len)
+      return fail(RESKV_ERR_INVALID_ARG, "seq_len[%d] = %d outside [obs_window=%d, max_seq_len=%d]", b, s, p->obs_window, p->max_seq_len);
+    if (budget[b] < 1 || budget[b] > shape->slot_cap)
+      return fail(RESKV_ERR_INVALID_ARG, "budget[%d] = %d outside [1, slot_cap=%d]", b, budget[b], shape->slot_cap);
+    for (int h = 0; h < Hkv; ++h) {
+      const int r = res_count[b * Hkv + h];
+      if (r < 0 || r >= budget[b] || r > shape->res_cap)
+        return fail(RESKV_ERR_INVALID_ARG, "res_count[%d] = %d must satisfy 0 <= r < budget (%d) and r <= res_cap (%d)",
+                    b * Hkv + h, r, budget[b], shape->res_cap);
+    }
+  }
+  return RESKV_OK;
+}
+
+size_t reskv_build_workspace_size(const reskv_shape_t* shape, const reskv_build_params_t* params,
+                                  const int32_t* seq_len_host, const int32_t* budget_host,
+                                  const int32_t* res_count_host) {
+  if (check_build(shape, params, seq_len_host, budget_host, res_count_host) != RESKV_OK) return 0;
+  BuildPlan plan;
+  if (!make_build_plan(*shape, *params, seq_len_host, budget_host, res_count_host, &plan)) return 0;
+  return plan.bytes;
+}
+
+reskv_status_t reskv_build_cache(const reskv_shape_t* shape, const reskv_build_params_t* params, const void* k,
+                                 const void* v, const int32_t* seq_len_host, const void* q_obs,
+                                 const int32_t* budget_host, const int32_t* res_count_host, void* kc, void* vc,
+                                 float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
+                                 float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  reskv_status_t st = check_build(shape, params, seq_len_host, budget_host, res_count_host);
+  if (st != RESKV_OK) return st;
+  if (!k || !v || !q_obs || !kc || !vc || !logc || !main_idx || !res_len || !main_len)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  BuildPlan plan;
+  if (!make_build_plan(*shape, *params, seq_len_host, budget_host, res_count_host, &plan))
+    return fail(RESKV_ERR_UNSUPPORTED, "construction plan could not be formed for these sizes");
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(RESKV_ERR_WORKSPACE, "build needs %zu workspace bytes, got %zu", plan.bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  hipError_t e = launch_build(*shape, *params, plan, k, v, seq_len_host, q_obs, budget_host, res_count_host, kc,
+                              vc, logc, main_idx, res_len, main_len, dbg_scores, dbg_assign, workspace,
+                              (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "build launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

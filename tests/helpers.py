@@ -1,0 +1,92 @@
+"""Test helpers: device tensors for the ResKV C ABI and parity metrics.
+
+Nothing here computes any part of the method: caches for decode tests are
+filled with rows of synthetic keys/values and with group means (plain data
+preparation), and the expected results always come from the oracle.
+"""
+
+import numpy as np
+import torch
+
+from paper_2607_29591_amd import reskv as rk
+
+TOL = {"f32": 1e-5, "bf16": 2e-3}
+
+
+def tdtype(dtype):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def to_dev(x, dtype):
+    return torch.as_tensor(np.asarray(x, np.float32)).to(tdtype(dtype)).cuda().contiguous()
+
+
+def as_f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def rel_err_rows(got, ref):
+    """max |got - ref| / max |ref| per row (last axis), as an array."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    num = np.abs(got - ref).max(axis=-1)
+    den = np.maximum(np.abs(ref).max(axis=-1), 1e-30)
+    return num / den
+
+
+def random_cache(rng, B, Hkv, C, Rcap, d, dtype, res, main, empty_frac=0.1, key_scale=1.0):
+    """A cache with residual slots [0, r) and main slots [r, r + n).
+
+    Main rows are drawn like keys/values; residual entries are means of 1..9
+    drawn rows with their counts (some entries empty: log-count -inf).
+    Returns host float64 arrays already rounded to `dtype` storage.
+    """
+    store = (lambda x: torch.as_tensor(x, dtype=torch.float32).to(torch.bfloat16).double().numpy()) \
+        if dtype == "bf16" else (lambda x: np.asarray(x, np.float32).astype(np.float64))
+    kc = np.zeros((B, Hkv, C, d))
+    vc = np.zeros((B, Hkv, C, d))
+    logc = np.full((B, Hkv, Rcap), -np.inf)
+    bias = np.zeros(d)
+    bias[: min(4, d)] = rng.normal(0, 3, size=min(4, d))
+    for b in range(B):
+        for h in range(Hkv):
+            r, n = int(res[b][h]), int(main[b][h])
+            K = rng.normal(size=(n, d)) * key_scale + bias
+            heavy = rng.choice(n, size=max(1, n // 64), replace=False)
+            K[heavy] *= 3
+            kc[b, h, r:r + n] = store(K)
+            vc[b, h, r:r + n] = store(rng.normal(size=(n, d)))
+            for j in range(r):
+                c = int(rng.integers(1, 10))
+                if rng.random() < empty_frac:
+                    continue
+                grp = rng.normal(size=(c, d)) * key_scale + bias
+                kc[b, h, j] = store(grp.mean(0))
+                vc[b, h, j] = store(rng.normal(size=(c, d)).mean(0))
+                logc[b, h, j] = np.log(c)
+    return kc, vc, logc
+
+
+def decode_on_gpu(shape, gate_kw, q, kc, vc, logc, res_len, main_len, tau=None, dbg=True):
+    """Run reskv_decode_attn through the C ABI; returns numpy outputs."""
+    dtype = "bf16" if shape.dtype == rk.RESKV_BF16 else "f32"
+    B, Hq, d = q.shape
+    qd = to_dev(q, dtype)
+    kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
+    lcd = torch.as_tensor(np.asarray(logc, np.float32)).cuda().contiguous()
+    rl = torch.as_tensor(np.asarray(res_len, np.int32).reshape(-1)).cuda()
+    ml = torch.as_tensor(np.asarray(main_len, np.int32).reshape(-1)).cuda()
+    out = torch.full((B, Hq, d), float("nan"), dtype=torch.float32, device="cuda")
+    taud = None if tau is None else torch.as_tensor(np.asarray(tau, np.float32).reshape(-1)).cuda()
+    ws = torch.empty(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    lm = torch.empty(B * Hq, device="cuda") if dbg else None
+    lr = torch.empty(B * Hq, device="cuda") if dbg else None
+    gt = torch.empty(B * Hq, device="cuda") if dbg else None
+    gate = rk.make_gate(tau=taud, **gate_kw)
+    rk.reskv_decode_attn(shape, gate, qd, kcd, vcd, lcd, rl, ml, out, ws, lm, lr, gt)
+    torch.cuda.synchronize()
+    res = dict(out=out.double().cpu().numpy())
+    if dbg:
+        res.update(lse_main=lm.double().cpu().numpy().reshape(B, Hq), lse_res=lr.double().cpu().numpy().reshape(B, Hq),
+                   gate=gt.double().cpu().numpy().reshape(B, Hq))
+    return res

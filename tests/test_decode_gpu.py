@@ -1,0 +1,159 @@
+"""GPU parity of reskv_decode_attn / reskv_append_kv against the fp64 oracle
+(Sec. 5.4 shared-softmax decode, Sec. 5.5.2 gate, App. D Algorithm 2).
+
+Bar: per (batch, query head), max|gpu - oracle| / max|oracle| <= 1e-5 for
+fp32 caches and <= 2e-3 for bf16 caches; the gate and both log-sum-exps to
+1e-5 relative (absolute near zero).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import reskv_oracle as orc
+from paper_2607_29591_amd import reskv as rk
+from paper_2607_29591_amd import synth
+from tests.helpers import TOL, decode_on_gpu, random_cache, rel_err_rows, to_dev
+
+pytestmark = pytest.mark.gpu
+
+GATE = dict(tau_scalar=0.25, alpha=12.0, g_min=0.0, beta=1.0)
+
+
+def check(dtype, shape, q, kc, vc, logc, res, main, tau=None, gate=GATE, heads=None, tol=None):
+    got = decode_on_gpu(shape, gate, q, kc, vc, logc, res, main, tau=tau)
+    t = gate["tau_scalar"] if tau is None else tau
+    ref, lm, lr, g = orc.decode(q, kc, vc, logc, np.asarray(res), np.asarray(main), t, gate["alpha"],
+                                gate["g_min"], gate["beta"], heads=heads)
+    tol = TOL[dtype] if tol is None else tol
+    sel = (slice(None),) if heads is None else tuple(np.array(heads).T)
+    err = rel_err_rows(got["out"][sel], ref[sel])
+    assert np.isfinite(got["out"][sel]).all()
+    assert err.max() <= tol, f"max rel err {err.max():.3e} > {tol}"
+    np.testing.assert_allclose(got["gate"][sel], g[sel], rtol=1e-5, atol=1e-6)
+    np.testing.assert_allclose(got["lse_main"][sel], lm[sel], rtol=1e-5, atol=1e-5)
+    fin = np.isfinite(lr[sel])
+    assert (np.isfinite(got["lse_res"][sel]) == fin).all()
+    np.testing.assert_allclose(got["lse_res"][sel][fin], lr[sel][fin], rtol=1e-5, atol=1e-5)
+    return err.max()
+
+
+def cache_case(seed, B, Hq, Hkv, d, dtype, C, Rcap, res, main, **kw):
+    rng = np.random.default_rng(seed)
+    kc, vc, logc = random_cache(rng, B, Hkv, C, Rcap, d, dtype, res, main, **kw)
+    q = rng.normal(size=(B, Hq, d)) * 1.5
+    q = np.asarray(torch.as_tensor(q, dtype=torch.float32).to(torch.bfloat16).double()) if dtype == "bf16" else \
+        q.astype(np.float32).astype(np.float64)
+    shape = rk.make_shape(B, Hq, Hkv, d, dtype, C, Rcap)
+    return shape, q, kc, vc, logc
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("G", [1, 2, 4, 7, 8, 16])
+def test_decode_ragged_shapes(dtype, d, G):
+    """Ragged lengths (tails inside a 16-slot tile, a 64-slot wave and a
+    256-slot block), r = 0 heads, empty entries, every supported group size."""
+    Hkv = 3
+    B = 2
+    C, Rcap = 700, 300
+    res = [[0, 17, 300], [255, 1, 64]]
+    main = [[1, 399, 300], [445, 257, 636]]
+    shape, q, kc, vc, logc = cache_case(10 + G + d, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+    check(dtype, shape, q, kc, vc, logc, res, main)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_decode_gate_variants(dtype):
+    B, Hkv, G, d, C, Rcap = 2, 2, 4, 128, 600, 128
+    res = [[128, 40], [0, 100]]
+    main = [[300, 472], [600, 20]]
+    shape, q, kc, vc, logc = cache_case(3, B, Hkv * G, Hkv, d, dtype, C, Rcap, res, main)
+    rng = np.random.default_rng(0)
+    tau = rng.normal(0, 0.5, size=(B, Hkv * G)).astype(np.float32)
+    check(dtype, shape, q, kc, vc, logc, res, main, tau=tau)
+    check(dtype, shape, q, kc, vc, logc, res, main, gate=dict(tau_scalar=0.25, alpha=12.0, g_min=1.0, beta=1.0))
+    check(dtype, shape, q, kc, vc, logc, res, main, gate=dict(tau_scalar=0.9, alpha=3.0, g_min=0.2, beta=0.5))
+
+
+def test_decode_all_residual_entries_empty():
+    B, Hkv, G, d, C, Rcap = 1, 2, 4, 64, 200, 64
+    res, main = [[64, 10]], [[100, 190]]
+    shape, q, kc, vc, logc = cache_case(4, B, Hkv * G, Hkv, d, "f32", C, Rcap, res, main)
+    logc[:] = -np.inf
+    check("f32", shape, q, kc, vc, logc, res, main)
+
+
+def test_decode_large_logits():
+    """Sharp attention (scaled queries) exercises the max shifts."""
+    B, Hkv, G, d, C, Rcap = 1, 2, 4, 128, 1100, 200
+    res, main = [[200, 33]], [[900, 1000]]
+    shape, q, kc, vc, logc = cache_case(5, B, Hkv * G, Hkv, d, "bf16", C, Rcap, res, main, key_scale=3.0)
+    q = np.asarray(torch.as_tensor(q * 8, dtype=torch.float32).to(torch.bfloat16).double())
+    check("bf16", shape, q, kc, vc, logc, res, main)
+
+
+def test_decode_is_deterministic():
+    B, Hkv, G, d, C, Rcap = 2, 2, 4, 128, 900, 256
+    res, main = [[256, 0], [13, 200]], [[600, 900], [700, 3]]
+    shape, q, kc, vc, logc = cache_case(6, B, Hkv * G, Hkv, d, "bf16", C, Rcap, res, main)
+    a = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main)
+    b = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main)
+    np.testing.assert_array_equal(a["out"], b["out"])
+
+
+def test_decode_workload0_oracle_built_cache():
+    """The fp32 toy workload: cache built by the oracle, 8 decode queries."""
+    wl = synth.workload(0)
+    x = synth.gen_layer(wl, 0)
+    cache = orc.build_cache(x["K"], x["V"], x["q_obs"], x["seq_len"], x["budget"], x["res"], wl.window,
+                            wl.lloyd_iters, wl.dtype, wl.slot_cap, wl.res_cap)
+    shape = rk.make_shape(wl.batch, wl.hq, wl.hkv, wl.d, wl.dtype, wl.slot_cap, wl.res_cap)
+    for step in range(wl.steps):
+        check("f32", shape, x["q_dec"][step], cache["kc"], cache["vc"], cache["logc"], cache["res_len"],
+              cache["main_len"])
+
+
+def test_decode_batched_llama_shape_sampled():
+    """32 sequences x 8 KV heads x 2048-slot budget + appended room (the
+    batched decode workload's per-layer shape); every head decoded on the
+    GPU, a sample checked against the oracle."""
+    wl = synth.workload(2)
+    B, Hkv, G, d = wl.batch, wl.hkv, wl.group, wl.d
+    C, Rcap = wl.slot_cap, wl.res_cap
+    rng = np.random.default_rng(7)
+    res = wl.res[0]
+    main = 2048 - res + rng.integers(0, 257, size=res.shape)
+    shape, q, kc, vc, logc = cache_case(8, B, Hkv * G, Hkv, d, "bf16", C, Rcap, res, main, empty_frac=0.0)
+    tau = (rng.normal(0, 0.5, size=(B, Hkv * G))).astype(np.float32)
+    heads = [(int(b), int(h)) for b, h in zip(rng.integers(0, B, 24), rng.integers(0, Hkv * G, 24))]
+    check("bf16", shape, q, kc, vc, logc, res, main, tau=tau, heads=heads)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_append_then_decode(dtype):
+    B, Hkv, G, d, C, Rcap = 2, 2, 4, 64, 140, 32
+    res = np.array([[32, 0], [5, 31]])
+    main = np.array([[100, 137], [1, 40]])
+    shape, q, kc, vc, logc = cache_case(9, B, Hkv * G, Hkv, d, dtype, C, Rcap, res, main)
+    rng = np.random.default_rng(1)
+    kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
+    rl = torch.as_tensor(res.astype(np.int32).reshape(-1)).cuda()
+    ml = torch.as_tensor(main.astype(np.int32).reshape(-1)).cuda()
+    kc2, vc2, main2 = kc.copy(), vc.copy(), main.copy()
+    for step in range(5):
+        kn = rng.normal(size=(B, Hkv, d))
+        vn = rng.normal(size=(B, Hkv, d))
+        knd, vnd = to_dev(kn, dtype), to_dev(vn, dtype)
+        rk.reskv_append_kv(shape, knd, vnd, kcd, vcd, rl, ml)
+        for b in range(B):
+            for h in range(Hkv):
+                slot = res[b, h] + main2[b, h]
+                if slot < C:
+                    kc2[b, h, slot] = knd[b, h].double().cpu().numpy()
+                    vc2[b, h, slot] = vnd[b, h].double().cpu().numpy()
+                    main2[b, h] += 1
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ml.cpu().numpy().reshape(B, Hkv), main2)
+    np.testing.assert_array_equal(kcd.double().cpu().numpy(), kc2)
+    check(dtype, shape, q, kc2, vc2, logc, res, main2)
