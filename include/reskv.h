@@ -151,6 +151,7 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
  *   dbg_lse_res     [B*Hq] optional: log sum_j e^{<q,kbar_j>/sqrt(d) + beta logc_j}
  *   dbg_gate        [B*Hq] optional: g
  *   workspace       device scratch of reskv_decode_workspace_size() bytes
+ *                   (split-K partials); calls sharing one must not overlap.
  *
  * Lengths read on the device are clamped to the capacities, so corrupt
  * lengths cannot make the kernels read outside the cache.
@@ -168,7 +169,8 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
                                  void* workspace, size_t workspace_bytes,
                                  void* stream);
 
-/* Bytes of device workspace reskv_decode_attn needs (0 if invalid). */
+/* Bytes of device workspace reskv_decode_attn needs (0 if invalid or if
+ * the capacities need more split-K partials than one block can merge). */
 size_t reskv_decode_workspace_size(const reskv_shape_t* shape);
 
 /*

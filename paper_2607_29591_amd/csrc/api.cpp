@@ -76,7 +76,9 @@ const char* reskv_last_error(void) { return g_last_error; }
 
 size_t reskv_decode_workspace_size(const reskv_shape_t* shape) {
   if (check_shape(shape) != RESKV_OK) return 0;
-  return make_decode_plan(*shape).bytes;
+  const DecodePlan plan = make_decode_plan(*shape);
+  if ((size_t)plan.GP * plan.P * sizeof(float) > decode_max_lds_weights()) return 0;
+  return plan.bytes;
 }
 
 reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
@@ -90,6 +92,8 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t*
   if (!q || !kc || !vc || !logc || !res_len || !main_len || !out)
     return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
   const DecodePlan plan = make_decode_plan(*shape);
+  if ((size_t)plan.GP * plan.P * sizeof(float) > decode_max_lds_weights())
+    return fail(RESKV_ERR_UNSUPPORTED, "%d split-K records per head do not fit the combine", plan.P);
   if (!workspace || workspace_bytes < plan.bytes)
     return fail(RESKV_ERR_WORKSPACE, "decode needs %zu workspace bytes, got %zu", plan.bytes,
                 workspace ? workspace_bytes : (size_t)0);

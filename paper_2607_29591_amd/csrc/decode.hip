@@ -1,21 +1,26 @@
 // Shared-softmax residual decode (Sec. 5.4; Sec. 5.5.2 gate; App. D, Algorithm 2).
 //
-// Split-K flash decode over the fixed-budget cache of one layer:
+// Split-K flash decode over the fixed-budget cache of one layer, in two
+// launches:
 //   decode_split   one block = 256 slots of one (b, kv head), all of one kind
-//                  (residual slots [0, r) or main slots [r, r+n)); it writes the
-//                  block's partial (running max m, sum l, unnormalised acc) per
-//                  query head of the group. Logits are kept in base 2
-//                  (log2(e)/sqrt(d) folded into one scale).
-//   decode_combine one block per (b, kv head): merges the main partials, takes
+//                  (residual slots [0, r) or main slots [r, r+n)), one 64-slot
+//                  unit per wave; it writes the block's partial record (max
+//                  m, sum l, unnormalised acc) per query head of the group.
+//                  Logits are kept in base 2, with log2(e)/sqrt(d) folded
+//                  into one scale.
+//   decode_combine one block per (b, kv head): the main records give
 //                  p_max = 1 / l_main (the max term contributes exactly 1),
-//                  evaluates the gate, shifts the residual partials by log g and
-//                  normalises main and residual under one denominator.
+//                  the gate follows, the residual records are shifted by
+//                  log g, and main and residual share one denominator.
+// The combine is a separate launch rather than a last-arriving-block epilogue:
+// on this multi-XCD part a device-scope release/acquire per block writes back
+// and invalidates L2, which costs far more than one more launch.
 //
-// Work split inside decode_split: 4 waves x 64 slots. Q.K^T runs on MFMA
-// (16 heads x 16 slots per tile; 16x16x32 bf16 or 16x16x4 f32), each lane
-// fetching one quarter of a key row with 16-byte loads. The softmax max/sum is
-// a 16-lane butterfly; probabilities go through LDS to the P.V stage, which
-// streams value rows with 16-byte loads and accumulates in fp32 registers.
+// Per unit: Q.K^T on MFMA (16 heads x 16 slots per tile; 16x16x32 bf16 or
+// 16x16x4 f32), each lane fetching one quarter of a key row with 16-byte
+// loads; the per-head max/sum is a 16-lane butterfly; probabilities and the
+// rescale factors pass through LDS (wave-private rows) to the P.V stage, which
+// widens 16-byte value loads and accumulates in fp32 registers.
 #include "common.h"
 #include "internal.h"
 
@@ -25,11 +30,11 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kWaveSlots = 64;
-constexpr int kTiles = kWaveSlots / 16;
-static_assert(kWaves * kWaveSlots == kDecChunk, "chunk = waves x wave slots");
+constexpr int kUnit = 64;              // slots per wave unit
+constexpr int kTiles = kUnit / 16;     // MFMA tiles per unit
+constexpr int kChunk = kWaves * kUnit; // slots per split block
 
-struct SplitArgs {
+struct DecodeArgs {
   const void* q;
   const void* kc;
   const void* vc;
@@ -38,23 +43,15 @@ struct SplitArgs {
   const int32_t* main_len;
   float* part_acc;  // [B*Hkv][P][GP][D]
   float* part_ml;   // [B*Hkv][P][GP][2]  (m in base 2, l)
-  int Hq, Hkv, G, C, Rcap, PR, P;
-  float qk_scale;   // log2(e) / sqrt(d)
-  float beta_log2;  // beta * log2(e)
-};
-
-struct CombineArgs {
-  const float* part_acc;
-  const float* part_ml;
-  const int32_t* res_len;
-  const int32_t* main_len;
   const float* tau;
-  float tau_scalar, alpha, g_min;
   float* out;
   float* dbg_lse_main;
   float* dbg_lse_res;
   float* dbg_gate;
   int Hq, Hkv, G, C, Rcap, PR, P;
+  float qk_scale;   // log2(e) / sqrt(d)
+  float beta_log2;  // beta * log2(e)
+  float tau_scalar, alpha, g_min;
 };
 
 __device__ __forceinline__ void cache_lengths(const int32_t* res_len, const int32_t* main_len,
@@ -68,11 +65,12 @@ __device__ __forceinline__ void cache_lengths(const int32_t* res_len, const int3
 // slot `col`; lane group `grp` owns the contiguous quarter
 // [grp*D/4, (grp+1)*D/4) of the head dimension for both operands.
 template <typename T, int D>
-struct QKTile;
+struct QK;
 
 template <int D>
-struct QKTile<uint16_t, D> {
+struct QK<uint16_t, D> {
   static constexpr int kSteps = D / 32;  // 16x16x32 bf16 steps per quarter row
+  struct KFrag { uint4 w[kSteps]; };
   bf16x8_t q[kSteps];
   __device__ void load_q(const uint16_t* qrow, bool live) {
 #pragma unroll
@@ -81,21 +79,23 @@ struct QKTile<uint16_t, D> {
       q[i] = as_bf16x8(w);
     }
   }
-  __device__ f32x4_t run(const uint16_t* krow) const {
-    uint4 k[kSteps];
+  __device__ static void load_k(KFrag& f, const uint16_t* krow) {
 #pragma unroll
-    for (int i = 0; i < kSteps; ++i) k[i] = *reinterpret_cast<const uint4*>(krow + 8 * i);
+    for (int i = 0; i < kSteps; ++i) f.w[i] = *reinterpret_cast<const uint4*>(krow + 8 * i);
+  }
+  __device__ f32x4_t run(const KFrag& f) const {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < kSteps; ++i)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[i], as_bf16x8(k[i]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[i], as_bf16x8(f.w[i]), acc, 0, 0, 0);
     return acc;
   }
 };
 
 template <int D>
-struct QKTile<float, D> {
+struct QK<float, D> {
   static constexpr int kSteps = D / 4;  // 16x16x4 f32 steps per quarter row
+  struct KFrag { float4 w[kSteps / 4]; };
   float q[kSteps];
   __device__ void load_q(const float* qrow, bool live) {
 #pragma unroll
@@ -104,161 +104,241 @@ struct QKTile<float, D> {
       q[i] = w.x; q[i + 1] = w.y; q[i + 2] = w.z; q[i + 3] = w.w;
     }
   }
-  __device__ f32x4_t run(const float* krow) const {
-    float k[kSteps];
+  __device__ static void load_k(KFrag& f, const float* krow) {
 #pragma unroll
-    for (int i = 0; i < kSteps; i += 4) {
-      float4 w = *reinterpret_cast<const float4*>(krow + i);
-      k[i] = w.x; k[i + 1] = w.y; k[i + 2] = w.z; k[i + 3] = w.w;
-    }
+    for (int i = 0; i < kSteps / 4; ++i) f.w[i] = *reinterpret_cast<const float4*>(krow + 4 * i);
+  }
+  __device__ f32x4_t run(const KFrag& f) const {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < kSteps; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[i], k[i], acc, 0, 0, 0);
+    for (int i = 0; i < kSteps / 4; ++i) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 0], f.w[i].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 1], f.w[i].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 2], f.w[i].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 3], f.w[i].w, acc, 0, 0, 0);
+    }
     return acc;
   }
 };
 
+// 8 consecutive value-row elements, loaded raw and widened later.
+template <typename T>
+struct VRow;
+template <>
+struct VRow<uint16_t> {
+  uint4 w;
+  __device__ void load(const uint16_t* p) { w = *reinterpret_cast<const uint4*>(p); }
+  __device__ void widen(float (&x)[8]) const {
+    x[0] = bf16_lo(w.x); x[1] = bf16_hi(w.x); x[2] = bf16_lo(w.y); x[3] = bf16_hi(w.y);
+    x[4] = bf16_lo(w.z); x[5] = bf16_hi(w.z); x[6] = bf16_lo(w.w); x[7] = bf16_hi(w.w);
+  }
+};
+template <>
+struct VRow<float> {
+  float4 a, b;
+  __device__ void load(const float* p) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ void widen(float (&x)[8]) const {
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  }
+};
+
+
+// Raw loads of one 64-slot unit for one lane.
+template <typename T, int D>
+struct UnitRegs {
+  static constexpr int CPR = D / 8;         // 8-column chunks per value row
+  static constexpr int RP = 64 / CPR;       // rows covered by one wave-wide load
+  static constexpr int NR = kUnit / RP;     // value rows per lane
+  typename QK<T, D>::KFrag k[kTiles];
+  VRow<T> v[NR];
+  float lc[kTiles];
+};
+
+// Issue every load of unit [s0, s0 + nvalid); rows past the tail are clamped
+// to the unit's first row (their probabilities are zero).
+template <typename T, int D>
+__device__ __forceinline__ void load_unit(UnitRegs<T, D>& u, const T* kc, const T* vc, const float* logc,
+                                          bool is_res, int s0, int nvalid, int col, int grp, int c, int ph) {
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t) {
+    const int row = (16 * t + col < nvalid) ? s0 + 16 * t + col : s0;
+    QK<T, D>::load_k(u.k[t], kc + (size_t)row * D + grp * (D / 4));
+  }
+#pragma unroll
+  for (int k = 0; k < UnitRegs<T, D>::NR; ++k) {
+    const int j = ph + UnitRegs<T, D>::RP * k;
+    u.v[k].load(vc + (size_t)(s0 + min(j, nvalid - 1)) * D + 8 * c);
+  }
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t)
+    u.lc[t] = (is_res && 16 * t + col < nvalid) ? logc[s0 + 16 * t + col] : 0.f;
+}
+
+// Online-softmax state of one wave for one kind.
+template <int GP>
+struct WaveState {
+  float m[4], l[4];   // per head 4*grp + i (replicated over the 16 lanes of a group)
+  float acc[GP][8];   // per head, 8 columns of this lane's chunk, this lane's row phase
+  __device__ void reset() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { m[i] = kNegInf; l[i] = 0.f; }
+#pragma unroll
+    for (int h = 0; h < GP; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+  }
+};
+
 template <typename T, int D, int GP>
-__global__ __launch_bounds__(kThreads) void decode_split(SplitArgs a) {
+__device__ __forceinline__ void process_unit(const UnitRegs<T, D>& u, const QK<T, D>& qk, WaveState<GP>& st,
+                                             float (*s_p)[GP], float* s_alpha, bool is_res, int nvalid,
+                                             float qk_scale, float beta_log2, int col, int grp, int c, int ph) {
+  f32x4_t s[kTiles];
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t) s[t] = qk.run(u.k[t]);
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t) {
+    const bool live = 16 * t + col < nvalid;
+    const bool dead = !live || (is_res && u.lc[t] == kNegInf);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = s[t][i] * qk_scale;
+      if (is_res) v += beta_log2 * u.lc[t];
+      s[t][i] = dead ? kNegInf : v;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float m = s[0][i];
+#pragma unroll
+    for (int t = 1; t < kTiles; ++t) m = fmaxf(m, s[t][i]);
+    m = wave_xor_max(m, 1); m = wave_xor_max(m, 2);
+    m = wave_xor_max(m, 4); m = wave_xor_max(m, 8);
+    const float m_new = fmaxf(st.m[i], m);
+    const float mu = (m_new == kNegInf) ? 0.f : m_new;
+    const float alpha = exp2f(st.m[i] - mu);
+    float l = 0.f;
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t) {
+      const float e = exp2f(s[t][i] - mu);
+      s[t][i] = e;
+      l += e;
+    }
+    l = wave_xor_add(l, 1); l = wave_xor_add(l, 2);
+    l = wave_xor_add(l, 4); l = wave_xor_add(l, 8);
+    st.l[i] = fmaf(st.l[i], alpha, l);
+    st.m[i] = m_new;
+    const int h = 4 * grp + i;
+    if (h < GP && col == 0) s_alpha[h] = alpha;
+  }
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * grp + i;
+      if (h < GP) s_p[16 * t + col][h] = s[t][i];
+    }
+  // LDS traffic of one wave executes in order; this keeps the compiler from
+  // moving the reads below above the writes
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  float al[GP];
+#pragma unroll
+  for (int h = 0; h < GP; ++h) al[h] = s_alpha[h];
+#pragma unroll
+  for (int h = 0; h < GP; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) st.acc[h][e] *= al[h];
+#pragma unroll
+  for (int k = 0; k < UnitRegs<T, D>::NR; ++k) {
+    const int j = ph + UnitRegs<T, D>::RP * k;
+    float v[8];
+    u.v[k].widen(v);
+    float pr[GP];
+#pragma unroll
+    for (int h = 0; h < GP; ++h) pr[h] = s_p[j][h];
+#pragma unroll
+    for (int h = 0; h < GP; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) st.acc[h][e] = fmaf(pr[h], v[e], st.acc[h][e]);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
+  using Regs = UnitRegs<T, D>;
   const int p = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  // block p < PR covers residual slots [256p, 256p + 256) of [0, r); block
+  // p >= PR covers main slots [r + 256(p-PR), ...) of [r, r + n)
   const bool is_res = p < a.PR;
-  int lo, hi;
-  if (is_res) {
-    lo = p * kDecChunk;
-    hi = min(lo + kDecChunk, r);
-  } else {
-    lo = r + (p - a.PR) * kDecChunk;
-    hi = min(lo + kDecChunk, r + n);
-  }
-  if (lo >= hi) return;  // block-uniform
+  const int base = is_res ? 0 : r;
+  const int end = is_res ? r : r + n;
+  const int lo = base + (is_res ? p : p - a.PR) * kChunk;
+  if (lo >= end) return;  // block-uniform
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int w_lo = lo + wave * kWaveSlots;
-  const int nvalid = min(w_lo + kWaveSlots, hi) - w_lo;  // wave-uniform, may be <= 0
+  const int c = lane % Regs::CPR, ph = lane / Regs::CPR;
 
-  __shared__ float s_p[kWaves][kWaveSlots][GP];
+  __shared__ float s_p[kWaves][kUnit][GP];
+  __shared__ float s_alpha[kWaves][GP];
   __shared__ float s_acc[kWaves][GP][D];
   __shared__ float s_m[kWaves][GP];
   __shared__ float s_l[kWaves][GP];
 
   const T* kc = static_cast<const T*>(a.kc) + (size_t)bh * a.C * D;
   const T* vc = static_cast<const T*>(a.vc) + (size_t)bh * a.C * D;
+  const float* logc = a.logc + (size_t)bh * a.Rcap;
 
-  float mrow[4], lrow[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { mrow[i] = kNegInf; lrow[i] = 0.f; }
-
-  if (nvalid > 0) {
-    QKTile<T, D> qk;
-    const T* qrow = static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + col) * D + grp * (D / 4);
-    qk.load_q(qrow, col < a.G);
-
-    f32x4_t s[kTiles];
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t) {
-      const int slot = w_lo + 16 * t + col;
-      const int row = (16 * t + col < nvalid) ? slot : w_lo;
-      s[t] = qk.run(kc + (size_t)row * D + grp * (D / 4));
-    }
-    // scale to base-2 logits, add beta*log c for residual entries, mask the tail
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t) {
-      const bool live = 16 * t + col < nvalid;
-      float lc = 0.f;
-      if (is_res && live) lc = a.logc[(size_t)bh * a.Rcap + w_lo + 16 * t + col];
-      const bool dead = !live || (is_res && lc == kNegInf);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v = s[t][i] * a.qk_scale;
-        if (is_res) v += a.beta_log2 * lc;
-        s[t][i] = dead ? kNegInf : v;
-      }
-    }
-    // per-head max and sum over the wave's slots (16-lane butterflies)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float m = s[0][i];
-#pragma unroll
-      for (int t = 1; t < kTiles; ++t) m = fmaxf(m, s[t][i]);
-      m = wave_xor_max(m, 1); m = wave_xor_max(m, 2);
-      m = wave_xor_max(m, 4); m = wave_xor_max(m, 8);
-      mrow[i] = m;
-      const float mu = (m == kNegInf) ? 0.f : m;
-      float l = 0.f;
-#pragma unroll
-      for (int t = 0; t < kTiles; ++t) {
-        const float e = exp2f(s[t][i] - mu);
-        s[t][i] = e;
-        l += e;
-      }
-      l = wave_xor_add(l, 1); l = wave_xor_add(l, 2);
-      l = wave_xor_add(l, 4); l = wave_xor_add(l, 8);
-      lrow[i] = l;
-    }
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int h = 4 * grp + i;
-        if (h < GP) s_p[wave][16 * t + col][h] = s[t][i];
-      }
-    }
+  WaveState<GP> st;
+  st.reset();
+  const int s0 = lo + wave * kUnit;
+  if (s0 < end) {  // wave-uniform
+    QK<T, D> qk;
+    qk.load_q(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + col) * D + grp * (D / 4),
+              col < a.G);
+    Regs u;
+    const int nvalid = min(kUnit, end - s0);
+    load_unit<T, D>(u, kc, vc, logc, is_res, s0, nvalid, col, grp, c, ph);
+    process_unit<T, D, GP>(u, qk, st, s_p[wave], s_alpha[wave], is_res, nvalid, a.qk_scale, a.beta_log2, col,
+                           grp, c, ph);
   }
-  __syncthreads();
-
-  // P.V: lane = (chunk c of 8 columns, row phase ph)
-  constexpr int CPR = D / 8;
-  constexpr int RP = 64 / CPR;
-  const int c = lane % CPR, ph = lane / CPR;
-  float acc[GP][8];
+  // wave state -> LDS: sum the row phases of acc, keep max and sum per head
 #pragma unroll
-  for (int h = 0; h < GP; ++h)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-  if (nvalid > 0) {
-    const T* vbase = vc + (size_t)w_lo * D + 8 * c;
-    for (int j = ph; j < nvalid; j += RP) {
-      float v[8];
-      load8_f32(vbase + (size_t)j * D, v);
-      float pr[GP];
-#pragma unroll
-      for (int h = 0; h < GP; ++h) pr[h] = s_p[wave][j][h];
-#pragma unroll
-      for (int h = 0; h < GP; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr[h], v[e], acc[h][e]);
-    }
-  }
-#pragma unroll
-  for (int msk = CPR; msk < 64; msk <<= 1)
+  for (int msk = Regs::CPR; msk < 64; msk <<= 1)
 #pragma unroll
     for (int h = 0; h < GP; ++h)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = wave_xor_add(acc[h][e], msk);
+      for (int e = 0; e < 8; ++e) st.acc[h][e] = wave_xor_add(st.acc[h][e], msk);
   if (ph == 0) {
 #pragma unroll
     for (int h = 0; h < GP; ++h)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s_acc[wave][h][8 * c + e] = acc[h][e];
+      for (int e = 0; e < 8; ++e) s_acc[wave][h][8 * c + e] = st.acc[h][e];
   }
   if (col == 0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int h = 4 * grp + i;
       if (h < GP) {
-        s_m[wave][h] = nvalid > 0 ? mrow[i] : kNegInf;
-        s_l[wave][h] = nvalid > 0 ? lrow[i] : 0.f;
+        s_m[wave][h] = st.m[i];
+        s_l[wave][h] = st.l[i];
       }
     }
   }
   __syncthreads();
-
-  // merge the 4 waves into the block's partial
-  const size_t pbase = ((size_t)bh * a.P + p) * GP;
+  // merge the 4 waves into this block's record
+  const size_t rec = ((size_t)bh * a.P + p) * GP;
   for (int idx = tid; idx < GP * D; idx += kThreads) {
     const int h = idx / D, d = idx % D;
     float M = s_m[0][h];
@@ -273,44 +353,46 @@ __global__ __launch_bounds__(kThreads) void decode_split(SplitArgs a) {
         l = fmaf(f, s_l[w][h], l);
       }
     }
-    a.part_acc[(pbase + h) * D + d] = o;
+    a.part_acc[(rec + h) * D + d] = o;
     if (d == 0) {
-      a.part_ml[(pbase + h) * 2 + 0] = M;
-      a.part_ml[(pbase + h) * 2 + 1] = l;
+      a.part_ml[(rec + h) * 2 + 0] = M;
+      a.part_ml[(rec + h) * 2 + 1] = l;
     }
   }
 }
 
+// Merge the records of one (b, kv head), evaluate the gate and write the G
+// outputs. Record p < PR is residual chunk p, record PR + q is main chunk q;
+// only chunks that hold slots were written.
 template <int D, int GP>
-__global__ __launch_bounds__(kThreads) void decode_combine(CombineArgs a) {
+__global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
+  extern __shared__ float s_w[];  // [GP][P] weights of the records
   const int kvh = blockIdx.x, b = blockIdx.y;
   const int bh = b * a.Hkv + kvh;
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
-  const int nRC = (r + kDecChunk - 1) / kDecChunk;
-  const int nMC = (n + kDecChunk - 1) / kDecChunk;
+  const int nRC = (r + kChunk - 1) / kChunk, nMC = (n + kChunk - 1) / kChunk;
   const float* ml = a.part_ml + (size_t)bh * a.P * GP * 2;
   const float* pacc = a.part_acc + (size_t)bh * a.P * GP * D;
-
-  __shared__ float s_mx[GP], s_lg2g[GP], s_inv[GP];
-  const int tid = threadIdx.x;
-  if (tid < a.G) {
-    const int h = tid;
+  const int tid = threadIdx.x, lane16 = tid & 15, h = tid >> 4;
+  if (h < a.G) {
     float mM = kNegInf, mR = kNegInf;
-    for (int q = 0; q < nMC; ++q) mM = fmaxf(mM, ml[((a.PR + q) * GP + h) * 2]);
-    for (int q = 0; q < nRC; ++q) mR = fmaxf(mR, ml[(q * GP + h) * 2]);
+    for (int q = lane16; q < nMC; q += 16) mM = fmaxf(mM, ml[((a.PR + q) * GP + h) * 2]);
+    for (int q = lane16; q < nRC; q += 16) mR = fmaxf(mR, ml[(q * GP + h) * 2]);
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) { mM = wave_xor_max(mM, msk); mR = wave_xor_max(mR, msk); }
     float lM = 0.f, lR = 0.f;
-    if (mM != kNegInf)
-      for (int q = 0; q < nMC; ++q) {
-        const float* e = ml + ((a.PR + q) * GP + h) * 2;
-        lM = fmaf(e[1], exp2f(e[0] - mM), lM);
-      }
-    if (mR != kNegInf)
-      for (int q = 0; q < nRC; ++q) {
-        const float* e = ml + (q * GP + h) * 2;
-        lR = fmaf(e[1], exp2f(e[0] - mR), lR);
-      }
-    // p_max = max_p e^{a_p} / sum_p e^{a_p} = 1 / lM (the max term is exactly 1)
+    for (int q = lane16; q < nMC; q += 16) {
+      const float* e = ml + ((a.PR + q) * GP + h) * 2;
+      if (e[0] != kNegInf) lM = fmaf(e[1], exp2f(e[0] - mM), lM);
+    }
+    for (int q = lane16; q < nRC; q += 16) {
+      const float* e = ml + (q * GP + h) * 2;
+      if (e[0] != kNegInf) lR = fmaf(e[1], exp2f(e[0] - mR), lR);
+    }
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) { lM = wave_xor_add(lM, msk); lR = wave_xor_add(lR, msk); }
+    // p_max = max_p e^{a_p} / sum_p e^{a_p} = 1 / lM: the max term is exactly 1
     const float pmax = lM > 0.f ? 1.f / lM : 1.f;
     const int qh = b * a.Hq + kvh * a.G + h;
     const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
@@ -321,29 +403,39 @@ __global__ __launch_bounds__(kThreads) void decode_combine(CombineArgs a) {
     float den = 0.f;
     if (mM != kNegInf) den += lM * exp2f(mM - Mx);
     if (mRg != kNegInf) den += lR * exp2f(mRg - Mx);
-    s_mx[h] = Mx;
-    s_lg2g[h] = lg2g;
-    s_inv[h] = den > 0.f ? 1.f / den : 0.f;
-    if (a.dbg_lse_main) a.dbg_lse_main[qh] = lM > 0.f ? (mM + log2f(lM)) * kLn2 : kNegInf;
-    if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
-    if (a.dbg_gate) a.dbg_gate[qh] = g;
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    for (int q = lane16; q < nMC; q += 16) {
+      const float m = ml[((a.PR + q) * GP + h) * 2];
+      s_w[h * a.P + a.PR + q] = m != kNegInf ? exp2f(m - Mx) * inv : 0.f;
+    }
+    for (int q = lane16; q < nRC; q += 16) {
+      const float m = ml[(q * GP + h) * 2];
+      s_w[h * a.P + q] = (m != kNegInf && mRg != kNegInf) ? exp2f(m + lg2g - Mx) * inv : 0.f;
+    }
+    if (lane16 == 0) {
+      if (a.dbg_lse_main) a.dbg_lse_main[qh] = lM > 0.f ? (mM + log2f(lM)) * kLn2 : kNegInf;
+      if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
+      if (a.dbg_gate) a.dbg_gate[qh] = g;
+    }
   }
   __syncthreads();
   for (int idx = tid; idx < a.G * D; idx += kThreads) {
-    const int h = idx / D, d = idx % D;
-    const float Mx = s_mx[h], lg2g = s_lg2g[h];
-    float o = 0.f;
-    for (int q = 0; q < nMC; ++q) {
-      const int pp = a.PR + q;
-      const float m = ml[(pp * GP + h) * 2];
-      if (m != kNegInf) o = fmaf(exp2f(m - Mx), pacc[(pp * GP + h) * D + d], o);
+    const int hh = idx / D, d = idx % D;
+    const float* w = s_w + hh * a.P;
+    float o0 = 0.f, o1 = 0.f;
+    int q = 0;
+    for (; q + 1 < nRC; q += 2) {
+      o0 = fmaf(w[q], pacc[(q * GP + hh) * D + d], o0);
+      o1 = fmaf(w[q + 1], pacc[((q + 1) * GP + hh) * D + d], o1);
     }
-    if (lg2g != kNegInf)
-      for (int q = 0; q < nRC; ++q) {
-        const float m = ml[(q * GP + h) * 2];
-        if (m != kNegInf) o = fmaf(exp2f(m + lg2g - Mx), pacc[(q * GP + h) * D + d], o);
-      }
-    a.out[((size_t)b * a.Hq + kvh * a.G + h) * D + d] = o * s_inv[h];
+    if (q < nRC) o0 = fmaf(w[q], pacc[(q * GP + hh) * D + d], o0);
+    for (q = 0; q + 1 < nMC; q += 2) {
+      const int pp = a.PR + q;
+      o0 = fmaf(w[pp], pacc[(pp * GP + hh) * D + d], o0);
+      o1 = fmaf(w[pp + 1], pacc[((pp + 1) * GP + hh) * D + d], o1);
+    }
+    if (q < nMC) o0 = fmaf(w[a.PR + q], pacc[((a.PR + q) * GP + hh) * D + d], o0);
+    a.out[((size_t)b * a.Hq + kvh * a.G + hh) * D + d] = o0 + o1;
   }
 }
 
@@ -365,26 +457,23 @@ __global__ void append_kernel(const T* k_new, const T* v_new, T* kc, T* vc, cons
 }
 
 template <typename T, int D, int GP>
-hipError_t launch_typed(const DecodePlan& pl, const SplitArgs& sa, const CombineArgs& ca,
-                        hipStream_t stream) {
-  dim3 g1(pl.P, pl.Hkv, pl.B);
-  hipLaunchKernelGGL((decode_split<T, D, GP>), g1, dim3(kThreads), 0, stream, sa);
+hipError_t launch_typed(const DecodePlan& pl, const DecodeArgs& da, hipStream_t stream) {
+  hipLaunchKernelGGL((decode_split<T, D, GP>), dim3(pl.P, pl.Hkv, pl.B), dim3(kThreads), 0, stream, da);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 g2(pl.Hkv, pl.B);
-  hipLaunchKernelGGL((decode_combine<D, GP>), g2, dim3(kThreads), 0, stream, ca);
+  const size_t lds = (size_t)GP * pl.P * sizeof(float);
+  hipLaunchKernelGGL((decode_combine<D, GP>), dim3(pl.Hkv, pl.B), dim3(kThreads), lds, stream, da);
   return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t launch_gp(const DecodePlan& pl, const SplitArgs& sa, const CombineArgs& ca,
-                     hipStream_t stream) {
+hipError_t launch_gp(const DecodePlan& pl, const DecodeArgs& da, hipStream_t stream) {
   switch (pl.GP) {
-    case 1: return launch_typed<T, D, 1>(pl, sa, ca, stream);
-    case 2: return launch_typed<T, D, 2>(pl, sa, ca, stream);
-    case 4: return launch_typed<T, D, 4>(pl, sa, ca, stream);
-    case 8: return launch_typed<T, D, 8>(pl, sa, ca, stream);
-    case 16: return launch_typed<T, D, 16>(pl, sa, ca, stream);
+    case 1: return launch_typed<T, D, 1>(pl, da, stream);
+    case 2: return launch_typed<T, D, 2>(pl, da, stream);
+    case 4: return launch_typed<T, D, 4>(pl, da, stream);
+    case 8: return launch_typed<T, D, 8>(pl, da, stream);
+    case 16: return launch_typed<T, D, 16>(pl, da, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -398,15 +487,16 @@ DecodePlan make_decode_plan(const reskv_shape_t& s) {
   p.GP = p.G <= 1 ? 1 : p.G <= 2 ? 2 : p.G <= 4 ? 4 : p.G <= 8 ? 8 : 16;
   p.D = s.head_dim; p.C = s.slot_cap; p.Rcap = s.res_cap;
   const int rmax = s.res_cap < s.slot_cap ? s.res_cap : s.slot_cap;
-  p.PR = (rmax + kDecChunk - 1) / kDecChunk;
-  p.PM = (s.slot_cap + kDecChunk - 1) / kDecChunk;
-  p.P = p.PR + p.PM;
-  const size_t units = (size_t)p.B * p.Hkv * p.P * p.GP;
+  p.PR = (rmax + kChunk - 1) / kChunk;
+  p.P = p.PR + (s.slot_cap + kChunk - 1) / kChunk;
+  const size_t recs = (size_t)p.B * p.Hkv * p.P * p.GP;
   p.acc_off = 0;
-  p.ml_off = align_up(units * p.D * sizeof(float), 256);
-  p.bytes = p.ml_off + align_up(units * 2 * sizeof(float), 256);
+  p.ml_off = align_up(recs * p.D * sizeof(float), 256);
+  p.bytes = p.ml_off + align_up(recs * 2 * sizeof(float), 256);
   return p;
 }
+
+size_t decode_max_lds_weights() { return 48 * 1024; }
 
 hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& pl,
                          const void* q, const void* kc, const void* vc, const float* logc,
@@ -414,25 +504,20 @@ hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const De
                          float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
                          void* workspace, hipStream_t stream) {
   char* ws = static_cast<char*>(workspace);
-  SplitArgs sa{};
-  sa.q = q; sa.kc = kc; sa.vc = vc; sa.logc = logc;
-  sa.res_len = res_len; sa.main_len = main_len;
-  sa.part_acc = reinterpret_cast<float*>(ws + pl.acc_off);
-  sa.part_ml = reinterpret_cast<float*>(ws + pl.ml_off);
-  sa.Hq = pl.Hq; sa.Hkv = pl.Hkv; sa.G = pl.G; sa.C = pl.C; sa.Rcap = pl.Rcap;
-  sa.PR = pl.PR; sa.P = pl.P;
-  sa.qk_scale = kLog2e / sqrtf((float)pl.D);
-  sa.beta_log2 = g.beta * kLog2e;
-  CombineArgs ca{};
-  ca.part_acc = sa.part_acc; ca.part_ml = sa.part_ml;
-  ca.res_len = res_len; ca.main_len = main_len;
-  ca.tau = g.tau; ca.tau_scalar = g.tau_scalar; ca.alpha = g.alpha; ca.g_min = g.g_min;
-  ca.out = out; ca.dbg_lse_main = dbg_lse_main; ca.dbg_lse_res = dbg_lse_res; ca.dbg_gate = dbg_gate;
-  ca.Hq = pl.Hq; ca.Hkv = pl.Hkv; ca.G = pl.G; ca.C = pl.C; ca.Rcap = pl.Rcap;
-  ca.PR = pl.PR; ca.P = pl.P;
+  DecodeArgs da{};
+  da.q = q; da.kc = kc; da.vc = vc; da.logc = logc;
+  da.res_len = res_len; da.main_len = main_len;
+  da.part_acc = reinterpret_cast<float*>(ws + pl.acc_off);
+  da.part_ml = reinterpret_cast<float*>(ws + pl.ml_off);
+  da.tau = g.tau; da.out = out;
+  da.dbg_lse_main = dbg_lse_main; da.dbg_lse_res = dbg_lse_res; da.dbg_gate = dbg_gate;
+  da.Hq = pl.Hq; da.Hkv = pl.Hkv; da.G = pl.G; da.C = pl.C; da.Rcap = pl.Rcap; da.PR = pl.PR; da.P = pl.P;
+  da.qk_scale = kLog2e / sqrtf((float)pl.D);
+  da.beta_log2 = g.beta * kLog2e;
+  da.tau_scalar = g.tau_scalar; da.alpha = g.alpha; da.g_min = g.g_min;
   const bool bf = s.dtype == RESKV_BF16;
-  if (pl.D == 128) return bf ? launch_gp<uint16_t, 128>(pl, sa, ca, stream) : launch_gp<float, 128>(pl, sa, ca, stream);
-  if (pl.D == 64) return bf ? launch_gp<uint16_t, 64>(pl, sa, ca, stream) : launch_gp<float, 64>(pl, sa, ca, stream);
+  if (pl.D == 128) return bf ? launch_gp<uint16_t, 128>(pl, da, stream) : launch_gp<float, 128>(pl, da, stream);
+  if (pl.D == 64) return bf ? launch_gp<uint16_t, 64>(pl, da, stream) : launch_gp<float, 64>(pl, da, stream);
   return hipErrorInvalidValue;
 }
 

@@ -9,14 +9,14 @@
 
 namespace reskv {
 
-// Decode: slots per split-K work unit (one block of 4 waves x 64 slots).
-constexpr int kDecChunk = 256;
-
 struct DecodePlan {
   int B, Hq, Hkv, G, GP, D, C, Rcap;
-  int PR, PM, P;  // residual chunks, main chunks, total chunks per (b, kv head)
+  int PR, P;  // residual blocks and all blocks of the split grid per (b, kv head)
   size_t acc_off, ml_off, bytes;
 };
+
+// Largest dynamic LDS the combine kernel may use for its weights.
+size_t decode_max_lds_weights();
 
 DecodePlan make_decode_plan(const reskv_shape_t& s);
 

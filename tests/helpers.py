@@ -67,7 +67,7 @@ def random_cache(rng, B, Hkv, C, Rcap, d, dtype, res, main, empty_frac=0.1, key_
     return kc, vc, logc
 
 
-def decode_on_gpu(shape, gate_kw, q, kc, vc, logc, res_len, main_len, tau=None, dbg=True):
+def decode_on_gpu(shape, gate_kw, q, kc, vc, logc, res_len, main_len, tau=None, dbg=True, ws=None):
     """Run reskv_decode_attn through the C ABI; returns numpy outputs."""
     dtype = "bf16" if shape.dtype == rk.RESKV_BF16 else "f32"
     B, Hq, d = q.shape
@@ -78,7 +78,8 @@ def decode_on_gpu(shape, gate_kw, q, kc, vc, logc, res_len, main_len, tau=None, 
     ml = torch.as_tensor(np.asarray(main_len, np.int32).reshape(-1)).cuda()
     out = torch.full((B, Hq, d), float("nan"), dtype=torch.float32, device="cuda")
     taud = None if tau is None else torch.as_tensor(np.asarray(tau, np.float32).reshape(-1)).cuda()
-    ws = torch.empty(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    if ws is None:
+        ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
     lm = torch.empty(B * Hq, device="cuda") if dbg else None
     lr = torch.empty(B * Hq, device="cuda") if dbg else None
     gt = torch.empty(B * Hq, device="cuda") if dbg else None

@@ -93,13 +93,22 @@ def test_decode_large_logits():
     check("bf16", shape, q, kc, vc, logc, res, main)
 
 
-def test_decode_is_deterministic():
+def test_decode_is_deterministic_and_workspace_reusable():
+    """Bitwise-equal reruns; one workspace serves calls with different
+    lengths."""
     B, Hkv, G, d, C, Rcap = 2, 2, 4, 128, 900, 256
     res, main = [[256, 0], [13, 200]], [[600, 900], [700, 3]]
     shape, q, kc, vc, logc = cache_case(6, B, Hkv * G, Hkv, d, "bf16", C, Rcap, res, main)
-    a = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main)
-    b = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main)
+    ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    a = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main, ws=ws)
+    b = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main, ws=ws)
     np.testing.assert_array_equal(a["out"], b["out"])
+    main2 = [[100, 300], [1, 3]]
+    c = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main2, ws=ws)
+    ref, *_ = orc.decode(q, kc, vc, logc, np.asarray(res), np.asarray(main2), 0.25, 12.0, 0.0, 1.0)
+    assert rel_err_rows(c["out"], ref).max() <= TOL["bf16"]
+    d2 = decode_on_gpu(shape, GATE, q, kc, vc, logc, res, main, ws=ws)
+    np.testing.assert_array_equal(a["out"], d2["out"])
 
 
 def test_decode_workload0_oracle_built_cache():
