@@ -125,6 +125,10 @@ static reskv_status_t check_build(const reskv_shape_t* shape, const reskv_build_
     return fail(RESKV_ERR_INVALID_ARG, "obs_window %d outside [1, %d]", p->obs_window, p->max_seq_len);
   if (p->recent_window < 0) return fail(RESKV_ERR_INVALID_ARG, "recent_window must be >= 0");
   if (p->lloyd_iters < 1 || p->lloyd_iters > 64) return fail(RESKV_ERR_INVALID_ARG, "lloyd_iters %d outside [1, 64]", p->lloyd_iters);
+  if ((long long)p->obs_window * (shape->num_q_heads / shape->num_kv_heads) > 1024)
+    return fail(RESKV_ERR_UNSUPPORTED, "observation rows per KV head (G*w = %d) above 1024",
+                p->obs_window * (shape->num_q_heads / shape->num_kv_heads));
+  if (shape->res_cap > 4096) return fail(RESKV_ERR_UNSUPPORTED, "res_cap %d above 4096", shape->res_cap);
   const int Hkv = shape->num_kv_heads;
   for (int b = 0; b < shape->batch; ++b) {
     const int s = seq_len[b];
@@ -137,6 +141,10 @@ static reskv_status_t check_build(const reskv_shape_t* shape, const reskv_build_
       if (r < 0 || r >= budget[b] || r > shape->res_cap)
         return fail(RESKV_ERR_INVALID_ARG, "res_count[%d] = %d must satisfy 0 <= r < budget (%d) and r <= res_cap (%d)",
                     b * Hkv + h, r, budget[b], shape->res_cap);
+      const int m = budget[b] - r;
+      const int main_len = s <= m ? s : m;
+      if (r + main_len > shape->slot_cap)
+        return fail(RESKV_ERR_INVALID_ARG, "r + main slots (%d) exceed slot_cap (%d)", r + main_len, shape->slot_cap);
     }
   }
   return RESKV_OK;

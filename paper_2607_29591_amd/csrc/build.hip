@@ -1,18 +1,866 @@
-// Construction kernels (placeholder until the construction pass lands).
+// Construction of the main + residual cache of one layer (App. D, Algorithm 1
+// with the residual count r given per (b, kv head)).
+//
+// Per (b, kv head), in launch order:
+//   lse_partial    MFMA logits of the G*w observation-window rows against a
+//                  256-key chunk; per row the max and sum of exp (base 2) over
+//                  the keys it can see (causal inside the window)
+//   lse_final      merges the chunk partials into one log-sum-exp per row
+//   score_accum    recomputes the logits; raw[p] = sum over rows of the
+//                  normalised weight of key p, for the scored positions
+//   pool5          5-tap zero-padded sum over the scored positions
+//   select         radix select (4 x 8-bit digits of the fp32 bit pattern) of
+//                  the k_top-th and (k_top + r')-th largest score; ties at a
+//                  threshold go to the lower position. Stable compaction writes
+//                  main_idx (top-k, then the protected window), the evicted
+//                  list E and the Lloyd seeds, all ascending
+//   gather_init    copies the main rows into slots [r, r + m), clears the
+//                  residual slots, seeds the Lloyd centres with K[seed]
+//   center_prep    splits each centre into bf16 hi + lo and its squared norm
+//   T x { lloyd_assign   MFMA distances ||mu||^2 - 2 k.mu with mu = hi + lo,
+//                        argmin with ties to the lower centre, and per-block
+//                        group histograms
+//         lloyd_offsets  group starts and per-block offsets (counting sort)
+//         lloyd_scatter  stable placement of E by group
+//         lloyd_update   fp64 sums of the members in fixed order -> new
+//                        centres; in the last round also the mean values,
+//                        counts and log-counts written to the cache }
+// Scores follow the SnapKV rule (App. B.2.2), selection the main-selection
+// equation (Sec. 5.2), the partition objective and summaries Sec. 5.3 and
+// App. B.3.
+#include <math.h>
+
+#include <vector>
+
 #include "common.h"
 #include "internal.h"
 
 namespace reskv {
 
-bool make_build_plan(const reskv_shape_t&, const reskv_build_params_t&, const int32_t*, const int32_t*,
-                     const int32_t*, BuildPlan*) {
-  return false;
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kKeyChunk = 256;     // keys per scoring block (16 MFMA tiles)
+constexpr int kKeyTiles = kKeyChunk / 16;
+constexpr int kTokBlock = 256;     // evicted tokens per Lloyd block
+constexpr int kCenterChunk = 64;   // centres staged in LDS per step
+constexpr int kSelThreads = 1024;
+
+struct BuildArgs {
+  const void* k;
+  const void* v;
+  const void* q_obs;
+  void* kc;
+  void* vc;
+  float* logc;
+  int32_t* main_idx;
+  int32_t* res_len;
+  int32_t* main_len;
+  float* dbg_scores;
+  int32_t* dbg_assign;
+  const HeadMeta* meta;
+  float2* lse_part;    // [BH][NCH][R] (max, sum) in base 2
+  float* lse2;         // [BH][R]
+  float* raw;          // [BH][S]
+  float* score;        // [BH][S]
+  int32_t* elist;      // [BH][S]   evicted positions, ascending
+  int32_t* seeds;      // [BH][Rcap]
+  float* cent;         // [BH][Rcap][D]
+  uint16_t* cent_hi;   // [BH][Rcap][D]
+  uint16_t* cent_lo;   // [BH][Rcap][D]
+  float* cnorm;        // [BH][Rcap]
+  int32_t* assign;     // [BH][S]   group of evicted token i
+  int32_t* hist;       // [BH][NBLK][Rcap] block histograms -> block offsets
+  int32_t* cstart;     // [BH][Rcap]
+  int32_t* ccount;     // [BH][Rcap]
+  int32_t* order;      // [BH][S]   evicted positions grouped by centre
+  int B, Hq, Hkv, G, C, Rcap, S, w, R, NCH, NBLK, T;
+  float scale2;        // log2(e) / sqrt(d)
+};
+
+__device__ __forceinline__ float to_f32(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ void store_elem(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
+__device__ __forceinline__ void store_elem(float* p, float x) { *p = x; }
+
+// Window row t = h*w + i of the group: query head kvh*G + h, position s-w+i.
+template <typename T, int D>
+__device__ __forceinline__ void load_window_row(Frag<T, D>& f, const BuildArgs& a, int b, int kvh, int t, int grp) {
+  if (t < a.R) {
+    const int h = t / a.w, i = t % a.w;
+    const T* q = static_cast<const T*>(a.q_obs) + (((size_t)b * a.Hq + kvh * a.G + h) * a.w + i) * D + grp * (D / 4);
+    f.load(q);
+  } else {
+    f.zero();
+  }
 }
 
-hipError_t launch_build(const reskv_shape_t&, const reskv_build_params_t&, const BuildPlan&, const void*,
-                        const void*, const int32_t*, const void*, const int32_t*, const int32_t*, void*, void*,
-                        float*, int32_t*, int32_t*, int32_t*, float*, int32_t*, void*, hipStream_t) {
-  return hipErrorNotSupported;
+// ---------------------------------------------------------------- scoring
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
+  const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int k0 = ch * kKeyChunk;
+  if (hm.all_main || k0 >= hm.s) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
+  Frag<T, D> kf[kKeyTiles];
+#pragma unroll
+  for (int kt = 0; kt < kKeyTiles; ++kt) {
+    const int p = min(k0 + 16 * kt + col, hm.s - 1);
+    kf[kt].load(K + (size_t)p * D + grp * (D / 4));
+  }
+  const int RT = (a.R + 15) / 16;
+  for (int rt = wave; rt < RT; rt += 4) {
+    Frag<T, D> qf;
+    load_window_row<T, D>(qf, a, b, kvh, 16 * rt + col, grp);
+    f32x4_t sc[kKeyTiles];
+#pragma unroll
+    for (int kt = 0; kt < kKeyTiles; ++kt) sc[kt] = mma<D>(qf, kf[kt], zero4());
+    float mx[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 16 * rt + 4 * grp + i;
+      const int pos = hm.s - a.w + (t < a.R ? t % a.w : 0);
+      float m = kNegInf;
+#pragma unroll
+      for (int kt = 0; kt < kKeyTiles; ++kt) {
+        const int p = k0 + 16 * kt + col;
+        const float v = (p < hm.s && p <= pos) ? sc[kt][i] * a.scale2 : kNegInf;
+        sc[kt][i] = v;
+        m = fmaxf(m, v);
+      }
+      m = wave_xor_max(m, 1); m = wave_xor_max(m, 2);
+      m = wave_xor_max(m, 4); m = wave_xor_max(m, 8);
+      mx[i] = m;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float mu = mx[i] == kNegInf ? 0.f : mx[i];
+      float l = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < kKeyTiles; ++kt) l += exp2f(sc[kt][i] - mu);
+      l = wave_xor_add(l, 1); l = wave_xor_add(l, 2);
+      l = wave_xor_add(l, 4); l = wave_xor_add(l, 8);
+      const int t = 16 * rt + 4 * grp + i;
+      if (col == 0 && t < a.R) a.lse_part[((size_t)bh * a.NCH + ch) * a.R + t] = make_float2(mx[i], l);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
+  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (hm.all_main || t >= a.R) return;
+  const int nch = (hm.s + kKeyChunk - 1) / kKeyChunk;
+  const float2* pp = a.lse_part + (size_t)bh * a.NCH * a.R + t;
+  float M = kNegInf;
+  for (int c = 0; c < nch; ++c) M = fmaxf(M, pp[(size_t)c * a.R].x);
+  float L = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float2 e = pp[(size_t)c * a.R];
+    if (e.x != kNegInf) L = fmaf(e.y, exp2f(e.x - M), L);
+  }
+  a.lse2[(size_t)bh * a.R + t] = M + log2f(L);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
+  const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int k0 = ch * kKeyChunk;
+  if (hm.all_main || k0 >= hm.n_sc) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  __shared__ float s_raw[4][kKeyChunk];
+  const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
+  Frag<T, D> kf[kKeyTiles];
+#pragma unroll
+  for (int kt = 0; kt < kKeyTiles; ++kt) {
+    const int p = min(k0 + 16 * kt + col, hm.s - 1);
+    kf[kt].load(K + (size_t)p * D + grp * (D / 4));
+  }
+  float ksum[kKeyTiles];
+#pragma unroll
+  for (int kt = 0; kt < kKeyTiles; ++kt) ksum[kt] = 0.f;
+  const int RT = (a.R + 15) / 16;
+  const float* lse2 = a.lse2 + (size_t)bh * a.R;
+  for (int rt = wave; rt < RT; rt += 4) {
+    Frag<T, D> qf;
+    load_window_row<T, D>(qf, a, b, kvh, 16 * rt + col, grp);
+    float lse[4];
+    int pos[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 16 * rt + 4 * grp + i;
+      lse[i] = t < a.R ? lse2[t] : 0.f;
+      pos[i] = t < a.R ? hm.s - a.w + t % a.w : -1;  // padded rows see no key
+    }
+#pragma unroll
+    for (int kt = 0; kt < kKeyTiles; ++kt) {
+      const f32x4_t sc = mma<D>(qf, kf[kt], zero4());
+      const int p = k0 + 16 * kt + col;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (p <= pos[i]) ksum[kt] += exp2f(fmaf(sc[i], a.scale2, -lse[i]));
+    }
+  }
+#pragma unroll
+  for (int kt = 0; kt < kKeyTiles; ++kt) {
+    float v = ksum[kt];
+    v = wave_xor_add(v, 16);
+    v = wave_xor_add(v, 32);
+    if (grp == 0) s_raw[wave][16 * kt + col] = v;
+  }
+  __syncthreads();
+  const int p = k0 + threadIdx.x;
+  if (p < hm.n_sc) {
+    const float v = ((s_raw[0][threadIdx.x] + s_raw[1][threadIdx.x]) + s_raw[2][threadIdx.x]) + s_raw[3][threadIdx.x];
+    a.raw[(size_t)bh * a.S + p] = v;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void pool5(BuildArgs a) {
+  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int p = blockIdx.x * kThreads + threadIdx.x;
+  if (p >= a.S) return;
+  const int n = hm.all_main ? 0 : hm.n_sc;
+  const float* raw = a.raw + (size_t)bh * a.S;
+  float v = -1.f;
+  if (p < n) {
+    v = 0.f;
+#pragma unroll
+    for (int o = -2; o <= 2; ++o) {
+      const int q = p + o;
+      if (q >= 0 && q < n) v += raw[q];
+    }
+    a.score[(size_t)bh * a.S + p] = v;
+  }
+  if (a.dbg_scores) a.dbg_scores[(size_t)bh * a.S + p] = v;
+}
+
+// -------------------------------------------------------------- selection
+
+// Exclusive scan of one int per thread over a block of NT threads.
+template <int NT>
+__device__ __forceinline__ int block_excl_scan(int v, int* s_tmp, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_tmp[wave] = x;
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int w2 = 0; w2 < NT / 64; ++w2) {
+    const int t = s_tmp[w2];
+    if (w2 < wave) off += t;
+    tot += t;
+  }
+  __syncthreads();
+  total = tot;
+  return off + x - v;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
+  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int tid = threadIdx.x;
+  int32_t* main_idx = a.main_idx + (size_t)bh * a.C;
+  if (tid == 0) {
+    a.res_len[bh] = hm.r;
+    a.main_len[bh] = hm.main_len;
+  }
+  if (hm.all_main) {
+    for (int i = tid; i < hm.s; i += kSelThreads) main_idx[i] = i;
+    return;
+  }
+  const int n = hm.n_sc;
+  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.score + (size_t)bh * a.S);
+  __shared__ int s_hist[2][256];
+  __shared__ int s_tmp[kSelThreads / 64];
+  __shared__ uint32_t s_pref[2];
+  __shared__ int s_krem[2];
+  // select the k-th largest value for k1 = k_top and k2 = k_top + r_eff
+  const int kk[2] = {hm.k_top, hm.k_top + hm.r_eff};
+  uint32_t prefix[2] = {0u, 0u}, mask = 0u;
+  int krem[2] = {kk[0], kk[1]};
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 512; i += kSelThreads) (&s_hist[0][0])[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < n; i += kSelThreads) {
+      const uint32_t u = key[i];
+      const int dig = (u >> shift) & 0xff;
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        if (krem[q] > 0 && (u & mask) == prefix[q]) atomicAdd(&s_hist[q][dig], 1);
+    }
+    __syncthreads();
+    if (tid < 2) {
+      const int q = tid;
+      if (krem[q] > 0) {
+        int acc = 0, d = 255;
+        for (; d > 0; --d) {
+          if (acc + s_hist[q][d] >= krem[q]) break;
+          acc += s_hist[q][d];
+        }
+        s_pref[q] = prefix[q] | ((uint32_t)d << shift);
+        s_krem[q] = krem[q] - acc;
+      } else {
+        s_pref[q] = prefix[q];
+        s_krem[q] = krem[q];
+      }
+    }
+    __syncthreads();
+    prefix[0] = s_pref[0]; prefix[1] = s_pref[1];
+    krem[0] = s_krem[0]; krem[1] = s_krem[1];
+    mask |= 0xffu << shift;
+    __syncthreads();
+  }
+  // thresholds T_q = prefix[q]; krem[q] = how many keys equal to T_q to take
+  // (lowest positions first); kk[q] == 0 selects nothing
+  const uint32_t T1 = prefix[0], T2 = prefix[1];
+  const int need1 = krem[0], need2 = krem[1];
+  const bool on1 = kk[0] > 0, on2 = kk[1] > 0;
+  const int L = (n + kSelThreads - 1) / kSelThreads;
+  const int lo = min(n, tid * L), hi = min(n, lo + L);
+  // pass 1: equal-to-threshold counts per segment, scanned
+  int e1 = 0, e2 = 0;
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t u = key[i];
+    e1 += (u == T1);
+    e2 += (u == T2);
+  }
+  int tot;
+  int eb1 = block_excl_scan<kSelThreads>(e1, s_tmp, tot);
+  int eb2 = block_excl_scan<kSelThreads>(e2, s_tmp, tot);
+  // pass 2: classify, count main / evicted / seed per segment
+  int c_top = 0, c_ev = 0, c_seed = 0;
+  {
+    int r1 = eb1, r2 = eb2;
+    for (int i = lo; i < hi; ++i) {
+      const uint32_t u = key[i];
+      const bool top = on1 && (u > T1 || (u == T1 && r1 < need1));
+      const bool sel2 = on2 && (u > T2 || (u == T2 && r2 < need2));
+      r1 += (u == T1);
+      r2 += (u == T2);
+      c_top += top;
+      c_ev += !top;
+      c_seed += (sel2 && !top);
+    }
+  }
+  int ob_top = block_excl_scan<kSelThreads>(c_top, s_tmp, tot);
+  int ob_ev = block_excl_scan<kSelThreads>(c_ev, s_tmp, tot);
+  int ob_seed = block_excl_scan<kSelThreads>(c_seed, s_tmp, tot);
+  // pass 3: write
+  int32_t* elist = a.elist + (size_t)bh * a.S;
+  int32_t* seeds = a.seeds + (size_t)bh * a.Rcap;
+  {
+    int r1 = eb1, r2 = eb2;
+    for (int i = lo; i < hi; ++i) {
+      const uint32_t u = key[i];
+      const bool top = on1 && (u > T1 || (u == T1 && r1 < need1));
+      const bool sel2 = on2 && (u > T2 || (u == T2 && r2 < need2));
+      r1 += (u == T1);
+      r2 += (u == T2);
+      if (top) main_idx[ob_top++] = i;
+      else elist[ob_ev++] = i;
+      if (sel2 && !top) seeds[ob_seed++] = i;
+    }
+  }
+  // the protected recent window follows the top-scored tokens
+  for (int i = tid; i < hm.P; i += kSelThreads) main_idx[hm.k_top + i] = hm.n_sc + i;
+}
+
+// ------------------------------------------------ gather + centre seeding
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void gather_init(BuildArgs a) {
+  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  constexpr int kChunks = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
+  const T* V = static_cast<const T*>(a.v) + (size_t)bh * a.S * D;
+  T* kc = static_cast<T*>(a.kc) + (size_t)bh * a.C * D;
+  T* vc = static_cast<T*>(a.vc) + (size_t)bh * a.C * D;
+  const int32_t* main_idx = a.main_idx + (size_t)bh * a.C;
+  const int rows = hm.main_len + hm.r;
+  for (int x = blockIdx.x * kThreads + threadIdx.x; x < rows * kChunks; x += gridDim.x * kThreads) {
+    const int row = x / kChunks, ck = x % kChunks;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    int dst;
+    if (row < hm.main_len) {
+      const int src = main_idx[row];
+      kv = reinterpret_cast<const uint4*>(K + (size_t)src * D)[ck];
+      vv = reinterpret_cast<const uint4*>(V + (size_t)src * D)[ck];
+      dst = hm.r + row;
+    } else {
+      dst = row - hm.main_len;  // residual slot, cleared
+    }
+    reinterpret_cast<uint4*>(kc + (size_t)dst * D)[ck] = kv;
+    reinterpret_cast<uint4*>(vc + (size_t)dst * D)[ck] = vv;
+  }
+  // every log-count starts empty; seeds become the first centres
+  for (int j = blockIdx.x * kThreads + threadIdx.x; j < a.Rcap; j += gridDim.x * kThreads)
+    a.logc[(size_t)bh * a.Rcap + j] = kNegInf;
+  const int32_t* seeds = a.seeds + (size_t)bh * a.Rcap;
+  for (int x = blockIdx.x * kThreads + threadIdx.x; x < hm.r_eff * D; x += gridDim.x * kThreads) {
+    const int j = x / D, d = x % D;
+    a.cent[((size_t)bh * a.Rcap + j) * D + d] = to_f32(K[(size_t)seeds[j] * D + d]);
+  }
+}
+
+// hi = bf16(mu), lo = bf16(mu - hi), norm = ||mu||^2 (fp64 sum, fixed order)
+template <int D>
+__device__ void prep_center(const BuildArgs& a, size_t ci, const float* mu, double* s_red) {
+  const int tid = threadIdx.x;
+  double sq = 0.0;
+  for (int d = tid; d < D; d += kThreads) {
+    const float x = mu[d];
+    const uint16_t h = f32_to_bf16_rne(x);
+    const uint16_t l = f32_to_bf16_rne(x - to_f32(h));
+    a.cent_hi[ci * D + d] = h;
+    a.cent_lo[ci * D + d] = l;
+    sq = (double)x * x;
+    s_red[d] = sq;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double t = 0.0;
+    for (int d = 0; d < D; ++d) t += s_red[d];
+    a.cnorm[ci] = (float)t;
+  }
+  __syncthreads();
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void center_prep(BuildArgs a) {
+  const int j = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  if (j >= hm.r_eff) return;
+  __shared__ double s_red[D];
+  const size_t ci = (size_t)bh * a.Rcap + j;
+  prep_center<D>(a, ci, a.cent + ci * D, s_red);
+}
+
+// ------------------------------------------------------------------ Lloyd
+
+// Centre fragments for one 16-centre tile: A operand rows.
+template <typename T, int D>
+struct CenterTile;
+
+template <int D>
+struct CenterTile<uint16_t, D> {   // split bf16: mu ~ hi + lo
+  Frag<uint16_t, D> hi, lo;
+};
+template <int D>
+struct CenterTile<float, D> {
+  Frag<float, D> f;
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void lloyd_assign(BuildArgs a, int iter) {
+  constexpr bool kBf = sizeof(T) == 2;
+  constexpr int kRowB = kBf ? D * 2 + 16 : D * 4 + 16;   // padded LDS row bytes
+  const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int t0 = blk * kTokBlock;
+  if (hm.r_eff == 0 || t0 >= hm.nE) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  // LDS: centre chunk (bf16: hi rows then lo rows; fp32: rows), norms, histogram
+  __shared__ __align__(16) unsigned char s_c[kCenterChunk * kRowB * (kBf ? 2 : 1)];
+  __shared__ float s_norm[kCenterChunk];
+  extern __shared__ int s_hist[];  // [r_eff]
+  for (int j = tid; j < hm.r_eff; j += kThreads) s_hist[j] = 0;
+
+  const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
+  const int32_t* elist = a.elist + (size_t)bh * a.S;
+  Frag<T, D> tk[4];  // token tiles of this wave
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) {
+    const int i = min(t0 + wave * 64 + 16 * tt + col, hm.nE - 1);
+    tk[tt].load(K + (size_t)elist[i] * D + grp * (D / 4));
+  }
+  float best[4][4];
+  int bidx[4][4];
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { best[tt][i] = __builtin_huge_valf(); bidx[tt][i] = 0x7fffffff; }
+
+  const size_t cbase = (size_t)bh * a.Rcap;
+  for (int j0 = 0; j0 < hm.r_eff; j0 += kCenterChunk) {
+    const int nj = min(kCenterChunk, hm.r_eff - j0);
+    __syncthreads();
+    // stage the chunk: 16-byte pieces
+    constexpr int kPieces = (kBf ? D * 2 : D * 4) / 16;
+    for (int x = tid; x < kCenterChunk * kPieces; x += kThreads) {
+      const int jj = x / kPieces, pc = x % kPieces;
+      uint4 hv = make_uint4(0, 0, 0, 0), lv = make_uint4(0, 0, 0, 0);
+      if (jj < nj) {
+        if (kBf) {
+          hv = reinterpret_cast<const uint4*>(a.cent_hi + (cbase + j0 + jj) * D)[pc];
+          lv = reinterpret_cast<const uint4*>(a.cent_lo + (cbase + j0 + jj) * D)[pc];
+        } else {
+          hv = reinterpret_cast<const uint4*>(a.cent + (cbase + j0 + jj) * D)[pc];
+        }
+      }
+      *reinterpret_cast<uint4*>(s_c + jj * kRowB + pc * 16) = hv;
+      if (kBf) *reinterpret_cast<uint4*>(s_c + (kCenterChunk + jj) * kRowB + pc * 16) = lv;
+    }
+    for (int jj = tid; jj < kCenterChunk; jj += kThreads) s_norm[jj] = jj < nj ? a.cnorm[cbase + j0 + jj] : 0.f;
+    __syncthreads();
+#pragma unroll
+    for (int ct = 0; ct < kCenterChunk / 16; ++ct) {
+      if (16 * ct >= nj) break;  // block-uniform
+      CenterTile<T, D> cf;
+      const int crow = 16 * ct + col;
+      if constexpr (kBf) {
+        cf.hi.load(reinterpret_cast<const uint16_t*>(s_c + crow * kRowB) + grp * (D / 4));
+        cf.lo.load(reinterpret_cast<const uint16_t*>(s_c + (kCenterChunk + crow) * kRowB) + grp * (D / 4));
+      } else {
+        cf.f.load(reinterpret_cast<const float*>(s_c + crow * kRowB) + grp * (D / 4));
+      }
+      float nrm[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) nrm[i] = s_norm[16 * ct + 4 * grp + i];
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        f32x4_t dot;
+        if constexpr (kBf) dot = mma<D>(cf.lo, tk[tt], mma<D>(cf.hi, tk[tt], zero4()));
+        else dot = mma<D>(cf.f, tk[tt], zero4());
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = j0 + 16 * ct + 4 * grp + i;
+          const float dist = fmaf(-2.f, dot[i], nrm[i]);
+          if (j < hm.r_eff && dist < best[tt][i]) { best[tt][i] = dist; bidx[tt][i] = j; }
+        }
+      }
+    }
+  }
+  // argmin over the 16 centres of a lane (4 rows x 4 lane groups): ties to lower index
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) {
+    float bv = best[tt][0];
+    int bi = bidx[tt][0];
+#pragma unroll
+    for (int i = 1; i < 4; ++i)
+      if (best[tt][i] < bv || (best[tt][i] == bv && bidx[tt][i] < bi)) { bv = best[tt][i]; bi = bidx[tt][i]; }
+#pragma unroll
+    for (int msk = 16; msk < 64; msk <<= 1) {
+      const float ov = __shfl_xor(bv, msk, 64);
+      const int oi = __shfl_xor(bi, msk, 64);
+      if (ov < bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    }
+    if (bi >= hm.r_eff) bi = 0;  // only reachable with non-finite keys
+    const int i = t0 + wave * 64 + 16 * tt + col;
+    if (grp == 0 && i < hm.nE) {
+      a.assign[(size_t)bh * a.S + i] = bi;
+      atomicAdd(&s_hist[bi], 1);
+      if (a.dbg_assign) a.dbg_assign[((size_t)iter * a.B * a.Hkv + bh) * a.S + elist[i]] = bi;
+    }
+  }
+  __syncthreads();
+  int32_t* hist = a.hist + ((size_t)bh * a.NBLK + blk) * a.Rcap;
+  for (int j = tid; j < hm.r_eff; j += kThreads) hist[j] = s_hist[j];
+}
+
+// Group sizes and counting-sort offsets: hist[blk][j] becomes the first
+// output position of block blk's members of group j.
+__global__ __launch_bounds__(kThreads) void lloyd_offsets(BuildArgs a) {
+  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  if (hm.r_eff == 0) return;
+  __shared__ int s_tmp[kThreads / 64];
+  const int nblk = (hm.nE + kTokBlock - 1) / kTokBlock;
+  int32_t* hist = a.hist + (size_t)bh * a.NBLK * a.Rcap;
+  int carry = 0;
+  for (int j0 = 0; j0 < hm.r_eff; j0 += kThreads) {
+    const int j = j0 + threadIdx.x;
+    int tot = 0;
+    if (j < hm.r_eff)
+      for (int q = 0; q < nblk; ++q) tot += hist[(size_t)q * a.Rcap + j];
+    int all;
+    const int start = carry + block_excl_scan<kThreads>(tot, s_tmp, all);
+    if (j < hm.r_eff) {
+      a.cstart[(size_t)bh * a.Rcap + j] = start;
+      a.ccount[(size_t)bh * a.Rcap + j] = tot;
+      int run = start;
+      for (int q = 0; q < nblk; ++q) {
+        const int c = hist[(size_t)q * a.Rcap + j];
+        hist[(size_t)q * a.Rcap + j] = run;
+        run += c;
+      }
+    }
+    carry += all;
+  }
+}
+
+// Stable placement: members of a group keep ascending evicted order.
+__global__ __launch_bounds__(kThreads) void lloyd_scatter(BuildArgs a) {
+  const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  const int t0 = blk * kTokBlock;
+  if (hm.r_eff == 0 || t0 >= hm.nE) return;
+  __shared__ int s_a[kTokBlock];
+  const int i = t0 + threadIdx.x;
+  const int g = i < hm.nE ? a.assign[(size_t)bh * a.S + i] : -1;
+  s_a[threadIdx.x] = g;
+  __syncthreads();
+  if (g < 0) return;
+  int rank = 0;
+  for (int q = 0; q < (int)threadIdx.x; ++q) rank += (s_a[q] == g);
+  const int dst = a.hist[((size_t)bh * a.NBLK + blk) * a.Rcap + g] + rank;
+  a.order[(size_t)bh * a.S + dst] = a.elist[(size_t)bh * a.S + i];
+}
+
+// New centre of group j = fp64 mean of its members' keys, summed in a fixed
+// order; an empty group keeps its centre. The last round also writes the
+// entry: mean key and mean value in the cache dtype, and log c_j.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void lloyd_update(BuildArgs a, int last) {
+  const int j = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const HeadMeta hm = a.meta[bh];
+  if (j >= hm.r_eff) return;
+  constexpr int CPR = D / 8;            // lanes per row, 8 elements each
+  constexpr int NG = kThreads / CPR;    // member groups
+  __shared__ double s_sum[NG][D];
+  __shared__ float s_mu[D];
+  __shared__ double s_red[D];
+  const int tid = threadIdx.x, c = tid % CPR, g = tid / CPR;
+  const size_t ci = (size_t)bh * a.Rcap + j;
+  const int cnt = a.ccount[ci];
+  const int32_t* mem = a.order + (size_t)bh * a.S + a.cstart[ci];
+  const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
+  const T* V = static_cast<const T*>(a.v) + (size_t)bh * a.S * D;
+  for (int pass = 0; pass < (last ? 2 : 1); ++pass) {
+    const T* X = pass == 0 ? K : V;
+    double acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    for (int q = g; q < cnt; q += NG) {
+      const T* row = X + (size_t)mem[q] * D + 8 * c;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += (double)to_f32(row[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s_sum[g][8 * c + e] = acc[e];
+    __syncthreads();
+    if (tid < D) {
+      double t = 0.0;
+      for (int gg = 0; gg < NG; ++gg) t += s_sum[gg][tid];
+      const float mean = cnt > 0 ? (float)(t / cnt) : 0.f;
+      if (pass == 0) {
+        const float mu = cnt > 0 ? mean : a.cent[ci * D + tid];  // empty group keeps its centre
+        s_mu[tid] = mu;
+        a.cent[ci * D + tid] = mu;
+        if (last) store_elem(static_cast<T*>(a.kc) + ((size_t)bh * a.C + j) * D + tid, mu);
+      } else {
+        store_elem(static_cast<T*>(a.vc) + ((size_t)bh * a.C + j) * D + tid, mean);
+      }
+    }
+    __syncthreads();
+  }
+  if (last) {
+    if (tid == 0) a.logc[ci] = cnt > 0 ? logf((float)cnt) : kNegInf;
+  } else {
+    prep_center<D>(a, ci, s_mu, s_red);
+  }
+}
+
+__global__ void fill_i32(int32_t* p, size_t n, int32_t v) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+// Sizes of one (b, kv head) from its context length s, residual count r and
+// budget b (main-selection equation, Sec. 5.2; reading R4 for |P|).
+__host__ __device__ inline HeadMeta make_meta(int s, int r, int budget, int recent) {
+  HeadMeta m{};
+  m.s = s;
+  m.r = r;
+  m.m = budget - r;
+  m.all_main = s <= m.m;
+  m.P = m.all_main ? 0 : (recent < m.m ? recent : m.m);
+  if (m.P > s) m.P = s;
+  m.n_sc = m.all_main ? 0 : s - m.P;
+  m.k_top = m.all_main ? 0 : m.m - m.P;
+  m.nE = m.all_main ? 0 : s - m.m;
+  m.r_eff = r < m.nE ? r : m.nE;
+  m.main_len = m.all_main ? s : m.m;
+  return m;
+}
+
+void head_meta(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
+               const int32_t* budget, const int32_t* res_count, std::vector<HeadMeta>& out) {
+  const int Hkv = s.num_kv_heads;
+  out.resize((size_t)s.batch * Hkv);
+  for (int b = 0; b < s.batch; ++b)
+    for (int h = 0; h < Hkv; ++h)
+      out[(size_t)b * Hkv + h] = make_meta(seq_len[b], res_count[b * Hkv + h], budget[b], p.recent_window);
+}
+
+// Per-head sizes travel as kernel arguments (copied at launch), in chunks.
+constexpr int kMetaChunk = 256;
+struct MetaChunk {
+  int first, count, recent;
+  int s[kMetaChunk], r[kMetaChunk], budget[kMetaChunk];
+};
+
+__global__ void meta_kernel(HeadMeta* meta, MetaChunk c) {
+  const int i = threadIdx.x;
+  if (i < c.count) meta[c.first + i] = make_meta(c.s[i], c.r[i], c.budget[i], c.recent);
+}
+
+template <typename T, int D>
+hipError_t launch_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
+  const dim3 bhg(1, pl.Hkv, pl.B);
+  auto grid = [&](int x) { return dim3(x < 1 ? 1 : x, pl.Hkv, pl.B); };
+  hipError_t e;
+#define RESKV_CHECK() do { e = hipGetLastError(); if (e != hipSuccess) return e; } while (0)
+  if (a.dbg_assign) {
+    hipLaunchKernelGGL(fill_i32, dim3(1024), dim3(256), 0, st, a.dbg_assign,
+                       (size_t)pl.T * pl.B * pl.Hkv * pl.S, -1);
+    RESKV_CHECK();
+  }
+  hipLaunchKernelGGL((lse_partial<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(pool5, grid((pl.S + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(select_kernel, bhg, dim3(kSelThreads), 0, st, a); RESKV_CHECK();
+  const int rows = pl.max_main + pl.Rcap;
+  const int gblocks = (rows * (D * (int)sizeof(T) / 16) + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL((gather_init<T, D>), grid(gblocks < 64 ? gblocks : 64), dim3(kThreads), 0, st, a);
+  RESKV_CHECK();
+  if (pl.max_reff > 0) {
+    hipLaunchKernelGGL((center_prep<D>), grid(pl.max_reff), dim3(kThreads), 0, st, a); RESKV_CHECK();
+    const size_t hist_lds = (size_t)pl.max_reff * sizeof(int);
+    for (int it = 0; it < pl.T; ++it) {
+      hipLaunchKernelGGL((lloyd_assign<T, D>), grid(pl.NBLK), dim3(kThreads), hist_lds, st, a, it); RESKV_CHECK();
+      hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
+      hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kThreads), 0, st, a); RESKV_CHECK();
+      hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, it == pl.T - 1 ? 1 : 0);
+      RESKV_CHECK();
+    }
+  }
+#undef RESKV_CHECK
+  return hipSuccess;
+}
+
+}  // namespace
+
+bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
+                     const int32_t* budget, const int32_t* res_count, BuildPlan* plan) {
+  std::vector<HeadMeta> hm;
+  head_meta(s, p, seq_len, budget, res_count, hm);
+  BuildPlan& pl = *plan;
+  pl = BuildPlan{};
+  pl.B = s.batch; pl.Hq = s.num_q_heads; pl.Hkv = s.num_kv_heads; pl.G = s.num_q_heads / s.num_kv_heads;
+  pl.D = s.head_dim; pl.C = s.slot_cap; pl.Rcap = s.res_cap; pl.S = p.max_seq_len; pl.w = p.obs_window;
+  pl.R = pl.G * pl.w; pl.T = p.lloyd_iters; pl.dtype = s.dtype;
+  if (pl.R > 1024 || pl.Rcap > 4096) return false;
+  int max_E = 0;
+  for (const HeadMeta& m : hm) {
+    if (m.s > pl.max_s) pl.max_s = m.s;
+    if (m.main_len > pl.max_main) pl.max_main = m.main_len;
+    if (m.r_eff > pl.max_reff) pl.max_reff = m.r_eff;
+    if (m.nE > max_E) max_E = m.nE;
+    if (m.main_len + m.r > pl.C) return false;
+  }
+  pl.NCH = (pl.max_s + kKeyChunk - 1) / kKeyChunk;
+  pl.NBLK = (max_E + kTokBlock - 1) / kTokBlock;
+  if (pl.NBLK < 1) pl.NBLK = 1;
+  const size_t BH = (size_t)pl.B * pl.Hkv;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off = align_up(off + bytes, 256); return o; };
+  pl.off_meta = take(BH * sizeof(HeadMeta));
+  pl.off_lsep = take(BH * pl.NCH * pl.R * sizeof(float2));
+  pl.off_lse = take(BH * pl.R * sizeof(float));
+  pl.off_raw = take(BH * pl.S * sizeof(float));
+  pl.off_score = take(BH * pl.S * sizeof(float));
+  pl.off_elist = take(BH * pl.S * sizeof(int32_t));
+  pl.off_seeds = take(BH * pl.Rcap * sizeof(int32_t));
+  pl.off_cent = take(BH * pl.Rcap * pl.D * sizeof(float));
+  pl.off_chi = take(BH * pl.Rcap * pl.D * sizeof(uint16_t));
+  pl.off_clo = take(BH * pl.Rcap * pl.D * sizeof(uint16_t));
+  pl.off_cnorm = take(BH * pl.Rcap * sizeof(float));
+  pl.off_assign = take(BH * pl.S * sizeof(int32_t));
+  pl.off_hist = take(BH * pl.NBLK * pl.Rcap * sizeof(int32_t));
+  pl.off_cstart = take(BH * pl.Rcap * sizeof(int32_t));
+  pl.off_ccount = take(BH * pl.Rcap * sizeof(int32_t));
+  pl.off_order = take(BH * pl.S * sizeof(int32_t));
+  pl.bytes = off;
+  return true;
+}
+
+hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, const BuildPlan& pl,
+                        const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
+                        const int32_t* budget, const int32_t* res_count, void* kc, void* vc,
+                        float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
+                        float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                        hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  HeadMeta* meta = reinterpret_cast<HeadMeta*>(ws + pl.off_meta);
+  const int BH = pl.B * pl.Hkv;
+  for (int first = 0; first < BH; first += kMetaChunk) {
+    MetaChunk c;
+    c.first = first;
+    c.count = BH - first < kMetaChunk ? BH - first : kMetaChunk;
+    c.recent = p.recent_window;
+    for (int i = 0; i < c.count; ++i) {
+      const int bh = first + i, b = bh / pl.Hkv;
+      c.s[i] = seq_len[b];
+      c.r[i] = res_count[bh];
+      c.budget[i] = budget[b];
+    }
+    hipLaunchKernelGGL(meta_kernel, dim3(1), dim3(kMetaChunk), 0, stream, meta, c);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  BuildArgs a{};
+  a.k = k; a.v = v; a.q_obs = q_obs; a.kc = kc; a.vc = vc; a.logc = logc; a.main_idx = main_idx;
+  a.res_len = res_len; a.main_len = main_len; a.dbg_scores = dbg_scores; a.dbg_assign = dbg_assign;
+  a.meta = meta;
+  a.lse_part = reinterpret_cast<float2*>(ws + pl.off_lsep);
+  a.lse2 = reinterpret_cast<float*>(ws + pl.off_lse);
+  a.raw = reinterpret_cast<float*>(ws + pl.off_raw);
+  a.score = reinterpret_cast<float*>(ws + pl.off_score);
+  a.elist = reinterpret_cast<int32_t*>(ws + pl.off_elist);
+  a.seeds = reinterpret_cast<int32_t*>(ws + pl.off_seeds);
+  a.cent = reinterpret_cast<float*>(ws + pl.off_cent);
+  a.cent_hi = reinterpret_cast<uint16_t*>(ws + pl.off_chi);
+  a.cent_lo = reinterpret_cast<uint16_t*>(ws + pl.off_clo);
+  a.cnorm = reinterpret_cast<float*>(ws + pl.off_cnorm);
+  a.assign = reinterpret_cast<int32_t*>(ws + pl.off_assign);
+  a.hist = reinterpret_cast<int32_t*>(ws + pl.off_hist);
+  a.cstart = reinterpret_cast<int32_t*>(ws + pl.off_cstart);
+  a.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
+  a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
+  a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
+  a.R = pl.R; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
+  a.scale2 = kLog2e / sqrtf((float)pl.D);
+  const bool bf = s.dtype == RESKV_BF16;
+  if (pl.D == 128) return bf ? launch_typed<uint16_t, 128>(pl, a, stream) : launch_typed<float, 128>(pl, a, stream);
+  if (pl.D == 64) return bf ? launch_typed<uint16_t, 64>(pl, a, stream) : launch_typed<float, 64>(pl, a, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace reskv

@@ -60,4 +60,63 @@ __device__ __forceinline__ int clampi(int x, int lo, int hi) {
   return x < lo ? lo : (x > hi ? hi : x);
 }
 
+// ---- 16x16 MFMA tiles over a full row of D elements ------------------------
+// C[16 x 16] = A[16 x D] . B[16 x D]^T. Lane l supplies A row (l % 16) and B
+// row (l % 16), both restricted to the quarter [(l/16)*D/4, (l/16+1)*D/4) of
+// the row; the contraction over D is split into MFMA k-steps inside that
+// quarter (the same split for A and B, so the sum covers every element once).
+// Result layout: lane l holds C[4*(l/16) + i][l % 16] for i = 0..3.
+template <typename T, int D>
+struct Frag;
+
+template <int D>
+struct Frag<uint16_t, D> {        // bf16: 16x16x32 steps, 8 elements per step
+  static constexpr int kSteps = D / 32;
+  uint4 w[kSteps];
+  __device__ __forceinline__ void load(const uint16_t* quarter) {
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const uint4*>(quarter + 8 * i);
+  }
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) w[i] = make_uint4(0, 0, 0, 0);
+  }
+};
+
+template <int D>
+struct Frag<float, D> {           // fp32: 16x16x4 steps, 1 element per step
+  static constexpr int kSteps = D / 16;  // float4 groups
+  float4 w[kSteps];
+  __device__ __forceinline__ void load(const float* quarter) {
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const float4*>(quarter + 4 * i);
+  }
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) w[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+};
+
+template <int D>
+__device__ __forceinline__ f32x4_t mma(const Frag<uint16_t, D>& a, const Frag<uint16_t, D>& b, f32x4_t acc) {
+#pragma unroll
+  for (int i = 0; i < Frag<uint16_t, D>::kSteps; ++i)
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a.w[i]), as_bf16x8(b.w[i]), acc, 0, 0, 0);
+  return acc;
+}
+
+template <int D>
+__device__ __forceinline__ f32x4_t mma(const Frag<float, D>& a, const Frag<float, D>& b, f32x4_t acc) {
+#pragma unroll
+  for (int i = 0; i < Frag<float, D>::kSteps; ++i) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w[i].x, b.w[i].x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w[i].y, b.w[i].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w[i].z, b.w[i].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w[i].w, b.w[i].w, acc, 0, 0, 0);
+  }
+  return acc;
+}
+
+__device__ __forceinline__ f32x4_t zero4() { return f32x4_t{0.f, 0.f, 0.f, 0.f}; }
+
 }  // namespace reskv

@@ -61,64 +61,16 @@ __device__ __forceinline__ void cache_lengths(const int32_t* res_len, const int3
 }
 
 // ---- Q.K^T on MFMA: C[head][slot] for 16 heads x 16 slots ------------------
-// Lane (col + 16*grp): A operand = query head `col`, B operand = key row of
-// slot `col`; lane group `grp` owns the contiguous quarter
-// [grp*D/4, (grp+1)*D/4) of the head dimension for both operands.
+// A operand = query head (lane % 16), B operand = key row of slot (lane % 16).
 template <typename T, int D>
-struct QK;
-
-template <int D>
-struct QK<uint16_t, D> {
-  static constexpr int kSteps = D / 32;  // 16x16x32 bf16 steps per quarter row
-  struct KFrag { uint4 w[kSteps]; };
-  bf16x8_t q[kSteps];
-  __device__ void load_q(const uint16_t* qrow, bool live) {
-#pragma unroll
-    for (int i = 0; i < kSteps; ++i) {
-      uint4 w = live ? *reinterpret_cast<const uint4*>(qrow + 8 * i) : make_uint4(0, 0, 0, 0);
-      q[i] = as_bf16x8(w);
-    }
+struct QK {
+  using KFrag = Frag<T, D>;
+  Frag<T, D> q;
+  __device__ void load_q(const T* qrow, bool live) {
+    if (live) q.load(qrow); else q.zero();
   }
-  __device__ static void load_k(KFrag& f, const uint16_t* krow) {
-#pragma unroll
-    for (int i = 0; i < kSteps; ++i) f.w[i] = *reinterpret_cast<const uint4*>(krow + 8 * i);
-  }
-  __device__ f32x4_t run(const KFrag& f) const {
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < kSteps; ++i)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[i], as_bf16x8(f.w[i]), acc, 0, 0, 0);
-    return acc;
-  }
-};
-
-template <int D>
-struct QK<float, D> {
-  static constexpr int kSteps = D / 4;  // 16x16x4 f32 steps per quarter row
-  struct KFrag { float4 w[kSteps / 4]; };
-  float q[kSteps];
-  __device__ void load_q(const float* qrow, bool live) {
-#pragma unroll
-    for (int i = 0; i < kSteps; i += 4) {
-      float4 w = live ? *reinterpret_cast<const float4*>(qrow + i) : make_float4(0.f, 0.f, 0.f, 0.f);
-      q[i] = w.x; q[i + 1] = w.y; q[i + 2] = w.z; q[i + 3] = w.w;
-    }
-  }
-  __device__ static void load_k(KFrag& f, const float* krow) {
-#pragma unroll
-    for (int i = 0; i < kSteps / 4; ++i) f.w[i] = *reinterpret_cast<const float4*>(krow + 4 * i);
-  }
-  __device__ f32x4_t run(const KFrag& f) const {
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < kSteps / 4; ++i) {
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 0], f.w[i].x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 1], f.w[i].y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 2], f.w[i].z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q[4 * i + 3], f.w[i].w, acc, 0, 0, 0);
-    }
-    return acc;
-  }
+  __device__ static void load_k(KFrag& f, const T* krow) { f.load(krow); }
+  __device__ f32x4_t run(const KFrag& f) const { return mma<D>(q, f, zero4()); }
 };
 
 // 8 consecutive value-row elements, loaded raw and widened later.

@@ -30,14 +30,27 @@ hipError_t launch_append(const reskv_shape_t& s, const void* k_new, const void* 
                          void* vc, const int32_t* res_len, int32_t* main_len, hipStream_t stream);
 
 // Construction.
+// Sizes of one (b, kv head), fixed on the host from seq_len, budget and r.
+struct HeadMeta {
+  int s;         // context length
+  int r;         // residual entries
+  int m;         // main slots of the budget (b - r)
+  int P;         // protected recent tokens, min(recent_window, m, s)
+  int n_sc;      // scored positions [0, n_sc), s - P
+  int k_top;     // top-scored tokens kept, m - P
+  int nE;        // evicted tokens, s - m (0 when every token is kept)
+  int r_eff;     // Lloyd groups, min(r, nE)
+  int main_len;  // min(m, s)
+  int all_main;  // 1 when s <= m
+};
+
 struct BuildPlan {
-  int B, Hq, Hkv, G, D, C, Rcap, S, w, T, dtype;
-  // per-(b, kv head) host-side sizes
-  int max_s, max_scored, max_E, max_r;
-  size_t bytes;
-  size_t off_lse, off_raw, off_score, off_meta, off_elist, off_seeds, off_cent, off_assign,
-      off_cnt, off_perm, off_sum, off_hist, off_misc;
-  int n_lse_parts;  // key chunks of the LSE pass
+  int B, Hq, Hkv, G, D, C, Rcap, S, w, R, T, dtype;
+  int NCH;    // 256-key chunks of the longest sequence
+  int NBLK;   // 256-token blocks of the largest evicted set
+  int max_s, max_main, max_reff;
+  size_t off_meta, off_lsep, off_lse, off_raw, off_score, off_elist, off_seeds, off_cent, off_chi,
+      off_clo, off_cnorm, off_assign, off_hist, off_cstart, off_ccount, off_order, bytes;
 };
 
 bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,

@@ -1,0 +1,165 @@
+"""Runs reskv_build_cache through the C ABI and checks it against the oracle.
+
+Parity contract for construction (scores, selection, Lloyd, entries):
+  * scores: |gpu - oracle| <= 1e-4 * |oracle| + 1e-30 per scored position;
+  * selection from the GPU's own fp32 scores is exact: the oracle's selection
+    run on those scores reproduces main_idx bit for bit;
+  * main_idx equals the oracle's own fp64 selection except where the oracle's
+    scores at the k_top boundary are closer than the score tolerance
+    (certified near-ties, counted and returned);
+  * Lloyd replay: in every round each evicted token's GPU group is an
+    eps-argmin of the fp64 distances to the centres the oracle recomputes from
+    the GPU's previous round (the first round uses the seeds the oracle selects
+    from the GPU scores);
+  * counts equal the oracle's recount of the GPU's last assignment; stored
+    mean keys/values are within one storage ulp of the fp64 means of the GPU's
+    groups (fp32 caches: 1e-6 relative); empty groups have log-count -inf.
+"""
+
+import math
+
+import numpy as np
+import torch
+
+from oracle import reskv_oracle as orc
+from paper_2607_29591_amd import reskv as rk
+
+SCORE_RTOL = 1e-4
+
+
+def to_dev(x, dtype):
+    t = torch.as_tensor(np.asarray(x, np.float32))
+    return (t.to(torch.bfloat16) if dtype == "bf16" else t).cuda().contiguous()
+
+
+def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None):
+    """Build one layer on the GPU; returns host numpy copies of every output."""
+    B, Hkv, d = wl.batch, wl.hkv, wl.d
+    S = x["K"].shape[2]
+    C, Rcap = wl.slot_cap, wl.res_cap
+    T = wl.lloyd_iters if iters is None else iters
+    shape = rk.make_shape(B, wl.hq, Hkv, d, wl.dtype, C, Rcap)
+    params = rk.BuildParams(S, wl.window, wl.window if recent is None else recent, T)
+    res = np.asarray(x["res"], np.int32).reshape(-1)
+    K = x["K"] if torch.is_tensor(x["K"]) else to_dev(x["K"], wl.dtype)
+    V = x["V"] if torch.is_tensor(x["V"]) else to_dev(x["V"], wl.dtype)
+    Q = x["q_obs"] if torch.is_tensor(x["q_obs"]) else to_dev(x["q_obs"], wl.dtype)
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    kc = torch.full((B, Hkv, C, d), 7.0, dtype=tdt, device="cuda")
+    vc = torch.full((B, Hkv, C, d), 7.0, dtype=tdt, device="cuda")
+    logc = torch.full((B, Hkv, Rcap), 7.0, device="cuda")
+    main_idx = torch.full((B, Hkv, C), -7, dtype=torch.int32, device="cuda")
+    res_len = torch.full((B * Hkv,), -7, dtype=torch.int32, device="cuda")
+    main_len = torch.full((B * Hkv,), -7, dtype=torch.int32, device="cuda")
+    dbg_s = torch.empty((B, Hkv, S), device="cuda") if dbg else None
+    dbg_a = torch.empty((T, B, Hkv, S), dtype=torch.int32, device="cuda") if dbg else None
+    nws = rk.reskv_build_workspace_size(shape, params, x["seq_len"], x["budget"], res)
+    assert nws > 0
+    ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
+    rk.reskv_build_cache(shape, params, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc, main_idx,
+                         res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
+    torch.cuda.synchronize()
+    out = dict(kc=kc.float().cpu().numpy().astype(np.float64), vc=vc.float().cpu().numpy().astype(np.float64),
+               logc=logc.cpu().numpy().astype(np.float64), main_idx=main_idx.cpu().numpy(),
+               res_len=res_len.cpu().numpy().reshape(B, Hkv), main_len=main_len.cpu().numpy().reshape(B, Hkv))
+    if dbg:
+        out["scores"] = dbg_s.cpu().numpy().astype(np.float64)
+        out["assign"] = dbg_a.cpu().numpy()
+    return out
+
+
+def ulp(x, dtype):
+    """Spacing of the storage format at |x| (bf16: 8 significant bits)."""
+    x = np.abs(np.asarray(x, np.float64))
+    if dtype == "bf16":
+        e = np.floor(np.log2(np.maximum(x, 2.0 ** -126)))
+        return np.exp2(e - 7)
+    return np.maximum(x, 1e-30) * 2.0 ** -23
+
+
+def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True):
+    """All construction checks for one (b, kv head). Returns a report dict."""
+    recent = wl.window if recent is None else recent
+    T = wl.lloyd_iters if iters is None else iters
+    G = wl.group
+    s = int(x["seq_len"][b])
+    r = int(x["res"][b][h])
+    m = int(x["budget"][b]) - r
+    K = np.asarray(x["K_host"][b, h, :s], np.float64)
+    V = np.asarray(x["V_host"][b, h, :s], np.float64)
+    Qw = np.asarray(x["q_host"][b, h * G:(h + 1) * G], np.float64)
+    rep = dict(near_ties=0, lloyd_agree=None)
+    assert got["res_len"][b, h] == r
+    ml = int(got["main_len"][b, h])
+    assert ml == min(m, s)
+    midx = got["main_idx"][b, h, :ml].astype(np.int64)
+    if s <= m:
+        assert (midx == np.arange(s)).all()
+        assert np.isinf(got["logc"][b, h, :r]).all() and (got["logc"][b, h, :r] < 0).all()
+        np.testing.assert_array_equal(got["kc"][b, h, r:r + ml], K)
+        return rep
+    n = orc.scored_length(s, m, recent)
+    gs = got["scores"][b, h, :n]
+    # (ii) score parity
+    if full_oracle:
+        raw = orc.window_raw_scores(K, Qw)
+        ref = orc.pool5(raw[:n])
+        err = np.abs(gs - ref)
+        assert (err <= SCORE_RTOL * np.abs(ref) + 1e-30).all(), \
+            f"score err {(err / np.maximum(np.abs(ref), 1e-30)).max():.2e}"
+    # (i) exact selection on the GPU's own scores
+    main_g, ev_g, seeds_g = orc.select_main(gs, s, m, recent, r)
+    np.testing.assert_array_equal(midx, main_g)
+    # (iii) end-to-end selection against the oracle's fp64 scores, with
+    # certified near-ties at the k_top boundary
+    if full_oracle:
+        main_o, _, _ = orc.select_main(ref, s, m, recent, r)
+        if not np.array_equal(main_o, main_g):
+            k_top = m - min(recent, m, s)
+            srt = np.sort(ref)[::-1]
+            gap = abs(srt[k_top - 1] - srt[k_top]) if 0 < k_top < n else 0.0
+            assert gap <= 2 * SCORE_RTOL * srt[max(k_top - 1, 0)], "selection differs outside a near-tie"
+            rep["near_ties"] += 1
+    # cache main rows are exact copies
+    np.testing.assert_array_equal(got["kc"][b, h, r:r + ml], K[midx])
+    np.testing.assert_array_equal(got["vc"][b, h, r:r + ml], V[midx])
+    if r == 0 or not replay:
+        return rep
+    # (iv) Lloyd replay
+    KE = K[ev_g]
+    nE = ev_g.size
+    r_eff = min(r, nE)
+    mu = K[seeds_g].copy()
+    assign = None
+    for it in range(T):
+        a = got["assign"][it, b, h][ev_g]
+        assert (a >= 0).all() and (a < r_eff).all()
+        _, dist = orc.assign_nearest(KE, mu)
+        chosen = dist[np.arange(nE), a]
+        M = np.sqrt((mu ** 2).sum(1).max())
+        kn = np.sqrt((KE ** 2).sum(1))
+        eps = 1e-4 * (kn * M + M * M) + 1e-6
+        bad = chosen > dist.min(axis=1) + eps
+        assert not bad.any(), f"round {it}: {bad.sum()} tokens not at an eps-argmin"
+        for j in range(r_eff):
+            mem = a == j
+            if mem.any():
+                mu[j] = KE[mem].mean(axis=0)
+        assign = a
+    cnt = np.bincount(assign, minlength=r)
+    lc = got["logc"][b, h, :r]
+    for j in range(r):
+        if cnt[j] == 0:
+            assert lc[j] == -np.inf
+            assert (got["vc"][b, h, j] == 0).all()
+        else:
+            assert abs(lc[j] - math.log(cnt[j])) <= 1e-6 * max(1.0, math.log(cnt[j]))
+            km = KE[assign == j].mean(axis=0)
+            vm = V[ev_g][assign == j].mean(axis=0)
+            assert (np.abs(got["kc"][b, h, j] - km) <= ulp(km, wl.dtype) * 1.0001).all(), f"kbar {j}"
+            assert (np.abs(got["vc"][b, h, j] - vm) <= ulp(vm, wl.dtype) * 1.0001).all(), f"vbar {j}"
+    assert cnt.sum() == nE
+    if full_oracle:
+        a_o, _, _ = orc.lloyd(KE, K[seeds_g], T)
+        rep["lloyd_agree"] = float((a_o == assign).mean())
+    return rep
