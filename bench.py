@@ -1,0 +1,355 @@
+#!/usr/bin/env python3
+"""Benchmark of the ResKV hot path on one MI355X.
+
+Workload (default): batched decode, bf16, 32 layers x (32 query / 8 KV heads,
+head_dim 128), batch 32, every sequence a 32768-token prefill compressed to a
+2048-slot budget per KV head, residual split per (layer, KV head) drawn from
+{0, 64, 128, 256, 512}, per-query gate thresholds tau ~ N(0, 0.5), 256 decode
+steps that each append one token per (sequence, KV head).
+
+One timed step = the whole job on one batch: reskv_build_cache for all 32
+layers (from prefill K/V resident in HBM), then 256 decode steps, each of
+which runs reskv_append_kv + reskv_decode_attn for all 32 layers.
+value = decode tokens (batch x layers x decode steps) / step time.
+
+Also reported: decode-only throughput and HBM GB/s, construction GB/s, the
+roofline of the decode kernels (algorithmic bytes per call / average call
+time from HIP events on the launch stream), and the fp64 oracle's throughput
+on the host cores over a bounded sample of the same job.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=2, help="index of the synthetic workload (2 = batched decode)")
+    ap.add_argument("--decode-steps", type=int, default=None, help="override decode steps per job (testing only)")
+    ap.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=25.0)
+    ap.add_argument("--mode", choices=["job", "decode"], default="job",
+                    help="job: the timed whole job (default); decode: build once, then only decode calls "
+                         "(for rocprofv3 counter runs), preceded by one 256 MiB plain copy used to calibrate "
+                         "the byte counters")
+    return ap.parse_args()
+
+
+def decode_call_bytes(B, Hq, Hkv, d, elem, r, main_len):
+    """Algorithmic HBM bytes of one decode call: every live K and V slot once,
+    the residual log-counts, the queries and the fp32 outputs."""
+    slots = int((r + main_len).sum())
+    return slots * 2 * d * elem + 4 * int(r.sum()) + B * Hq * d * elem + B * Hq * d * 4
+
+
+def build_call_bytes(wl, elem, res):
+    """Algorithmic bytes of one construction call: prefill K and V read once,
+    window queries, the written cache rows, log-counts and main indices."""
+    B, Hkv, d = wl.batch, wl.hkv, wl.d
+    kv = sum(2 * wl.ctx[b] * d * elem * Hkv for b in range(B))
+    q = B * wl.hq * wl.window * d * elem
+    out = 0
+    for b in range(B):
+        for h in range(Hkv):
+            r = int(res[b][h])
+            m = min(wl.budget[b] - r, wl.ctx[b])
+            out += (r + m) * 2 * d * elem + 4 * r + 4 * m
+    return kv + q + out
+
+
+def source_hash(*paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(src_hash):
+    """HBM bytes per decode call measured by rocprofv3 counters, if the
+    committed measurement was taken on the current decode source."""
+    path = os.path.join(ROOT, "profiles", "decode_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("decode_source_sha256_16") != src_hash:
+        return None
+    return rec.get("bytes_per_call")
+
+
+def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
+    """Time the fp64 oracle on a bounded sample of the job on the host and
+    extrapolate to the whole job: one (sequence, KV head) of construction
+    (scores + selection, then Lloyd, whose cost grows with r) and one decode
+    layer-step for every query head of every sequence."""
+    import numpy as np
+    import torch
+    from oracle import reskv_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max(int(i.get("num_threads", 1)) for i in threadpool_info()) if threadpool_info() else 1
+    except Exception:
+        blas_threads = None
+    cores = len(os.sched_getaffinity(0))
+    B, Hkv, G, d = wl.batch, wl.hkv, wl.group, wl.d
+    # sample head: first (b=0, kv head) whose r is positive, smallest such r
+    r_row = res_layers[0][0]
+    cand = [h for h in range(Hkv) if r_row[h] > 0] or [0]
+    h = min(cand, key=lambda j: r_row[j])
+    r = int(r_row[h])
+    s = wl.ctx[0]
+    m = wl.budget[0] - r
+    K = x0["K"][0, h, :s].float().cpu().numpy().astype(np.float64)
+    V = x0["V"][0, h, :s].float().cpu().numpy().astype(np.float64)
+    Qw = x0["q_obs"][0, h * G:(h + 1) * G].float().cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    n = orc.scored_length(s, m, wl.window)
+    raw = orc.window_raw_scores(K, Qw)
+    sc = orc.pool5(raw[:n])
+    main, ev, seeds = orc.select_main(sc, s, m, wl.window, r)
+    t_score = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    if r > 0:
+        a, mu, _ = orc.lloyd(K[ev], K[seeds], wl.lloyd_iters)
+        orc.residual_entries(K[ev], V[ev], a, mu, r, d)
+    t_lloyd = time.perf_counter() - t0
+    per_center = t_lloyd / max(r, 1)
+    # decode: one layer-step, every (sequence, query head), on a cache of the
+    # decode shape (main rows drawn from the prefill, residual rows from means)
+    rng = np.random.default_rng(0)
+    n_main = m + wl.steps // 2
+    kc = np.zeros((B, Hkv, r + n_main, d))
+    vc = np.zeros_like(kc)
+    Kall = x0["K"][:, :, :n_main + r].float().cpu().numpy().astype(np.float64)
+    Vall = x0["V"][:, :, :n_main + r].float().cpu().numpy().astype(np.float64)
+    kc[:] = Kall
+    vc[:] = Vall
+    logc = np.log(rng.integers(1, 100, size=(B, Hkv, max(r, 1))).astype(np.float64))
+    res_len = np.full((B, Hkv), r)
+    main_len = np.full((B, Hkv), n_main)
+    q = q0.float().cpu().numpy().astype(np.float64)
+    tau = tau0.cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    orc.decode(q, kc, vc, logc, res_len, main_len, tau, wl.alpha, wl.g_min, wl.beta)
+    t_dec = time.perf_counter() - t0
+    # extrapolate to one job
+    job = 0.0
+    for l in range(wl.layers):
+        for b in range(B):
+            for hh in range(Hkv):
+                job += t_score + per_center * int(res_layers[l][b][hh])
+    job += t_dec * wl.layers * wl.steps
+    tokens = B * wl.layers * wl.steps
+    return dict(value=tokens / job, unit="tokens/s", cores=cores, blas_threads=blas_threads, kind="oracle",
+                sample=(f"fp64 numpy oracle on the host: construction of 1 (sequence, KV head) of layer 0 "
+                        f"(s={s}, r={r}: scoring+selection {t_score:.2f}s, Lloyd+summaries {t_lloyd:.2f}s) "
+                        f"and one decode layer-step for all {B}x{wl.hq} query heads ({t_dec:.2f}s); "
+                        f"extrapolated to the whole job ({job:.0f}s) with Lloyd cost scaled by r"),
+                seconds_measured=t_score + t_lloyd + t_dec)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "bench.py measures one GPU: the ResKV hot path here is built and timed on a "
+                                   "single MI355X; multi-GPU runs are not part of this build", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2607_29591_amd import reskv as rk
+    from paper_2607_29591_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    rk.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.workload(args.workload)
+    if args.decode_steps is not None:
+        wl.steps = args.decode_steps
+    if args.layers is not None:
+        wl.layers = args.layers
+        wl.res = wl.res[:args.layers]
+    L, B, Hq, Hkv, d = wl.layers, wl.batch, wl.hq, wl.hkv, wl.d
+    elem = 2 if wl.dtype == "bf16" else 4
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    C, Rcap, S = wl.slot_cap, wl.res_cap, wl.max_ctx
+    shape = rk.make_shape(B, Hq, Hkv, d, wl.dtype, C, Rcap)
+    params = rk.BuildParams(S, wl.window, wl.window, wl.lloyd_iters)
+
+    t_setup = time.perf_counter()
+    layers = []
+    for l in range(L):
+        x = synth.gen_layer_device(wl, l, dev)
+        layers.append(x)
+    q_stage = torch.stack([x["q_dec"] for x in layers])      # [L, steps, B, Hq, d]
+    kn_stage = torch.stack([x["k_new"] for x in layers])
+    vn_stage = torch.stack([x["v_new"] for x in layers])
+    tau_stage = torch.stack([x["tau"] for x in layers])       # [L, steps, B, Hq]
+    for x in layers:
+        del x["q_dec"], x["k_new"], x["v_new"], x["tau"]
+    caches = []
+    for l in range(L):
+        caches.append(dict(kc=torch.empty((B, Hkv, C, d), dtype=tdt, device=dev),
+                           vc=torch.empty((B, Hkv, C, d), dtype=tdt, device=dev),
+                           logc=torch.empty((B, Hkv, Rcap), device=dev),
+                           main_idx=torch.empty((B, Hkv, C), dtype=torch.int32, device=dev),
+                           res_len=torch.empty((B * Hkv,), dtype=torch.int32, device=dev),
+                           main_len=torch.empty((B * Hkv,), dtype=torch.int32, device=dev)))
+    res_layers = [np.asarray(wl.res[l], np.int32) for l in range(L)]
+    nws = max(rk.reskv_build_workspace_size(shape, params, layers[l]["seq_len"], layers[l]["budget"],
+                                            res_layers[l].reshape(-1)) for l in range(L))
+    build_ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    dec_ws = torch.empty(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device=dev)
+    out = torch.empty((B, Hq, d), device=dev)
+    gates = [[rk.make_gate(tau=tau_stage[l, t], alpha=wl.alpha, g_min=wl.g_min, beta=wl.beta)
+              for t in range(wl.steps)] for l in range(L)]
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t_setup
+
+    stream = torch.cuda.current_stream()
+    timed_steps = {wl.steps // 2, wl.steps - 1}
+    ev_pairs = []
+
+    def job(record):
+        eb0 = torch.cuda.Event(enable_timing=True)
+        eb1 = torch.cuda.Event(enable_timing=True)
+        eb0.record(stream)
+        for l in range(L):
+            x, c = layers[l], caches[l]
+            rk.reskv_build_cache(shape, params, x["K"], x["V"], x["seq_len"], x["q_obs"], x["budget"],
+                                 res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"], c["main_idx"],
+                                 c["res_len"], c["main_len"], build_ws)
+        eb1.record(stream)
+        for t in range(wl.steps):
+            for l in range(L):
+                c = caches[l]
+                rk.reskv_append_kv(shape, kn_stage[l, t], vn_stage[l, t], c["kc"], c["vc"], c["res_len"],
+                                   c["main_len"])
+                if record and t in timed_steps:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
+                                         c["res_len"], c["main_len"], out, dec_ws)
+                    e1.record(stream)
+                    ev_pairs.append((l, t, e0, e1))
+                else:
+                    rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
+                                         c["res_len"], c["main_len"], out, dec_ws)
+        ed = torch.cuda.Event(enable_timing=True)
+        ed.record(stream)
+        return eb0, eb1, ed
+
+    if args.mode == "decode":
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)                      # plain copy kernel: 256 MiB read + 256 MiB written
+        torch.cuda.synchronize()
+        for l in range(L):
+            x, c = layers[l], caches[l]
+            rk.reskv_build_cache(shape, params, x["K"], x["V"], x["seq_len"], x["q_obs"], x["budget"],
+                                 res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"], c["main_idx"],
+                                 c["res_len"], c["main_len"], build_ws)
+        for t in range(args.steps):
+            for l in range(L):
+                c = caches[l]
+                rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
+                                     c["res_len"], c["main_len"], out, dec_ws)
+        torch.cuda.synchronize()
+        r0 = res_layers[0].astype(np.int64)
+        m0 = np.minimum(np.asarray(wl.budget)[:, None] - r0, np.asarray(wl.ctx)[:, None])
+        print(json.dumps({"mode": "decode", "layers": L, "steps": args.steps,
+                          "bytes_per_call_layer0": decode_call_bytes(B, Hq, Hkv, d, elem, r0, m0),
+                          "copy_bytes_each_way": 256 << 20}), flush=True)
+        return
+
+    for _ in range(args.warmup):
+        job(False)
+    torch.cuda.synchronize()
+    phase = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        phase.append(job(True))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1000 / args.steps
+    build_ms = sum(a.elapsed_time(b) for a, b, _ in phase) / args.steps
+    decode_ms = sum(b.elapsed_time(c) for _, b, c in phase) / args.steps
+
+    # algorithmic bytes
+    build_bytes = sum(build_call_bytes(wl, elem, res_layers[l]) for l in range(L))
+    dec_bytes_job = 0
+    call_bytes = {}
+    for l in range(L):
+        r = res_layers[l].astype(np.int64)
+        m0 = np.minimum(np.asarray(wl.budget)[:, None] - r, np.asarray(wl.ctx)[:, None])
+        for t in range(wl.steps):
+            ml = np.minimum(m0 + t + 1, C - r)
+            nb = decode_call_bytes(B, Hq, Hkv, d, elem, r, ml) + 2 * B * Hkv * d * elem * 2  # + append r/w
+            dec_bytes_job += nb
+            if t in timed_steps:
+                call_bytes[(l, t)] = decode_call_bytes(B, Hq, Hkv, d, elem, r, ml)
+    tokens = B * L * wl.steps
+    # decode roofline from the per-call events
+    durs = [(call_bytes[(l, t)], e0.elapsed_time(e1)) for (l, t, e0, e1) in ev_pairs]
+    avg_ms = sum(ms for _, ms in durs) / len(durs)
+    avg_bytes = sum(b for b, _ in durs) / len(durs)
+    achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
+    src = source_hash("paper_2607_29591_amd/csrc/decode.hip", "paper_2607_29591_amd/csrc/common.h")
+    traffic = traffic_from_profile(src)
+
+    result = {
+        "metric": "decode attn tokens/s (batch x layers)",
+        "value": tokens / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded; LLM-shaped keys with outlier channels and heavy tokens)",
+        "config": {"workload": (f"batched decode: {L} layers x (Hq {Hq} / Hkv {Hkv}, head_dim {d}), batch {B}, "
+                                f"context {wl.ctx[0]} -> budget {wl.budget[0]} per KV head, residual r per "
+                                f"(layer, head) in {{0,64,128,256,512}}, {wl.steps} decode steps with appends; "
+                                f"step = construction of all layers + all decode steps"),
+                   "global_batch": B, "seq_len": wl.ctx[0], "layers": L, "decode_steps": wl.steps,
+                   "budget": wl.budget[0], "parallelism": "single GPU"},
+        "decode_tokens_per_s": tokens / (decode_ms * 1e-3),
+        "decode_ms_per_job": decode_ms,
+        "decode_gbs": dec_bytes_job / (decode_ms * 1e-3) / 1e9,
+        "build_ms_per_layer": build_ms / L,
+        "build_gbs": build_bytes / (build_ms * 1e-3) / 1e9,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "reskv_decode_attn (decode_split + decode_combine)",
+                     "bytes_per_call": avg_bytes, "us_per_call": avg_ms * 1e3,
+                     "calls_timed": len(durs)},
+        "setup_s": t_setup,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, layers[0], q_stage[0, 0], tau_stage[0, 0], res_layers,
+                                              args.cpu_budget_s)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -184,13 +184,13 @@ def gen_layer(wl, layer=0, seed=SEED, n_decode=None):
 # torch generator (device): full-size workloads generated in HBM
 # --------------------------------------------------------------------------
 
-def gen_layer_device(wl, layer, device, seed=SEED, n_decode=None, heads_out=None):
+def gen_layer_device(wl, layer, device, seed=SEED, n_decode=None, out=None):
     """Device tensors for one layer, drawn with a seeded device generator.
 
     Same recipe and layout as gen_layer, stored in the workload dtype
-    (torch.bfloat16 or torch.float32). If `heads_out` is a list of (b, kvh)
-    pairs, the host copies of those heads' inputs are also returned for the
-    checker under "host".
+    (torch.bfloat16 or torch.float32), vectorised over the KV heads of each
+    sequence. `out` may hold preallocated K, V (rows past a sequence's length
+    are left as they are: nothing reads them).
     """
     import torch
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
@@ -199,40 +199,49 @@ def gen_layer_device(wl, layer, device, seed=SEED, n_decode=None, heads_out=None
     steps = wl.steps if n_decode is None else n_decode
     gen = torch.Generator(device=device)
     gen.manual_seed(int(np.random.SeedSequence([seed, layer, 31337]).generate_state(1)[0]))
-    K = torch.zeros((B, Hkv, S, d), dtype=tdt, device=device)
-    V = torch.zeros((B, Hkv, S, d), dtype=tdt, device=device)
+    f32 = dict(dtype=torch.float32, device=device, generator=gen)
+    out = {} if out is None else out
+    K = out.get("K")
+    V = out.get("V")
+    if K is None:
+        K = torch.empty((B, Hkv, S, d), dtype=tdt, device=device)
+        V = torch.empty((B, Hkv, S, d), dtype=tdt, device=device)
     q_obs = torch.empty((B, wl.hq, w, d), dtype=tdt, device=device)
     q_dec = torch.empty((steps, B, wl.hq, d), dtype=tdt, device=device)
     k_new = torch.empty((steps, B, Hkv, d), dtype=tdt, device=device)
     v_new = torch.empty((steps, B, Hkv, d), dtype=tdt, device=device)
-    f32 = dict(dtype=torch.float32, device=device, generator=gen)
+
+    def queries(hk, n):
+        # [Hkv, G, n, d]: 0.7 * mean of 4 distinct heavy keys + 0.3 * N(0, 1)
+        nh = hk.shape[1]
+        pick = torch.rand((Hkv, G, n, nh), **f32).argsort(dim=-1)[..., :min(4, nh)]
+        src = hk[:, None, None].expand(Hkv, G, n, nh, d)
+        sel = torch.gather(src, 3, pick[..., None].expand(*pick.shape, d))
+        return 0.7 * sel.mean(dim=3) + 0.3 * torch.randn((Hkv, G, n, d), **f32)
+
     for b in range(B):
         s = int(wl.ctx[b])
         nh = max(1, min(int(wl.n_heavy[b]), s))
-        for h in range(Hkv):
-            ch = torch.randperm(d, generator=gen, device=device)[:4]
-            bias = torch.zeros(d, dtype=torch.float32, device=device)
-            bias[ch] = 3.0 * torch.randn(4, **f32)
-            kh = torch.randn((s, d), **f32) + bias
-            heavy = torch.randperm(s, generator=gen, device=device)[:nh]
-            kh[heavy] *= 3.0
-            kh = kh.to(tdt)
-            K[b, h, :s] = kh
-            V[b, h, :s] = torch.randn((s, d), **f32).to(tdt)
-            hk = kh[heavy].float()                       # [nh, d]
-            npick = min(4, nh)
-            for g in range(G):
-                for dst, n in ((q_obs[b, h * G + g], w), (q_dec[:, b, h * G + g], steps)):
-                    pick = torch.argsort(torch.rand((n, nh), **f32), dim=1)[:, :npick]
-                    qv = 0.7 * hk[pick].mean(dim=1) + 0.3 * torch.randn((n, d), **f32)
-                    dst.copy_(qv.to(tdt))
-            k_new[:, b, h] = (torch.randn((steps, d), **f32) + bias).to(tdt)
-            v_new[:, b, h] = torch.randn((steps, d), **f32).to(tdt)
+        ch = torch.rand((Hkv, d), **f32).argsort(dim=-1)[:, :4]
+        bias = torch.zeros((Hkv, d), dtype=torch.float32, device=device)
+        bias.scatter_(1, ch, 3.0 * torch.randn((Hkv, 4), **f32))
+        kh = torch.randn((Hkv, s, d), **f32) + bias[:, None, :]
+        heavy = torch.rand((Hkv, s), **f32).argsort(dim=-1)[:, :nh]
+        idx = heavy[:, :, None].expand(Hkv, nh, d)
+        kh.scatter_(1, idx, kh.gather(1, idx) * 3.0)
+        khs = kh.to(tdt)
+        del kh
+        K[b, :, :s] = khs
+        V[b, :, :s] = torch.randn((Hkv, s, d), **f32).to(tdt)
+        hk = khs.gather(1, idx).float()
+        q_obs[b] = queries(hk, w).reshape(Hkv * G, w, d).to(tdt)
+        q_dec[:, b] = queries(hk, steps).permute(2, 0, 1, 3).reshape(steps, Hkv * G, d).to(tdt)
+        k_new[:, b] = (torch.randn((steps, Hkv, d), **f32) + bias).to(tdt)
+        v_new[:, b] = torch.randn((steps, Hkv, d), **f32).to(tdt)
     if wl.tau == "normal":
         tau = 0.5 * torch.randn((steps, B, wl.hq), **f32)
     else:
         tau = torch.full((steps, B, wl.hq), float(wl.tau), dtype=torch.float32, device=device)
-    out = dict(K=K, V=V, q_obs=q_obs, q_dec=q_dec, k_new=k_new, v_new=v_new, tau=tau,
-               seq_len=np.asarray(wl.ctx, np.int32), budget=np.asarray(wl.budget, np.int32),
-               res=np.asarray(wl.res[layer], np.int32))
-    return out
+    return dict(K=K, V=V, q_obs=q_obs, q_dec=q_dec, k_new=k_new, v_new=v_new, tau=tau,
+                seq_len=np.asarray(wl.ctx, np.int32), budget=np.asarray(wl.budget, np.int32),
+                res=np.asarray(wl.res[layer], np.int32))
