@@ -146,6 +146,9 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
  *   q               [B, Hq, d]       this step's queries
  *   kc, vc, logc    cache as written by reskv_build_cache / reskv_append_kv
  *   res_len, main_len  [B*Hkv] int32, read on the device
+ *   k_new, v_new    [B, Hkv, d] optional (both or neither): this step's
+ *                   token, appended as by reskv_append_kv before attending
+ *                   (kc, vc and main_len are then written)
  *   out             [B, Hq, d] fp32
  *   dbg_lse_main    [B*Hq] optional: log sum_p e^{a_p}
  *   dbg_lse_res     [B*Hq] optional: log sum_j e^{<q,kbar_j>/sqrt(d) + beta logc_j}
@@ -159,10 +162,11 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
 reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
                                  const reskv_gate_t* gate,
                                  const void* q,
-                                 const void* kc, const void* vc,
+                                 void* kc, void* vc,
                                  const float* logc,
                                  const int32_t* res_len,
-                                 const int32_t* main_len,
+                                 int32_t* main_len,
+                                 const void* k_new, const void* v_new,
                                  float* out,
                                  float* dbg_lse_main, float* dbg_lse_res,
                                  float* dbg_gate,

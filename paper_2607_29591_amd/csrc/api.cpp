@@ -82,8 +82,9 @@ size_t reskv_decode_workspace_size(const reskv_shape_t* shape) {
 }
 
 reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
-                                 const void* kc, const void* vc, const float* logc,
-                                 const int32_t* res_len, const int32_t* main_len, float* out,
+                                 void* kc, void* vc, const float* logc,
+                                 const int32_t* res_len, int32_t* main_len,
+                                 const void* k_new, const void* v_new, float* out,
                                  float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
                                  void* workspace, size_t workspace_bytes, void* stream) {
   reskv_status_t st = check_shape(shape);
@@ -91,14 +92,16 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t*
   if ((st = check_gate(gate)) != RESKV_OK) return st;
   if (!q || !kc || !vc || !logc || !res_len || !main_len || !out)
     return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return fail(RESKV_ERR_INVALID_ARG, "k_new and v_new must both be given or both be NULL");
   const DecodePlan plan = make_decode_plan(*shape);
   if ((size_t)plan.GP * plan.P * sizeof(float) > decode_max_lds_weights())
     return fail(RESKV_ERR_UNSUPPORTED, "%d split-K records per head do not fit the combine", plan.P);
   if (!workspace || workspace_bytes < plan.bytes)
     return fail(RESKV_ERR_WORKSPACE, "decode needs %zu workspace bytes, got %zu", plan.bytes,
                 workspace ? workspace_bytes : (size_t)0);
-  hipError_t e = launch_decode(*shape, *gate, plan, q, kc, vc, logc, res_len, main_len, out, dbg_lse_main,
-                               dbg_lse_res, dbg_gate, workspace, (hipStream_t)stream);
+  hipError_t e = launch_decode(*shape, *gate, plan, q, kc, vc, logc, res_len, main_len, k_new, v_new, out,
+                               dbg_lse_main, dbg_lse_res, dbg_gate, workspace, (hipStream_t)stream);
   if (e != hipSuccess) return fail(RESKV_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -33,6 +33,7 @@ constexpr int kWaves = 4;
 constexpr int kUnit = 64;              // slots per wave unit
 constexpr int kTiles = kUnit / 16;     // MFMA tiles per unit
 constexpr int kChunk = kWaves * kUnit; // slots per split block
+constexpr int kWholeHeadMin = 256;     // (b, kv head) pairs that fill the 256 CUs
 
 struct DecodeArgs {
   const void* q;
@@ -40,7 +41,9 @@ struct DecodeArgs {
   const void* vc;
   const float* logc;
   const int32_t* res_len;
-  const int32_t* main_len;
+  int32_t* main_len;
+  const void* k_new;  // fused append (decode_head only), or NULL
+  const void* v_new;
   float* part_acc;  // [B*Hkv][P][GP][D]
   float* part_ml;   // [B*Hkv][P][GP][2]  (m in base 2, l)
   const float* tau;
@@ -98,35 +101,43 @@ struct VRow<float> {
 };
 
 
-// Raw loads of one 64-slot unit for one lane.
+// Raw loads of one 64-slot unit for one lane: key fragments (+ log-counts)
+// and value-row chunks.
 template <typename T, int D>
-struct UnitRegs {
+struct KRegs {
+  typename QK<T, D>::KFrag k[kTiles];
+  float lc[kTiles];
+};
+template <typename T, int D>
+struct VRegs {
   static constexpr int CPR = D / 8;         // 8-column chunks per value row
   static constexpr int RP = 64 / CPR;       // rows covered by one wave-wide load
   static constexpr int NR = kUnit / RP;     // value rows per lane
-  typename QK<T, D>::KFrag k[kTiles];
   VRow<T> v[NR];
-  float lc[kTiles];
 };
 
-// Issue every load of unit [s0, s0 + nvalid); rows past the tail are clamped
-// to the unit's first row (their probabilities are zero).
+// Loads of unit [s0, s0 + nvalid); rows past the tail are clamped to the
+// unit's first row (their probabilities are zero).
 template <typename T, int D>
-__device__ __forceinline__ void load_unit(UnitRegs<T, D>& u, const T* kc, const T* vc, const float* logc,
-                                          bool is_res, int s0, int nvalid, int col, int grp, int c, int ph) {
+__device__ __forceinline__ void load_unit_k(KRegs<T, D>& u, const T* kc, const float* logc, bool is_res, int s0,
+                                            int nvalid, int col, int grp) {
 #pragma unroll
   for (int t = 0; t < kTiles; ++t) {
     const int row = (16 * t + col < nvalid) ? s0 + 16 * t + col : s0;
     QK<T, D>::load_k(u.k[t], kc + (size_t)row * D + grp * (D / 4));
   }
 #pragma unroll
-  for (int k = 0; k < UnitRegs<T, D>::NR; ++k) {
-    const int j = ph + UnitRegs<T, D>::RP * k;
-    u.v[k].load(vc + (size_t)(s0 + min(j, nvalid - 1)) * D + 8 * c);
-  }
-#pragma unroll
   for (int t = 0; t < kTiles; ++t)
     u.lc[t] = (is_res && 16 * t + col < nvalid) ? logc[s0 + 16 * t + col] : 0.f;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void load_unit_v(VRegs<T, D>& u, const T* vc, int s0, int nvalid, int c, int ph) {
+#pragma unroll
+  for (int k = 0; k < VRegs<T, D>::NR; ++k) {
+    const int j = ph + VRegs<T, D>::RP * k;
+    u.v[k].load(vc + (size_t)(s0 + min(j, nvalid - 1)) * D + 8 * c);
+  }
 }
 
 // Online-softmax state of one wave for one kind.
@@ -144,13 +155,17 @@ struct WaveState {
   }
 };
 
+// One unit: logits on MFMA, then (once the key fragments are consumed) the
+// value loads, then the online softmax update and P.V.
 template <typename T, int D, int GP>
-__device__ __forceinline__ void process_unit(const UnitRegs<T, D>& u, const QK<T, D>& qk, WaveState<GP>& st,
-                                             float (*s_p)[GP], float* s_alpha, bool is_res, int nvalid,
-                                             float qk_scale, float beta_log2, int col, int grp, int c, int ph) {
+__device__ __forceinline__ void process_unit(const KRegs<T, D>& u, VRegs<T, D>& vr, const QK<T, D>& qk,
+                                             WaveState<GP>& st, float (*s_p)[GP], float* s_alpha, bool is_res,
+                                             int nvalid, float qk_scale, float beta_log2, int col, int grp, int c,
+                                             int ph, const T* vc, int s0) {
   f32x4_t s[kTiles];
 #pragma unroll
   for (int t = 0; t < kTiles; ++t) s[t] = qk.run(u.k[t]);
+  load_unit_v<T, D>(vr, vc, s0, nvalid, c, ph);
 #pragma unroll
   for (int t = 0; t < kTiles; ++t) {
     const bool live = 16 * t + col < nvalid;
@@ -206,10 +221,10 @@ __device__ __forceinline__ void process_unit(const UnitRegs<T, D>& u, const QK<T
 #pragma unroll
     for (int e = 0; e < 8; ++e) st.acc[h][e] *= al[h];
 #pragma unroll
-  for (int k = 0; k < UnitRegs<T, D>::NR; ++k) {
-    const int j = ph + UnitRegs<T, D>::RP * k;
+  for (int k = 0; k < VRegs<T, D>::NR; ++k) {
+    const int j = ph + VRegs<T, D>::RP * k;
     float v[8];
-    u.v[k].widen(v);
+    vr.v[k].widen(v);
     float pr[GP];
 #pragma unroll
     for (int h = 0; h < GP; ++h) pr[h] = s_p[j][h];
@@ -225,7 +240,7 @@ __device__ __forceinline__ void process_unit(const UnitRegs<T, D>& u, const QK<T
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
-  using Regs = UnitRegs<T, D>;
+  using Regs = VRegs<T, D>;
   const int p = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   int r, n;
@@ -259,11 +274,12 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
     QK<T, D> qk;
     qk.load_q(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + col) * D + grp * (D / 4),
               col < a.G);
-    Regs u;
+    KRegs<T, D> kr;
+    VRegs<T, D> vr;
     const int nvalid = min(kUnit, end - s0);
-    load_unit<T, D>(u, kc, vc, logc, is_res, s0, nvalid, col, grp, c, ph);
-    process_unit<T, D, GP>(u, qk, st, s_p[wave], s_alpha[wave], is_res, nvalid, a.qk_scale, a.beta_log2, col,
-                           grp, c, ph);
+    load_unit_k<T, D>(kr, kc, logc, is_res, s0, nvalid, col, grp);
+    process_unit<T, D, GP>(kr, vr, qk, st, s_p[wave], s_alpha[wave], is_res, nvalid, a.qk_scale, a.beta_log2,
+                           col, grp, c, ph, vc, s0);
   }
   // wave state -> LDS: sum the row phases of acc, keep max and sum per head
 #pragma unroll
@@ -391,6 +407,139 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
   }
 }
 
+
+// One block of 16 waves per (b, kv head): streams every slot of the head,
+// merges the wave states in LDS, applies the gate and writes the G outputs;
+// optionally appends this step's token first. Used when the (b, kv head)
+// pairs alone fill the GPU, so no split-K records or second launch are needed.
+// 8 waves (2 per SIMD, up to 256 registers each): every variant that needed
+// more registers (a second key buffer for prefetch, or 12-16 waves) spilled
+// to scratch and ran 1.5-3x slower.
+constexpr int kHeadWaves = 8;
+constexpr int kHeadThreads = 64 * kHeadWaves;
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
+  using Regs = VRegs<T, D>;
+  const int kvh = blockIdx.x, b = blockIdx.y;
+  const int bh = b * a.Hkv + kvh;
+  int r, n;
+  cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int c = lane % Regs::CPR, ph = lane / Regs::CPR;
+  T* kc = static_cast<T*>(const_cast<void*>(a.kc)) + (size_t)bh * a.C * D;
+  T* vc = static_cast<T*>(const_cast<void*>(a.vc)) + (size_t)bh * a.C * D;
+  const float* logc = a.logc + (size_t)bh * a.Rcap;
+
+  // fused append of this step's token as main slot r + n (Sec. 3.1)
+  const bool app = a.k_new != nullptr && r + n < a.C;
+  if (app) {
+    const T* kn = static_cast<const T*>(a.k_new) + (size_t)bh * D;
+    const T* vn = static_cast<const T*>(a.v_new) + (size_t)bh * D;
+    for (int x = tid; x < D; x += kHeadThreads) {
+      kc[(size_t)(r + n) * D + x] = kn[x];
+      vc[(size_t)(r + n) * D + x] = vn[x];
+    }
+  }
+  __syncthreads();  // the appended row is visible to every wave of the block
+  if (app) n += 1;
+
+  __shared__ float s_p[kHeadWaves][kUnit][GP];
+  __shared__ float s_alpha[kHeadWaves][GP];
+  __shared__ float s_acc[kHeadWaves][GP][D];
+  __shared__ float s_m[kHeadWaves][GP];
+  __shared__ float s_l[kHeadWaves][GP];
+  __shared__ float s_res[GP][D + 2];  // merged residual state: acc[D], m, l
+
+  QK<T, D> qk;
+  qk.load_q(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + col) * D + grp * (D / 4),
+            col < a.G);
+
+  for (int kind = 0; kind < 2; ++kind) {
+    const bool is_res = kind == 0;
+    const int base = is_res ? 0 : r;
+    const int end = is_res ? r : r + n;
+    const int U = (end - base + kUnit - 1) / kUnit;
+    WaveState<GP> st;
+    st.reset();
+    for (int u = wave; u < U; u += kHeadWaves) {  // wave-uniform
+      const int s0 = base + u * kUnit;
+      const int nvalid = min(kUnit, end - s0);
+      KRegs<T, D> kr;
+      VRegs<T, D> vr;
+      load_unit_k<T, D>(kr, kc, logc, is_res, s0, nvalid, col, grp);
+      process_unit<T, D, GP>(kr, vr, qk, st, s_p[wave], s_alpha[wave], is_res, nvalid, a.qk_scale, a.beta_log2,
+                             col, grp, c, ph, vc, s0);
+    }
+#pragma unroll
+    for (int msk = Regs::CPR; msk < 64; msk <<= 1)
+#pragma unroll
+      for (int h = 0; h < GP; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) st.acc[h][e] = wave_xor_add(st.acc[h][e], msk);
+    if (ph == 0) {
+#pragma unroll
+      for (int h = 0; h < GP; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s_acc[wave][h][8 * c + e] = st.acc[h][e];
+    }
+    if (col == 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int h = 4 * grp + i;
+        if (h < GP) {
+          s_m[wave][h] = st.m[i];
+          s_l[wave][h] = st.l[i];
+        }
+      }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < GP * D; idx += kHeadThreads) {
+      const int h = idx / D, d = idx % D;
+      float M = s_m[0][h];
+#pragma unroll
+      for (int w = 1; w < kHeadWaves; ++w) M = fmaxf(M, s_m[w][h]);
+      float o = 0.f, l = 0.f;
+      if (M != kNegInf) {
+#pragma unroll
+        for (int w = 0; w < kHeadWaves; ++w) {
+          const float f = exp2f(s_m[w][h] - M);
+          o = fmaf(f, s_acc[w][h][d], o);
+          l = fmaf(f, s_l[w][h], l);
+        }
+      }
+      if (is_res) {
+        s_res[h][d] = o;
+        if (d == 0) { s_res[h][D] = M; s_res[h][D + 1] = l; }
+        continue;
+      }
+      if (h >= a.G) continue;
+      // main merged: p_max = 1 / l (the max term is exactly 1), then the gate
+      const float pmax = l > 0.f ? 1.f / l : 1.f;
+      const int qh = b * a.Hq + kvh * a.G + h;
+      const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
+      const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
+      const float lg2g = g > 0.f ? log2f(g) : kNegInf;
+      const float mR = s_res[h][D], lR = s_res[h][D + 1];
+      const float mRg = (mR == kNegInf || lg2g == kNegInf) ? kNegInf : mR + lg2g;
+      const float Mx = fmaxf(M, mRg);
+      const float fM = M != kNegInf ? exp2f(M - Mx) : 0.f;
+      const float fR = mRg != kNegInf ? exp2f(mRg - Mx) : 0.f;
+      const float den = l * fM + lR * fR;
+      const float num = o * fM + s_res[h][d] * fR;
+      a.out[(size_t)qh * D + d] = den > 0.f ? num / den : 0.f;
+      if (d == 0) {
+        if (a.dbg_lse_main) a.dbg_lse_main[qh] = l > 0.f ? (M + log2f(l)) * kLn2 : kNegInf;
+        if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
+        if (a.dbg_gate) a.dbg_gate[qh] = g;
+      }
+    }
+    __syncthreads();
+  }
+  if (app && tid == 0) a.main_len[bh] = n;
+}
+
 template <typename T, int D>
 __global__ void append_kernel(const T* k_new, const T* v_new, T* kc, T* vc, const int32_t* res_len,
                               int32_t* main_len, int C) {
@@ -410,6 +559,12 @@ __global__ void append_kernel(const T* k_new, const T* v_new, T* kc, T* vc, cons
 
 template <typename T, int D, int GP>
 hipError_t launch_typed(const DecodePlan& pl, const DecodeArgs& da, hipStream_t stream) {
+  if constexpr (GP <= 4) {
+    if (pl.whole_head) {
+      hipLaunchKernelGGL((decode_head<T, D, GP>), dim3(pl.Hkv, pl.B), dim3(kHeadThreads), 0, stream, da);
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL((decode_split<T, D, GP>), dim3(pl.P, pl.Hkv, pl.B), dim3(kThreads), 0, stream, da);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -441,6 +596,8 @@ DecodePlan make_decode_plan(const reskv_shape_t& s) {
   const int rmax = s.res_cap < s.slot_cap ? s.res_cap : s.slot_cap;
   p.PR = (rmax + kChunk - 1) / kChunk;
   p.P = p.PR + (s.slot_cap + kChunk - 1) / kChunk;
+  // one block per (b, kv head) when those alone fill the chip's CUs
+  p.whole_head = p.GP <= 4 && (long long)p.B * p.Hkv >= kWholeHeadMin;
   const size_t recs = (size_t)p.B * p.Hkv * p.P * p.GP;
   p.acc_off = 0;
   p.ml_off = align_up(recs * p.D * sizeof(float), 256);
@@ -451,12 +608,17 @@ DecodePlan make_decode_plan(const reskv_shape_t& s) {
 size_t decode_max_lds_weights() { return 48 * 1024; }
 
 hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& pl,
-                         const void* q, const void* kc, const void* vc, const float* logc,
-                         const int32_t* res_len, const int32_t* main_len, float* out,
-                         float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
+                         const void* q, void* kc, void* vc, const float* logc,
+                         const int32_t* res_len, int32_t* main_len, const void* k_new, const void* v_new,
+                         float* out, float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
                          void* workspace, hipStream_t stream) {
   char* ws = static_cast<char*>(workspace);
+  if (k_new && !pl.whole_head) {  // split-K path: append as its own launch first
+    const hipError_t e = launch_append(s, k_new, v_new, kc, vc, res_len, main_len, stream);
+    if (e != hipSuccess) return e;
+  }
   DecodeArgs da{};
+  if (pl.whole_head) { da.k_new = k_new; da.v_new = v_new; }
   da.q = q; da.kc = kc; da.vc = vc; da.logc = logc;
   da.res_len = res_len; da.main_len = main_len;
   da.part_acc = reinterpret_cast<float*>(ws + pl.acc_off);

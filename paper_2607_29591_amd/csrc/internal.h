@@ -12,6 +12,7 @@ namespace reskv {
 struct DecodePlan {
   int B, Hq, Hkv, G, GP, D, C, Rcap;
   int PR, P;  // residual blocks and all blocks of the split grid per (b, kv head)
+  bool whole_head;  // one block per (b, kv head), no split-K records
   size_t acc_off, ml_off, bytes;
 };
 
@@ -21,9 +22,9 @@ size_t decode_max_lds_weights();
 DecodePlan make_decode_plan(const reskv_shape_t& s);
 
 hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& plan,
-                         const void* q, const void* kc, const void* vc, const float* logc,
-                         const int32_t* res_len, const int32_t* main_len, float* out,
-                         float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
+                         const void* q, void* kc, void* vc, const float* logc,
+                         const int32_t* res_len, int32_t* main_len, const void* k_new, const void* v_new,
+                         float* out, float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
                          void* workspace, hipStream_t stream);
 
 hipError_t launch_append(const reskv_shape_t& s, const void* k_new, const void* v_new, void* kc,

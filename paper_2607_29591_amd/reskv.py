@@ -53,7 +53,7 @@ _SIG = {
     "reskv_build_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
                                                      _P, _P, _P]),
     "reskv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
-                                         _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+                                         _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_decode_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape)]),
     "reskv_append_kv": (ctypes.c_int, [ctypes.POINTER(Shape), _P, _P, _P, _P, _P, _P, _P]),
     "reskv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -135,10 +135,10 @@ def reskv_decode_workspace_size(shape):
 
 
 def reskv_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, workspace,
-                      dbg_lse_main=None, dbg_lse_res=None, dbg_gate=None, stream=None):
+                      dbg_lse_main=None, dbg_lse_res=None, dbg_gate=None, k_new=None, v_new=None, stream=None):
     _check(lib().reskv_decode_attn(ctypes.byref(shape), ctypes.byref(gate), _ptr(q), _ptr(kc), _ptr(vc),
-                                   _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(out), _ptr(dbg_lse_main),
-                                   _ptr(dbg_lse_res), _ptr(dbg_gate), _ptr(workspace),
+                                   _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(k_new), _ptr(v_new), _ptr(out),
+                                   _ptr(dbg_lse_main), _ptr(dbg_lse_res), _ptr(dbg_gate), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
 
 

@@ -32,8 +32,19 @@ def to_dev(x, dtype):
     return (t.to(torch.bfloat16) if dtype == "bf16" else t).cuda().contiguous()
 
 
-def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None):
-    """Build one layer on the GPU; returns host numpy copies of every output."""
+class HostView:
+    """Host float64 copies of slices of a device tensor, made on indexing."""
+
+    def __init__(self, t):
+        self.t = t
+
+    def __getitem__(self, idx):
+        return self.t[idx].float().cpu().numpy().astype(np.float64)
+
+
+def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=False, host_cache=True):
+    """Build one layer on the GPU; returns host numpy copies of the outputs
+    (and the device tensors under "dev" when keep_device is set)."""
     B, Hkv, d = wl.batch, wl.hkv, wl.d
     S = x["K"].shape[2]
     C, Rcap = wl.slot_cap, wl.res_cap
@@ -59,9 +70,15 @@ def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None):
     rk.reskv_build_cache(shape, params, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc, main_idx,
                          res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
     torch.cuda.synchronize()
-    out = dict(kc=kc.float().cpu().numpy().astype(np.float64), vc=vc.float().cpu().numpy().astype(np.float64),
-               logc=logc.cpu().numpy().astype(np.float64), main_idx=main_idx.cpu().numpy(),
+    out = dict(logc=logc.cpu().numpy().astype(np.float64), main_idx=main_idx.cpu().numpy(),
                res_len=res_len.cpu().numpy().reshape(B, Hkv), main_len=main_len.cpu().numpy().reshape(B, Hkv))
+    if host_cache:
+        out["kc"] = kc.float().cpu().numpy().astype(np.float64)
+        out["vc"] = vc.float().cpu().numpy().astype(np.float64)
+    else:
+        out["kc"], out["vc"] = HostView(kc), HostView(vc)
+    if keep_device:
+        out["dev"] = dict(kc=kc, vc=vc, logc=logc, res_len=res_len, main_len=main_len, main_idx=main_idx)
     if dbg:
         out["scores"] = dbg_s.cpu().numpy().astype(np.float64)
         out["assign"] = dbg_a.cpu().numpy()

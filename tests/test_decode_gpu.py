@@ -166,3 +166,57 @@ def test_append_then_decode(dtype):
     np.testing.assert_array_equal(ml.cpu().numpy().reshape(B, Hkv), main2)
     np.testing.assert_array_equal(kcd.double().cpu().numpy(), kc2)
     check(dtype, shape, q, kc2, vc2, logc, res, main2)
+
+
+@pytest.mark.parametrize("dtype,d,G,B,Hkv", [("bf16", 128, 4, 32, 8), ("f32", 64, 2, 64, 4), ("bf16", 64, 1, 16, 16),
+                                             ("bf16", 128, 4, 2, 2), ("f32", 128, 7, 2, 2)])
+def test_decode_fused_append(dtype, d, G, B, Hkv):
+    """reskv_decode_attn with this step's K/V: the token is appended as main
+    slot r + n (cache and main_len written) and attended in the same call.
+    B*Hkv >= 256 with G <= 4 takes the one-block-per-head kernel; the others
+    the split-K kernels; full caches are left unchanged."""
+    rng = np.random.default_rng(11 + d + G)
+    C, Rcap = 300, 64
+    res = rng.choice([0, 16, 64], size=(B, Hkv))
+    main = rng.integers(1, C - 64, size=(B, Hkv))
+    main[0, 0] = C - res[0, 0]  # full: no append
+    shape, q, kc, vc, logc = cache_case(20 + d, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+    kn = rng.normal(size=(B, Hkv, d))
+    vn = rng.normal(size=(B, Hkv, d))
+    knd, vnd = to_dev(kn, dtype), to_dev(vn, dtype)
+    kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
+    lcd = torch.as_tensor(logc.astype(np.float32)).cuda()
+    rl = torch.as_tensor(res.astype(np.int32).reshape(-1)).cuda()
+    ml = torch.as_tensor(main.astype(np.int32).reshape(-1)).cuda()
+    qd = to_dev(q, dtype)
+    out = torch.empty((B, G * Hkv, d), device="cuda")
+    ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    rk.reskv_decode_attn(shape, rk.make_gate(), qd, kcd, vcd, lcd, rl, ml, out, ws, k_new=knd, v_new=vnd)
+    torch.cuda.synchronize()
+    kc2, vc2, main2 = kc.copy(), vc.copy(), main.copy()
+    for b in range(B):
+        for h in range(Hkv):
+            slot = res[b, h] + main[b, h]
+            if slot < C:
+                kc2[b, h, slot] = knd[b, h].double().cpu().numpy()
+                vc2[b, h, slot] = vnd[b, h].double().cpu().numpy()
+                main2[b, h] += 1
+    np.testing.assert_array_equal(ml.cpu().numpy().reshape(B, Hkv), main2)
+    np.testing.assert_array_equal(kcd.double().cpu().numpy(), kc2)
+    np.testing.assert_array_equal(vcd.double().cpu().numpy(), vc2)
+    ref, *_ = orc.decode(q, kc2, vc2, logc, res, main2, 0.25, 12.0, 0.0, 1.0)
+    assert rel_err_rows(out.double().cpu().numpy(), ref).max() <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 64), ("f32", 128)])
+def test_decode_whole_head_path_shapes(dtype, d):
+    """256 (b, kv head) pairs: the one-block-per-head kernel, with ragged
+    lengths, r = 0 heads and empty entries."""
+    B, Hkv, G = 64, 4, 4
+    rng = np.random.default_rng(30 + d)
+    C, Rcap = 700, 130
+    res = rng.choice([0, 1, 63, 130], size=(B, Hkv))
+    main = rng.integers(1, C - 130, size=(B, Hkv))
+    shape, q, kc, vc, logc = cache_case(40 + d, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+    heads = [(int(b), int(h)) for b, h in zip(rng.integers(0, B, 40), rng.integers(0, G * Hkv, 40))]
+    check(dtype, shape, q, kc, vc, logc, res, main, heads=heads)
