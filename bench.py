@@ -9,7 +9,8 @@ steps that each append one token per (sequence, KV head).
 
 One timed step = the whole job on one batch: reskv_build_cache for all 32
 layers (from prefill K/V resident in HBM), then 256 decode steps, each of
-which runs reskv_append_kv + reskv_decode_attn for all 32 layers.
+which runs reskv_decode_attn for all 32 layers with that step's token
+appended inside the call.
 value = decode tokens (batch x layers x decode steps) / step time.
 
 Also reported: decode-only throughput and HBM GB/s, construction GB/s, the
@@ -51,10 +52,13 @@ def parse():
 
 
 def decode_call_bytes(B, Hq, Hkv, d, elem, r, main_len):
-    """Algorithmic HBM bytes of one decode call: every live K and V slot once,
-    the residual log-counts, the queries and the fp32 outputs."""
+    """Algorithmic HBM bytes of one decode call with its fused append: every
+    live K and V slot once (the appended token included), the residual
+    log-counts, the queries, the fp32 outputs, and the appended token's K/V
+    read from its staging buffer."""
     slots = int((r + main_len).sum())
-    return slots * 2 * d * elem + 4 * int(r.sum()) + B * Hq * d * elem + B * Hq * d * 4
+    return (slots * 2 * d * elem + 4 * int(r.sum()) + B * Hq * d * elem + B * Hq * d * 4
+            + B * Hkv * 2 * d * elem)
 
 
 def build_call_bytes(wl, elem, res):
@@ -239,19 +243,18 @@ def main():
         for t in range(wl.steps):
             for l in range(L):
                 c = caches[l]
-                rk.reskv_append_kv(shape, kn_stage[l, t], vn_stage[l, t], c["kc"], c["vc"], c["res_len"],
-                                   c["main_len"])
-                if record and t in timed_steps:
+                timed = record and t in timed_steps
+                if timed:
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record(stream)
-                    rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
-                                         c["res_len"], c["main_len"], out, dec_ws)
+                # this step's token is appended inside the decode call
+                rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
+                                     c["res_len"], c["main_len"], out, dec_ws, k_new=kn_stage[l, t],
+                                     v_new=vn_stage[l, t])
+                if timed:
                     e1.record(stream)
                     ev_pairs.append((l, t, e0, e1))
-                else:
-                    rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
-                                         c["res_len"], c["main_len"], out, dec_ws)
         ed = torch.cuda.Event(enable_timing=True)
         ed.record(stream)
         return eb0, eb1, ed
@@ -270,12 +273,17 @@ def main():
             for l in range(L):
                 c = caches[l]
                 rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
-                                     c["res_len"], c["main_len"], out, dec_ws)
+                                     c["res_len"], c["main_len"], out, dec_ws, k_new=kn_stage[l, t],
+                                     v_new=vn_stage[l, t])
         torch.cuda.synchronize()
-        r0 = res_layers[0].astype(np.int64)
-        m0 = np.minimum(np.asarray(wl.budget)[:, None] - r0, np.asarray(wl.ctx)[:, None])
+        per_call = []
+        for l in range(L):
+            r0 = res_layers[l].astype(np.int64)
+            m0 = np.minimum(np.asarray(wl.budget)[:, None] - r0, np.asarray(wl.ctx)[:, None])
+            for t in range(args.steps):
+                per_call.append(decode_call_bytes(B, Hq, Hkv, d, elem, r0, np.minimum(m0 + t + 1, C - r0)))
         print(json.dumps({"mode": "decode", "layers": L, "steps": args.steps,
-                          "bytes_per_call_layer0": decode_call_bytes(B, Hq, Hkv, d, elem, r0, m0),
+                          "algorithmic_bytes_per_call": float(np.mean(per_call)),
                           "copy_bytes_each_way": 256 << 20}), flush=True)
         return
 
@@ -301,10 +309,10 @@ def main():
         m0 = np.minimum(np.asarray(wl.budget)[:, None] - r, np.asarray(wl.ctx)[:, None])
         for t in range(wl.steps):
             ml = np.minimum(m0 + t + 1, C - r)
-            nb = decode_call_bytes(B, Hq, Hkv, d, elem, r, ml) + 2 * B * Hkv * d * elem * 2  # + append r/w
+            nb = decode_call_bytes(B, Hq, Hkv, d, elem, r, ml)
             dec_bytes_job += nb
             if t in timed_steps:
-                call_bytes[(l, t)] = decode_call_bytes(B, Hq, Hkv, d, elem, r, ml)
+                call_bytes[(l, t)] = nb
     tokens = B * L * wl.steps
     # decode roofline from the per-call events
     durs = [(call_bytes[(l, t)], e0.elapsed_time(e1)) for (l, t, e0, e1) in ev_pairs]
@@ -340,7 +348,8 @@ def main():
         "build_gbs": build_bytes / (build_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "reskv_decode_attn (decode_split + decode_combine)",
+                     "kernel": "reskv_decode_attn (one launch per layer-step: decode_head, one block per "
+                               "(sequence, KV head), append fused)",
                      "bytes_per_call": avg_bytes, "us_per_call": avg_ms * 1e3,
                      "calls_timed": len(durs)},
         "setup_s": t_setup,
