@@ -3,8 +3,9 @@
 //
 // Per (b, kv head), in launch order:
 //   lse_partial    MFMA logits of the G*w observation-window rows against a
-//                  256-key chunk; per row the max and sum of exp (base 2) over
-//                  the keys it can see (causal inside the window)
+//                  256-key chunk (each wave owns 64 keys and runs over all
+//                  rows); per row the max and sum of exp (base 2) over the
+//                  keys it can see (causal inside the window)
 //   lse_final      merges the chunk partials into one log-sum-exp per row
 //   score_accum    recomputes the logits; raw[p] = sum over rows of the
 //                  normalised weight of key p, for the scored positions
@@ -41,8 +42,10 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kKeyChunk = 256;     // keys per scoring block (16 MFMA tiles)
-constexpr int kKeyTiles = kKeyChunk / 16;
-constexpr int kTokBlock = 256;     // evicted tokens per Lloyd block
+constexpr int kTokTiles = 4;       // 16-token MFMA tiles per wave in the assignment
+constexpr int kAssignWaves = 8;    // 2 waves per SIMD: one's argmin VALU overlaps the other's MFMAs
+constexpr int kAssignThreads = 64 * kAssignWaves;
+constexpr int kTokBlock = kAssignWaves * 16 * kTokTiles;  // evicted tokens per Lloyd block (512)
 constexpr int kCenterChunk = 64;   // centres staged in LDS per step
 constexpr int kSelThreads = 1024;
 
@@ -97,6 +100,10 @@ __device__ __forceinline__ void load_window_row(Frag<T, D>& f, const BuildArgs& 
 
 // ---------------------------------------------------------------- scoring
 
+// Each wave owns 64 keys of the block's 256-key chunk (its key fragments are
+// read once) and runs over every window row. The MFMA is oriented keys x rows,
+// C[key][row]: a lane holds 16 keys of one row, so a row's max and sum need
+// only two cross-lane steps.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -106,48 +113,58 @@ __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
   if (hm.all_main || k0 >= hm.s) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
+  __shared__ float2 s_ml[4][1024];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
-  Frag<T, D> kf[kKeyTiles];
+  const int kw = k0 + 64 * wave;  // this wave's first key
+  Frag<T, D> kf[4];
 #pragma unroll
-  for (int kt = 0; kt < kKeyTiles; ++kt) {
-    const int p = min(k0 + 16 * kt + col, hm.s - 1);
-    kf[kt].load(K + (size_t)p * D + grp * (D / 4));
+  for (int t = 0; t < 4; ++t) {
+    const int p = min(kw + 16 * t + col, hm.s - 1);
+    kf[t].load(K + (size_t)p * D + grp * (D / 4));
   }
   const int RT = (a.R + 15) / 16;
-  for (int rt = wave; rt < RT; rt += 4) {
+  for (int rt = 0; rt < RT; ++rt) {
+    const int t_row = 16 * rt + col;  // window row of this lane's column
     Frag<T, D> qf;
-    load_window_row<T, D>(qf, a, b, kvh, 16 * rt + col, grp);
-    f32x4_t sc[kKeyTiles];
+    load_window_row<T, D>(qf, a, b, kvh, t_row, grp);
+    const int pos = t_row < a.R ? hm.s - a.w + t_row % a.w : -1;
+    float v[16];
+    float m = kNegInf;
 #pragma unroll
-    for (int kt = 0; kt < kKeyTiles; ++kt) sc[kt] = mma<D>(qf, kf[kt], zero4());
-    float mx[4];
+    for (int t = 0; t < 4; ++t) {
+      const f32x4_t c = mma<D>(kf[t], qf, zero4());
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int t = 16 * rt + 4 * grp + i;
-      const int pos = hm.s - a.w + (t < a.R ? t % a.w : 0);
-      float m = kNegInf;
-#pragma unroll
-      for (int kt = 0; kt < kKeyTiles; ++kt) {
-        const int p = k0 + 16 * kt + col;
-        const float v = (p < hm.s && p <= pos) ? sc[kt][i] * a.scale2 : kNegInf;
-        sc[kt][i] = v;
-        m = fmaxf(m, v);
+      for (int i = 0; i < 4; ++i) {
+        const int p = kw + 16 * t + 4 * grp + i;
+        const float x = (p < hm.s && p <= pos) ? c[i] * a.scale2 : kNegInf;
+        v[4 * t + i] = x;
+        m = fmaxf(m, x);
       }
-      m = wave_xor_max(m, 1); m = wave_xor_max(m, 2);
-      m = wave_xor_max(m, 4); m = wave_xor_max(m, 8);
-      mx[i] = m;
     }
+    m = wave_xor_max(m, 16);
+    m = wave_xor_max(m, 32);
+    const float mu = m == kNegInf ? 0.f : m;
+    float l = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float mu = mx[i] == kNegInf ? 0.f : mx[i];
-      float l = 0.f;
+    for (int j = 0; j < 16; ++j) l += exp2f(v[j] - mu);
+    l = wave_xor_add(l, 16);
+    l = wave_xor_add(l, 32);
+    if (grp == 0 && t_row < a.R) s_ml[wave][t_row] = make_float2(m, l);
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < a.R; t += kThreads) {
+    float M = kNegInf;
 #pragma unroll
-      for (int kt = 0; kt < kKeyTiles; ++kt) l += exp2f(sc[kt][i] - mu);
-      l = wave_xor_add(l, 1); l = wave_xor_add(l, 2);
-      l = wave_xor_add(l, 4); l = wave_xor_add(l, 8);
-      const int t = 16 * rt + 4 * grp + i;
-      if (col == 0 && t < a.R) a.lse_part[((size_t)bh * a.NCH + ch) * a.R + t] = make_float2(mx[i], l);
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][t].x);
+    float L = 0.f;
+    if (M != kNegInf) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float2 e = s_ml[w][t];
+        if (e.x != kNegInf) L = fmaf(e.y, exp2f(e.x - M), L);
+      }
     }
+    a.lse_part[((size_t)bh * a.NCH + ch) * a.R + t] = make_float2(M, L);
   }
 }
 
@@ -169,6 +186,9 @@ __global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
   a.lse2[(size_t)bh * a.R + t] = M + log2f(L);
 }
 
+// Each wave owns 64 keys and runs over every window row; C[row][key]: a lane
+// holds one key of 4 rows, so the per-key sums stay in registers until two
+// final cross-lane steps, and no cross-wave merge is needed.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -178,20 +198,21 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
   if (hm.all_main || k0 >= hm.n_sc) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  __shared__ float s_raw[4][kKeyChunk];
+  __shared__ float s_lse[1024];
+  for (int t = threadIdx.x; t < a.R; t += kThreads) s_lse[t] = a.lse2[(size_t)bh * a.R + t];
+  __syncthreads();
+  const int kw = k0 + 64 * wave;
+  if (kw >= hm.n_sc) return;  // wave-uniform; no barrier follows
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
-  Frag<T, D> kf[kKeyTiles];
+  Frag<T, D> kf[4];
 #pragma unroll
-  for (int kt = 0; kt < kKeyTiles; ++kt) {
-    const int p = min(k0 + 16 * kt + col, hm.s - 1);
-    kf[kt].load(K + (size_t)p * D + grp * (D / 4));
+  for (int t = 0; t < 4; ++t) {
+    const int p = min(kw + 16 * t + col, hm.s - 1);
+    kf[t].load(K + (size_t)p * D + grp * (D / 4));
   }
-  float ksum[kKeyTiles];
-#pragma unroll
-  for (int kt = 0; kt < kKeyTiles; ++kt) ksum[kt] = 0.f;
+  float ksum[4] = {0.f, 0.f, 0.f, 0.f};
   const int RT = (a.R + 15) / 16;
-  const float* lse2 = a.lse2 + (size_t)bh * a.R;
-  for (int rt = wave; rt < RT; rt += 4) {
+  for (int rt = 0; rt < RT; ++rt) {
     Frag<T, D> qf;
     load_window_row<T, D>(qf, a, b, kvh, 16 * rt + col, grp);
     float lse[4];
@@ -199,30 +220,25 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = 16 * rt + 4 * grp + i;
-      lse[i] = t < a.R ? lse2[t] : 0.f;
+      lse[i] = t < a.R ? s_lse[t] : 0.f;
       pos[i] = t < a.R ? hm.s - a.w + t % a.w : -1;  // padded rows see no key
     }
 #pragma unroll
-    for (int kt = 0; kt < kKeyTiles; ++kt) {
-      const f32x4_t sc = mma<D>(qf, kf[kt], zero4());
-      const int p = k0 + 16 * kt + col;
+    for (int t = 0; t < 4; ++t) {
+      const f32x4_t c = mma<D>(qf, kf[t], zero4());
+      const int p = kw + 16 * t + col;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (p <= pos[i]) ksum[kt] += exp2f(fmaf(sc[i], a.scale2, -lse[i]));
+        if (p <= pos[i]) ksum[t] += exp2f(fmaf(c[i], a.scale2, -lse[i]));
     }
   }
 #pragma unroll
-  for (int kt = 0; kt < kKeyTiles; ++kt) {
-    float v = ksum[kt];
+  for (int t = 0; t < 4; ++t) {
+    float v = ksum[t];
     v = wave_xor_add(v, 16);
     v = wave_xor_add(v, 32);
-    if (grp == 0) s_raw[wave][16 * kt + col] = v;
-  }
-  __syncthreads();
-  const int p = k0 + threadIdx.x;
-  if (p < hm.n_sc) {
-    const float v = ((s_raw[0][threadIdx.x] + s_raw[1][threadIdx.x]) + s_raw[2][threadIdx.x]) + s_raw[3][threadIdx.x];
-    a.raw[(size_t)bh * a.S + p] = v;
+    const int p = kw + 16 * t + col;
+    if (grp == 0 && p < hm.n_sc) a.raw[(size_t)bh * a.S + p] = v;
   }
 }
 
@@ -472,10 +488,32 @@ struct CenterTile<float, D> {
   Frag<float, D> f;
 };
 
+// One MFMA k-step of a centre tile against one token tile (bf16: 8 elements,
+// fp32: 1 element per lane).
+template <int D>
+__device__ __forceinline__ f32x4_t mma_step(const Frag<uint16_t, D>& c, const Frag<uint16_t, D>& t, int k,
+                                            f32x4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(c.w[k]), as_bf16x8(t.w[k]), acc, 0, 0, 0);
+}
+template <int D>
+__device__ __forceinline__ f32x4_t mma_step(const Frag<float, D>& c, const Frag<float, D>& t, int k, f32x4_t acc) {
+  const float4 x = c.w[k >> 2], y = t.w[k >> 2];
+  const int e = k & 3;
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(e == 0 ? x.x : e == 1 ? x.y : e == 2 ? x.z : x.w,
+                                              e == 0 ? y.x : e == 1 ? y.y : e == 2 ? y.z : y.w, acc, 0, 0, 0);
+}
+
+// Assignment of kTokBlock evicted tokens (8 waves x kTokTiles x 16) to the
+// nearest centre: C[centre][token] = mu.k on MFMA with mu = hi + lo (bf16
+// pair) or fp32, dist = ||mu||^2 - 2 mu.k, argmin with ties to the lower
+// centre. The token tiles of a wave advance through each k-step together so
+// the MFMA chains are independent. Centres past r' are staged with an
+// infinite norm and never win.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void lloyd_assign(BuildArgs a, int iter) {
+__global__ __launch_bounds__(kAssignThreads) void lloyd_assign(BuildArgs a, int iter) {
   constexpr bool kBf = sizeof(T) == 2;
   constexpr int kRowB = kBf ? D * 2 + 16 : D * 4 + 16;   // padded LDS row bytes
+  constexpr int kSteps = kBf ? D / 32 : D / 4;           // MFMA k-steps over a quarter row
   const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
@@ -483,80 +521,112 @@ __global__ __launch_bounds__(kThreads) void lloyd_assign(BuildArgs a, int iter) 
   if (hm.r_eff == 0 || t0 >= hm.nE) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  // LDS: centre chunk (bf16: hi rows then lo rows; fp32: rows), norms, histogram
   __shared__ __align__(16) unsigned char s_c[kCenterChunk * kRowB * (kBf ? 2 : 1)];
   __shared__ float s_norm[kCenterChunk];
   extern __shared__ int s_hist[];  // [r_eff]
-  for (int j = tid; j < hm.r_eff; j += kThreads) s_hist[j] = 0;
+  for (int j = tid; j < hm.r_eff; j += kAssignThreads) s_hist[j] = 0;
 
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
   const int32_t* elist = a.elist + (size_t)bh * a.S;
-  Frag<T, D> tk[4];  // token tiles of this wave
+  const int tw = t0 + wave * 16 * kTokTiles;  // this wave's first token
+  Frag<T, D> tk[kTokTiles];
 #pragma unroll
-  for (int tt = 0; tt < 4; ++tt) {
-    const int i = min(t0 + wave * 64 + 16 * tt + col, hm.nE - 1);
+  for (int tt = 0; tt < kTokTiles; ++tt) {
+    const int i = min(tw + 16 * tt + col, hm.nE - 1);
     tk[tt].load(K + (size_t)elist[i] * D + grp * (D / 4));
   }
-  float best[4][4];
-  int bidx[4][4];
+  float best[kTokTiles][4];
+  int bidx[kTokTiles][4];
 #pragma unroll
-  for (int tt = 0; tt < 4; ++tt)
+  for (int tt = 0; tt < kTokTiles; ++tt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) { best[tt][i] = __builtin_huge_valf(); bidx[tt][i] = 0x7fffffff; }
 
   const size_t cbase = (size_t)bh * a.Rcap;
-  for (int j0 = 0; j0 < hm.r_eff; j0 += kCenterChunk) {
+  // centre chunks are staged through one LDS buffer; the next chunk's global
+  // loads are issued before this chunk's MFMAs and written after a barrier
+  constexpr int kPieces = (kBf ? D * 2 : D * 4) / 16;       // 16-byte pieces per row
+  constexpr int kPer = kCenterChunk * kPieces / kAssignThreads;   // pieces per thread
+  static_assert(kCenterChunk * kPieces % kAssignThreads == 0, "staging split");
+  uint4 ph[kPer], pl[kPer];
+  float pn = 0.f;
+  auto fetch = [&](int j0) {
     const int nj = min(kCenterChunk, hm.r_eff - j0);
-    __syncthreads();
-    // stage the chunk: 16-byte pieces
-    constexpr int kPieces = (kBf ? D * 2 : D * 4) / 16;
-    for (int x = tid; x < kCenterChunk * kPieces; x += kThreads) {
-      const int jj = x / kPieces, pc = x % kPieces;
-      uint4 hv = make_uint4(0, 0, 0, 0), lv = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int x = tid + u * kAssignThreads, jj = x / kPieces, pc = x % kPieces;
+      ph[u] = pl[u] = make_uint4(0, 0, 0, 0);
       if (jj < nj) {
         if (kBf) {
-          hv = reinterpret_cast<const uint4*>(a.cent_hi + (cbase + j0 + jj) * D)[pc];
-          lv = reinterpret_cast<const uint4*>(a.cent_lo + (cbase + j0 + jj) * D)[pc];
+          ph[u] = reinterpret_cast<const uint4*>(a.cent_hi + (cbase + j0 + jj) * D)[pc];
+          pl[u] = reinterpret_cast<const uint4*>(a.cent_lo + (cbase + j0 + jj) * D)[pc];
         } else {
-          hv = reinterpret_cast<const uint4*>(a.cent + (cbase + j0 + jj) * D)[pc];
+          ph[u] = reinterpret_cast<const uint4*>(a.cent + (cbase + j0 + jj) * D)[pc];
         }
       }
-      *reinterpret_cast<uint4*>(s_c + jj * kRowB + pc * 16) = hv;
-      if (kBf) *reinterpret_cast<uint4*>(s_c + (kCenterChunk + jj) * kRowB + pc * 16) = lv;
     }
-    for (int jj = tid; jj < kCenterChunk; jj += kThreads) s_norm[jj] = jj < nj ? a.cnorm[cbase + j0 + jj] : 0.f;
-    __syncthreads();
+    if (tid < kCenterChunk) pn = tid < nj ? a.cnorm[cbase + j0 + tid] : __builtin_huge_valf();
+  };
+  auto commit = [&]() {
 #pragma unroll
-    for (int ct = 0; ct < kCenterChunk / 16; ++ct) {
-      if (16 * ct >= nj) break;  // block-uniform
-      CenterTile<T, D> cf;
+    for (int u = 0; u < kPer; ++u) {
+      const int x = tid + u * kAssignThreads, jj = x / kPieces, pc = x % kPieces;
+      *reinterpret_cast<uint4*>(s_c + jj * kRowB + pc * 16) = ph[u];
+      if (kBf) *reinterpret_cast<uint4*>(s_c + (kCenterChunk + jj) * kRowB + pc * 16) = pl[u];
+    }
+    if (tid < kCenterChunk) s_norm[tid] = pn;
+  };
+  fetch(0);
+  commit();
+  for (int j0 = 0; j0 < hm.r_eff; j0 += kCenterChunk) {
+    const int nj = min(kCenterChunk, hm.r_eff - j0);
+    __syncthreads();  // the chunk in LDS is complete
+    if (j0 + kCenterChunk < hm.r_eff) fetch(j0 + kCenterChunk);
+    const int nct = (nj + 15) / 16;
+    for (int ct = 0; ct < nct; ++ct) {  // block-uniform
       const int crow = 16 * ct + col;
+      Frag<T, D> ch, cl;
       if constexpr (kBf) {
-        cf.hi.load(reinterpret_cast<const uint16_t*>(s_c + crow * kRowB) + grp * (D / 4));
-        cf.lo.load(reinterpret_cast<const uint16_t*>(s_c + (kCenterChunk + crow) * kRowB) + grp * (D / 4));
+        ch.load(reinterpret_cast<const uint16_t*>(s_c + crow * kRowB) + grp * (D / 4));
+        cl.load(reinterpret_cast<const uint16_t*>(s_c + (kCenterChunk + crow) * kRowB) + grp * (D / 4));
       } else {
-        cf.f.load(reinterpret_cast<const float*>(s_c + crow * kRowB) + grp * (D / 4));
+        ch.load(reinterpret_cast<const float*>(s_c + crow * kRowB) + grp * (D / 4));
+      }
+      f32x4_t acc[kTokTiles];
+#pragma unroll
+      for (int tt = 0; tt < kTokTiles; ++tt) acc[tt] = zero4();
+#pragma unroll
+      for (int k = 0; k < kSteps; ++k)
+#pragma unroll
+        for (int tt = 0; tt < kTokTiles; ++tt) acc[tt] = mma_step<D>(ch, tk[tt], k, acc[tt]);
+      if constexpr (kBf) {
+#pragma unroll
+        for (int k = 0; k < kSteps; ++k)
+#pragma unroll
+          for (int tt = 0; tt < kTokTiles; ++tt) acc[tt] = mma_step<D>(cl, tk[tt], k, acc[tt]);
       }
       float nrm[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) nrm[i] = s_norm[16 * ct + 4 * grp + i];
+      const int jb = j0 + 16 * ct + 4 * grp;
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        f32x4_t dot;
-        if constexpr (kBf) dot = mma<D>(cf.lo, tk[tt], mma<D>(cf.hi, tk[tt], zero4()));
-        else dot = mma<D>(cf.f, tk[tt], zero4());
+      for (int tt = 0; tt < kTokTiles; ++tt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int j = j0 + 16 * ct + 4 * grp + i;
-          const float dist = fmaf(-2.f, dot[i], nrm[i]);
-          if (j < hm.r_eff && dist < best[tt][i]) { best[tt][i] = dist; bidx[tt][i] = j; }
+          const float dist = fmaf(-2.f, acc[tt][i], nrm[i]);
+          const bool win = dist < best[tt][i];
+          best[tt][i] = win ? dist : best[tt][i];
+          bidx[tt][i] = win ? jb + i : bidx[tt][i];
         }
-      }
+    }
+    if (j0 + kCenterChunk < hm.r_eff) {  // block-uniform
+      __syncthreads();  // every wave is done with this chunk
+      commit();
     }
   }
   // argmin over the 16 centres of a lane (4 rows x 4 lane groups): ties to lower index
 #pragma unroll
-  for (int tt = 0; tt < 4; ++tt) {
+  for (int tt = 0; tt < kTokTiles; ++tt) {
     float bv = best[tt][0];
     int bi = bidx[tt][0];
 #pragma unroll
@@ -569,7 +639,7 @@ __global__ __launch_bounds__(kThreads) void lloyd_assign(BuildArgs a, int iter) 
       if (ov < bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
     }
     if (bi >= hm.r_eff) bi = 0;  // only reachable with non-finite keys
-    const int i = t0 + wave * 64 + 16 * tt + col;
+    const int i = tw + 16 * tt + col;
     if (grp == 0 && i < hm.nE) {
       a.assign[(size_t)bh * a.S + i] = bi;
       atomicAdd(&s_hist[bi], 1);
@@ -578,7 +648,7 @@ __global__ __launch_bounds__(kThreads) void lloyd_assign(BuildArgs a, int iter) 
   }
   __syncthreads();
   int32_t* hist = a.hist + ((size_t)bh * a.NBLK + blk) * a.Rcap;
-  for (int j = tid; j < hm.r_eff; j += kThreads) hist[j] = s_hist[j];
+  for (int j = tid; j < hm.r_eff; j += kAssignThreads) hist[j] = s_hist[j];
 }
 
 // Group sizes and counting-sort offsets: hist[blk][j] becomes the first
@@ -614,7 +684,7 @@ __global__ __launch_bounds__(kThreads) void lloyd_offsets(BuildArgs a) {
 }
 
 // Stable placement: members of a group keep ascending evicted order.
-__global__ __launch_bounds__(kThreads) void lloyd_scatter(BuildArgs a) {
+__global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
   const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
@@ -657,10 +727,22 @@ __global__ __launch_bounds__(kThreads) void lloyd_update(BuildArgs a, int last) 
     double acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-    for (int q = g; q < cnt; q += NG) {
-      const T* row = X + (size_t)mem[q] * D + 8 * c;
+    // members g, g + NG, g + 2NG, ... in order; four 16-byte row loads in flight
+    int q = g;
+    for (; q + 3 * NG < cnt; q += 4 * NG) {
+      float x[4][8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (double)to_f32(row[e]);
+      for (int u = 0; u < 4; ++u) load8_f32(X + (size_t)mem[q + u * NG] * D + 8 * c, x[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += (double)x[u][e];
+    }
+    for (; q < cnt; q += NG) {
+      float x[8];
+      load8_f32(X + (size_t)mem[q] * D + 8 * c, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += (double)x[e];
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) s_sum[g][8 * c + e] = acc[e];
@@ -754,9 +836,10 @@ hipError_t launch_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st)
     hipLaunchKernelGGL((center_prep<D>), grid(pl.max_reff), dim3(kThreads), 0, st, a); RESKV_CHECK();
     const size_t hist_lds = (size_t)pl.max_reff * sizeof(int);
     for (int it = 0; it < pl.T; ++it) {
-      hipLaunchKernelGGL((lloyd_assign<T, D>), grid(pl.NBLK), dim3(kThreads), hist_lds, st, a, it); RESKV_CHECK();
+      hipLaunchKernelGGL((lloyd_assign<T, D>), grid(pl.NBLK), dim3(kAssignThreads), hist_lds, st, a, it);
+      RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
-      hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kThreads), 0, st, a); RESKV_CHECK();
+      hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), 0, st, a); RESKV_CHECK();
       hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, it == pl.T - 1 ? 1 : 0);
       RESKV_CHECK();
     }
