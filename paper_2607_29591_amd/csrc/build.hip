@@ -91,8 +91,8 @@ template <typename T, int D>
 __device__ __forceinline__ void load_window_row(Frag<T, D>& f, const BuildArgs& a, int b, int kvh, int t, int grp) {
   if (t < a.R) {
     const int h = t / a.w, i = t % a.w;
-    const T* q = static_cast<const T*>(a.q_obs) + (((size_t)b * a.Hq + kvh * a.G + h) * a.w + i) * D + grp * (D / 4);
-    f.load(q);
+    const T* q = static_cast<const T*>(a.q_obs) + (((size_t)b * a.Hq + kvh * a.G + h) * a.w + i) * D;
+    f.load(q, grp);
   } else {
     f.zero();
   }
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int p = min(kw + 16 * t + col, hm.s - 1);
-    kf[t].load(K + (size_t)p * D + grp * (D / 4));
+    kf[t].load(K + (size_t)p * D, grp);
   }
   const int RT = (a.R + 15) / 16;
   for (int rt = 0; rt < RT; ++rt) {
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int p = min(kw + 16 * t + col, hm.s - 1);
-    kf[t].load(K + (size_t)p * D + grp * (D / 4));
+    kf[t].load(K + (size_t)p * D, grp);
   }
   float ksum[4] = {0.f, 0.f, 0.f, 0.f};
   const int RT = (a.R + 15) / 16;
@@ -513,7 +513,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(kAssignThreads) void lloyd_assign(BuildArgs a, int iter) {
   constexpr bool kBf = sizeof(T) == 2;
   constexpr int kRowB = kBf ? D * 2 + 16 : D * 4 + 16;   // padded LDS row bytes
-  constexpr int kSteps = kBf ? D / 32 : D / 4;           // MFMA k-steps over a quarter row
+  constexpr int kSteps = kBf ? D / 32 : D / 4;           // MFMA k-steps over the lane's share of a row
   const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
@@ -533,7 +533,7 @@ __global__ __launch_bounds__(kAssignThreads) void lloyd_assign(BuildArgs a, int 
 #pragma unroll
   for (int tt = 0; tt < kTokTiles; ++tt) {
     const int i = min(tw + 16 * tt + col, hm.nE - 1);
-    tk[tt].load(K + (size_t)elist[i] * D + grp * (D / 4));
+    tk[tt].load(K + (size_t)elist[i] * D, grp);
   }
   float best[kTokTiles][4];
   int bidx[kTokTiles][4];
@@ -587,10 +587,10 @@ __global__ __launch_bounds__(kAssignThreads) void lloyd_assign(BuildArgs a, int 
       const int crow = 16 * ct + col;
       Frag<T, D> ch, cl;
       if constexpr (kBf) {
-        ch.load(reinterpret_cast<const uint16_t*>(s_c + crow * kRowB) + grp * (D / 4));
-        cl.load(reinterpret_cast<const uint16_t*>(s_c + (kCenterChunk + crow) * kRowB) + grp * (D / 4));
+        ch.load(reinterpret_cast<const uint16_t*>(s_c + crow * kRowB), grp);
+        cl.load(reinterpret_cast<const uint16_t*>(s_c + (kCenterChunk + crow) * kRowB), grp);
       } else {
-        ch.load(reinterpret_cast<const float*>(s_c + crow * kRowB) + grp * (D / 4));
+        ch.load(reinterpret_cast<const float*>(s_c + crow * kRowB), grp);
       }
       f32x4_t acc[kTokTiles];
 #pragma unroll

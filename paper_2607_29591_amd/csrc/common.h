@@ -56,15 +56,42 @@ __device__ __forceinline__ float wave_xor_add(float v, int mask) {
   return v + __shfl_xor(v, mask, 64);
 }
 
+// Reductions over the 16 lanes of one DPP row (lanes 16g .. 16g+15) with DPP
+// moves: swap neighbours, swap pairs, mirror within 8, mirror within 16. Each
+// step combines a lane with a partner that holds the same partial set size,
+// and fp32 add and max are commutative, so all 16 lanes end with the same
+// bits.
+template <int Ctrl>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), Ctrl, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_move<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_move<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_move<0x141>(v));  // row_half_mirror
+  return fmaxf(v, dpp_move<0x140>(v));  // row_mirror
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_move<0xB1>(v);
+  v += dpp_move<0x4E>(v);
+  v += dpp_move<0x141>(v);
+  return v + dpp_move<0x140>(v);
+}
+
+// 2^x on the hardware exponential unit (no denormal rescaling); 2^-inf = 0.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ int clampi(int x, int lo, int hi) {
   return x < lo ? lo : (x > hi ? hi : x);
 }
 
 // ---- 16x16 MFMA tiles over a full row of D elements ------------------------
 // C[16 x 16] = A[16 x D] . B[16 x D]^T. Lane l supplies A row (l % 16) and B
-// row (l % 16), both restricted to the quarter [(l/16)*D/4, (l/16+1)*D/4) of
-// the row; the contraction over D is split into MFMA k-steps inside that
-// quarter (the same split for A and B, so the sum covers every element once).
+// row (l % 16); lane group g = l / 16 takes the 16-byte pieces g, g + 4,
+// g + 8, ... of the row, so that one load instruction of the wave reads 64
+// contiguous bytes of each of 16 rows (whole cache segments). The MFMA k-steps
+// walk those pieces in the same order for A and B, so the sum covers every
+// element of the row once.
 // Result layout: lane l holds C[4*(l/16) + i][l % 16] for i = 0..3.
 template <typename T, int D>
 struct Frag;
@@ -73,9 +100,9 @@ template <int D>
 struct Frag<uint16_t, D> {        // bf16: 16x16x32 steps, 8 elements per step
   static constexpr int kSteps = D / 32;
   uint4 w[kSteps];
-  __device__ __forceinline__ void load(const uint16_t* quarter) {
+  __device__ __forceinline__ void load(const uint16_t* row, int grp) {
 #pragma unroll
-    for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const uint4*>(quarter + 8 * i);
+    for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const uint4*>(row + 8 * grp + 32 * i);
   }
   __device__ __forceinline__ void zero() {
 #pragma unroll
@@ -87,9 +114,9 @@ template <int D>
 struct Frag<float, D> {           // fp32: 16x16x4 steps, 1 element per step
   static constexpr int kSteps = D / 16;  // float4 groups
   float4 w[kSteps];
-  __device__ __forceinline__ void load(const float* quarter) {
+  __device__ __forceinline__ void load(const float* row, int grp) {
 #pragma unroll
-    for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const float4*>(quarter + 4 * i);
+    for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const float4*>(row + 4 * grp + 16 * i);
   }
   __device__ __forceinline__ void zero() {
 #pragma unroll

@@ -1,26 +1,37 @@
 // Shared-softmax residual decode (Sec. 5.4; Sec. 5.5.2 gate; App. D, Algorithm 2).
 //
-// Split-K flash decode over the fixed-budget cache of one layer, in two
-// launches:
-//   decode_split   one block = 256 slots of one (b, kv head), all of one kind
-//                  (residual slots [0, r) or main slots [r, r+n)), one 64-slot
-//                  unit per wave; it writes the block's partial record (max
-//                  m, sum l, unnormalised acc) per query head of the group.
-//                  Logits are kept in base 2, with log2(e)/sqrt(d) folded
-//                  into one scale.
-//   decode_combine one block per (b, kv head): the main records give
-//                  p_max = 1 / l_main (the max term contributes exactly 1),
-//                  the gate follows, the residual records are shifted by
-//                  log g, and main and residual share one denominator.
+// Flash decode over the fixed-budget cache of one layer. Two shapes:
+//   decode_head    one block of 8 waves per (b, kv head) streams every slot
+//                  of the head, merges the waves in LDS, applies the gate
+//                  and writes the outputs (used when the (b, kv head) pairs
+//                  alone fill the GPU); it can append this step's token.
+//   decode_split + decode_combine
+//                  split-K: one block = 256 slots of one (b, kv head), all of
+//                  one kind (residual slots [0, r) or main slots [r, r+n)),
+//                  writes a partial record (max m, sum l, unnormalised acc)
+//                  per query head; the combine merges the main records
+//                  (p_max = 1 / l_main: the max term contributes exactly 1),
+//                  evaluates the gate, shifts the residual records by log g
+//                  and gives main and residual one shared denominator.
 // The combine is a separate launch rather than a last-arriving-block epilogue:
 // on this multi-XCD part a device-scope release/acquire per block writes back
 // and invalidates L2, which costs far more than one more launch.
 //
-// Per unit: Q.K^T on MFMA (16 heads x 16 slots per tile; 16x16x32 bf16 or
-// 16x16x4 f32), each lane fetching one quarter of a key row with 16-byte
-// loads; the per-head max/sum is a 16-lane butterfly; probabilities and the
-// rescale factors pass through LDS (wave-private rows) to the P.V stage, which
-// widens 16-byte value loads and accumulates in fp32 registers.
+// One wave handles a unit of 64 slots entirely in registers. With
+// hd = lane % 16 and g = lane / 16:
+//   * logits S^T = K Q^T on MFMA per 16-slot tile t (A = key rows, B = query
+//     rows), so lane (hd, g) holds S[slot 16t + 4g + i][head hd], i = 0..3;
+//     logits are kept in base 2 with log2(e)/sqrt(d) folded into one scale;
+//   * the per-head max and sum run over the lane's 16 values, then across
+//     the four lane groups;
+//   * O^T += V^T P^T on MFMA: lane (m, g) loads the m-th (D/16)-element piece
+//     of value rows 16T + 4g + u, which is exactly the A operand when the
+//     MFMA contraction index k = 8g + i' stands for slot
+//     16(2h + i'/4) + 4g + i'%4 (k-step h); the B operand is then the lane's
+//     own probabilities. bf16 probabilities are split into hi + lo bf16 parts
+//     (two MFMAs), fp32 caches use the fp32 MFMA. Lane (hd, g) ends with
+//     O[head hd][columns g*D/4 .. (g+1)*D/4), so rescaling by the per-head
+//     alpha and the final write need no cross-lane traffic.
 #include "common.h"
 #include "internal.h"
 
@@ -31,7 +42,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kUnit = 64;              // slots per wave unit
-constexpr int kTiles = kUnit / 16;     // MFMA tiles per unit
+constexpr int kTiles = kUnit / 16;     // 16-slot MFMA tiles per unit
 constexpr int kChunk = kWaves * kUnit; // slots per split block
 constexpr int kWholeHeadMin = 256;     // (b, kv head) pairs that fill the 256 CUs
 
@@ -63,184 +74,211 @@ __device__ __forceinline__ void cache_lengths(const int32_t* res_len, const int3
   n = clampi(main_len[bh], 0, C - r);
 }
 
-// ---- Q.K^T on MFMA: C[head][slot] for 16 heads x 16 slots ------------------
-// A operand = query head (lane % 16), B operand = key row of slot (lane % 16).
+// Raw words of one value-row piece (D/16 elements) of one lane.
 template <typename T, int D>
-struct QK {
-  using KFrag = Frag<T, D>;
-  Frag<T, D> q;
-  __device__ void load_q(const T* qrow, bool live) {
-    if (live) q.load(qrow); else q.zero();
-  }
-  __device__ static void load_k(KFrag& f, const T* krow) { f.load(krow); }
-  __device__ f32x4_t run(const KFrag& f) const { return mma<D>(q, f, zero4()); }
-};
-
-// 8 consecutive value-row elements, loaded raw and widened later.
-template <typename T>
-struct VRow;
-template <>
-struct VRow<uint16_t> {
-  uint4 w;
-  __device__ void load(const uint16_t* p) { w = *reinterpret_cast<const uint4*>(p); }
-  __device__ void widen(float (&x)[8]) const {
-    x[0] = bf16_lo(w.x); x[1] = bf16_hi(w.x); x[2] = bf16_lo(w.y); x[3] = bf16_hi(w.y);
-    x[4] = bf16_lo(w.z); x[5] = bf16_hi(w.z); x[6] = bf16_lo(w.w); x[7] = bf16_hi(w.w);
-  }
-};
-template <>
-struct VRow<float> {
-  float4 a, b;
-  __device__ void load(const float* p) {
-    a = *reinterpret_cast<const float4*>(p);
-    b = *reinterpret_cast<const float4*>(p + 4);
-  }
-  __device__ void widen(float (&x)[8]) const {
-    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-  }
-};
-
-
-// Raw loads of one 64-slot unit for one lane: key fragments (+ log-counts)
-// and value-row chunks.
-template <typename T, int D>
-struct KRegs {
-  typename QK<T, D>::KFrag k[kTiles];
-  float lc[kTiles];
-};
-template <typename T, int D>
-struct VRegs {
-  static constexpr int CPR = D / 8;         // 8-column chunks per value row
-  static constexpr int RP = 64 / CPR;       // rows covered by one wave-wide load
-  static constexpr int NR = kUnit / RP;     // value rows per lane
-  VRow<T> v[NR];
-};
-
-// Loads of unit [s0, s0 + nvalid); rows past the tail are clamped to the
-// unit's first row (their probabilities are zero).
-template <typename T, int D>
-__device__ __forceinline__ void load_unit_k(KRegs<T, D>& u, const T* kc, const float* logc, bool is_res, int s0,
-                                            int nvalid, int col, int grp) {
+struct VPiece {
+  static constexpr int kElems = D / 16;
+  static constexpr int kWords = kElems * (int)sizeof(T) / 4;
+  uint32_t w[kWords];
+  __device__ __forceinline__ void load(const T* p) {
+    if constexpr (kWords == 2) {
+      const uint2 x = *reinterpret_cast<const uint2*>(p);
+      w[0] = x.x; w[1] = x.y;
+    } else {
 #pragma unroll
-  for (int t = 0; t < kTiles; ++t) {
-    const int row = (16 * t + col < nvalid) ? s0 + 16 * t + col : s0;
-    QK<T, D>::load_k(u.k[t], kc + (size_t)row * D + grp * (D / 4));
+      for (int j = 0; j < kWords / 4; ++j) {
+        const uint4 x = reinterpret_cast<const uint4*>(p)[j];
+        w[4 * j] = x.x; w[4 * j + 1] = x.y; w[4 * j + 2] = x.z; w[4 * j + 3] = x.w;
+      }
+    }
+  }
+};
+
+// Key fragments (+ log-counts) and value pieces of one 64-slot unit.
+template <typename T, int D>
+struct UnitRegs {
+  Frag<T, D> k[kTiles];    // key row 16t + hd
+  float lc[kTiles][4];     // log-count of slot 16t + 4g + i (residual units)
+  VPiece<T, D> v[16];      // v[4T + u]: piece hd of value row 16T + 4g + u
+};
+
+// Loads of unit [s0, s0 + nvalid); rows past the tail are clamped into the
+// unit (their probabilities are zero). Slot app_row (or none if -1) is taken
+// from the token being appended (kn / vn) instead of the cache: the unit that
+// holds it (wave-uniform test) reloads the lanes that read that row.
+template <typename T, int D>
+__device__ __forceinline__ void load_unit_k(UnitRegs<T, D>& u, const T* kc, const float* logc, bool is_res,
+                                            int s0, int nvalid, int hd, int g, int app_row, const T* kn) {
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t) u.k[t].load(kc + (size_t)(s0 + min(16 * t + hd, nvalid - 1)) * D, g);
+  if (app_row >= s0 && app_row < s0 + nvalid) {
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+      if (s0 + min(16 * t + hd, nvalid - 1) == app_row) u.k[t].load(kn, g);
   }
 #pragma unroll
   for (int t = 0; t < kTiles; ++t)
-    u.lc[t] = (is_res && 16 * t + col < nvalid) ? logc[s0 + 16 * t + col] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = 16 * t + 4 * g + i;
+      u.lc[t][i] = (is_res && j < nvalid) ? logc[s0 + j] : 0.f;
+    }
 }
 
 template <typename T, int D>
-__device__ __forceinline__ void load_unit_v(VRegs<T, D>& u, const T* vc, int s0, int nvalid, int c, int ph) {
+__device__ __forceinline__ void load_unit_v(UnitRegs<T, D>& u, const T* vc, int s0, int nvalid, int hd, int g,
+                                            int app_row, const T* vn) {
+  constexpr int kE = VPiece<T, D>::kElems;
 #pragma unroll
-  for (int k = 0; k < VRegs<T, D>::NR; ++k) {
-    const int j = ph + VRegs<T, D>::RP * k;
-    u.v[k].load(vc + (size_t)(s0 + min(j, nvalid - 1)) * D + 8 * c);
+  for (int T4 = 0; T4 < 4; ++T4)
+#pragma unroll
+    for (int uu = 0; uu < 4; ++uu)
+      u.v[4 * T4 + uu].load(vc + (size_t)(s0 + min(16 * T4 + 4 * g + uu, nvalid - 1)) * D + kE * hd);
+  if (app_row >= s0 && app_row < s0 + nvalid) {
+#pragma unroll
+    for (int T4 = 0; T4 < 4; ++T4)
+#pragma unroll
+      for (int uu = 0; uu < 4; ++uu)
+        if (s0 + min(16 * T4 + 4 * g + uu, nvalid - 1) == app_row) u.v[4 * T4 + uu].load(vn + kE * hd);
   }
 }
 
-// Online-softmax state of one wave for one kind.
-template <int GP>
+// Online-softmax state of one wave for one kind: head hd's running max and
+// sum (replicated over the four lane groups) and O^T tiles (lane (hd, g)
+// holds O[hd][(D/16)(4g + i) + e] in acc[e][i]).
+template <int D>
 struct WaveState {
-  float m[4], l[4];   // per head 4*grp + i (replicated over the 16 lanes of a group)
-  float acc[GP][8];   // per head, 8 columns of this lane's chunk, this lane's row phase
+  static constexpr int kE = D / 16;
+  float m, l;
+  f32x4_t acc[kE];
   __device__ void reset() {
+    m = kNegInf;
+    l = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) { m[i] = kNegInf; l[i] = 0.f; }
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+    for (int e = 0; e < kE; ++e) acc[e] = zero4();
   }
 };
+
+// bf16 halves of two fp32 values packed into one word (a low, b high),
+// truncating; perm selector 0x07060302 takes the upper halves of both.
+__device__ __forceinline__ uint32_t pack_hi(float a, float b) {
+  return __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+}
+__device__ __forceinline__ float trunc_bf16(float x) { return __uint_as_float(__float_as_uint(x) & 0xffff0000u); }
+
+// P.V of one unit: O^T tiles += V^T P^T (see the file comment for the
+// slot order of the contraction index).
+template <int D>
+__device__ __forceinline__ void pv_unit(WaveState<D>& st, const UnitRegs<uint16_t, D>& u, const float (&p)[kTiles][4]) {
+  constexpr int kE = D / 16;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    // B operands: probabilities of slots 16(2h + i'/4) + 4g + i'%4, i' = 0..7,
+    // as bf16 hi and lo parts
+    uint32_t bh[4], bl[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float pa = p[2 * h + (2 * w) / 4][(2 * w) % 4];
+      const float pb = p[2 * h + (2 * w + 1) / 4][(2 * w + 1) % 4];
+      bh[w] = pack_hi(pa, pb);
+      bl[w] = pack_hi(pa - trunc_bf16(pa), pb - trunc_bf16(pb));
+    }
+    const bf16x8_t Bh = __builtin_bit_cast(bf16x8_t, make_uint4(bh[0], bh[1], bh[2], bh[3]));
+    const bf16x8_t Bl = __builtin_bit_cast(bf16x8_t, make_uint4(bl[0], bl[1], bl[2], bl[3]));
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+      // A operand: element e of value rows 8h + i', packed in pairs
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+      uint32_t av[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        av[w] = __builtin_amdgcn_perm(u.v[8 * h + 2 * w + 1].w[e >> 1], u.v[8 * h + 2 * w].w[e >> 1], sel);
+      const bf16x8_t A = __builtin_bit_cast(bf16x8_t, make_uint4(av[0], av[1], av[2], av[3]));
+      st.acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Bh, st.acc[e], 0, 0, 0);
+      st.acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, Bl, st.acc[e], 0, 0, 0);
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void pv_unit(WaveState<D>& st, const UnitRegs<float, D>& u, const float (&p)[kTiles][4]) {
+  constexpr int kE = D / 16;
+#pragma unroll
+  for (int T4 = 0; T4 < 4; ++T4)
+#pragma unroll
+    for (int uu = 0; uu < 4; ++uu)
+#pragma unroll
+      for (int e = 0; e < kE; ++e)
+        st.acc[e] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(u.v[4 * T4 + uu].w[e]), p[T4][uu],
+                                                         st.acc[e], 0, 0, 0);
+}
 
 // One unit: logits on MFMA, then (once the key fragments are consumed) the
-// value loads, then the online softmax update and P.V.
-template <typename T, int D, int GP>
-__device__ __forceinline__ void process_unit(const KRegs<T, D>& u, VRegs<T, D>& vr, const QK<T, D>& qk,
-                                             WaveState<GP>& st, float (*s_p)[GP], float* s_alpha, bool is_res,
-                                             int nvalid, float qk_scale, float beta_log2, int col, int grp, int c,
-                                             int ph, const T* vc, int s0) {
+// value loads, the online softmax update and P.V.
+template <typename T, int D>
+__device__ __forceinline__ void process_unit(UnitRegs<T, D>& u, const Frag<T, D>& q, WaveState<D>& st,
+                                             bool is_res, int nvalid, float qk_scale, float beta_log2, int hd,
+                                             int g, const T* vc, int s0, int app_row, const T* vn) {
   f32x4_t s[kTiles];
 #pragma unroll
-  for (int t = 0; t < kTiles; ++t) s[t] = qk.run(u.k[t]);
-  load_unit_v<T, D>(vr, vc, s0, nvalid, c, ph);
-#pragma unroll
-  for (int t = 0; t < kTiles; ++t) {
-    const bool live = 16 * t + col < nvalid;
-    const bool dead = !live || (is_res && u.lc[t] == kNegInf);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float v = s[t][i] * qk_scale;
-      if (is_res) v += beta_log2 * u.lc[t];
-      s[t][i] = dead ? kNegInf : v;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float m = s[0][i];
-#pragma unroll
-    for (int t = 1; t < kTiles; ++t) m = fmaxf(m, s[t][i]);
-    m = wave_xor_max(m, 1); m = wave_xor_max(m, 2);
-    m = wave_xor_max(m, 4); m = wave_xor_max(m, 8);
-    const float m_new = fmaxf(st.m[i], m);
-    const float mu = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = exp2f(st.m[i] - mu);
-    float l = 0.f;
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t) {
-      const float e = exp2f(s[t][i] - mu);
-      s[t][i] = e;
-      l += e;
-    }
-    l = wave_xor_add(l, 1); l = wave_xor_add(l, 2);
-    l = wave_xor_add(l, 4); l = wave_xor_add(l, 8);
-    st.l[i] = fmaf(st.l[i], alpha, l);
-    st.m[i] = m_new;
-    const int h = 4 * grp + i;
-    if (h < GP && col == 0) s_alpha[h] = alpha;
-  }
+  for (int t = 0; t < kTiles; ++t) s[t] = mma<D>(u.k[t], q, zero4());
+  load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, app_row, vn);
+  float p[kTiles][4];
+  float mloc = kNegInf;
 #pragma unroll
   for (int t = 0; t < kTiles; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int h = 4 * grp + i;
-      if (h < GP) s_p[16 * t + col][h] = s[t][i];
+      const bool live = 16 * t + 4 * g + i < nvalid && !(is_res && u.lc[t][i] == kNegInf);
+      float v = s[t][i] * qk_scale;
+      if (is_res) v = fmaf(beta_log2, u.lc[t][i], v);
+      p[t][i] = live ? v : kNegInf;
+      mloc = fmaxf(mloc, p[t][i]);
     }
-  // LDS traffic of one wave executes in order; this keeps the compiler from
-  // moving the reads below above the writes
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  float al[GP];
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+  mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+  const float m_new = fmaxf(st.m, mloc);
+  const float mu = (m_new == kNegInf) ? 0.f : m_new;
+  const float alpha = fast_exp2(st.m - mu);
+  float lsum = 0.f;
 #pragma unroll
-  for (int h = 0; h < GP; ++h) al[h] = s_alpha[h];
+  for (int t = 0; t < kTiles; ++t)
 #pragma unroll
-  for (int h = 0; h < GP; ++h)
+    for (int i = 0; i < 4; ++i) {
+      p[t][i] = fast_exp2(p[t][i] - mu);
+      lsum += p[t][i];
+    }
+  lsum += __shfl_xor(lsum, 16, 64);
+  lsum += __shfl_xor(lsum, 32, 64);
+  st.l = fmaf(st.l, alpha, lsum);
+  st.m = m_new;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) st.acc[h][e] *= al[h];
+  for (int e = 0; e < WaveState<D>::kE; ++e)
 #pragma unroll
-  for (int k = 0; k < VRegs<T, D>::NR; ++k) {
-    const int j = ph + VRegs<T, D>::RP * k;
-    float v[8];
-    vr.v[k].widen(v);
-    float pr[GP];
+    for (int i = 0; i < 4; ++i) st.acc[e][i] *= alpha;
+  pv_unit<D>(st, u, p);
+}
+
+// Wave state -> LDS rows of the query heads this block serves: acc as
+// [GP][D], max and sum per head.
+template <int D, int GP>
+__device__ __forceinline__ void store_wave_state(const WaveState<D>& st, float (*acc)[D], float* m, float* l,
+                                                 int hd, int g) {
+  if (hd < GP) {
+    constexpr int kE = D / 16;
 #pragma unroll
-    for (int h = 0; h < GP; ++h) pr[h] = s_p[j][h];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) st.acc[h][e] = fmaf(pr[h], v[e], st.acc[h][e]);
+      for (int e = 0; e < kE; ++e) acc[hd][kE * (4 * g + i) + e] = st.acc[e][i];
+    if (g == 0) {
+      m[hd] = st.m;
+      l[hd] = st.l;
+    }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
-  using Regs = VRegs<T, D>;
   const int p = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   int r, n;
@@ -254,11 +292,8 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
   if (lo >= end) return;  // block-uniform
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int col = lane & 15, grp = lane >> 4;
-  const int c = lane % Regs::CPR, ph = lane / Regs::CPR;
+  const int hd = lane & 15, g = lane >> 4;
 
-  __shared__ float s_p[kWaves][kUnit][GP];
-  __shared__ float s_alpha[kWaves][GP];
   __shared__ float s_acc[kWaves][GP][D];
   __shared__ float s_m[kWaves][GP];
   __shared__ float s_l[kWaves][GP];
@@ -267,43 +302,19 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
   const T* vc = static_cast<const T*>(a.vc) + (size_t)bh * a.C * D;
   const float* logc = a.logc + (size_t)bh * a.Rcap;
 
-  WaveState<GP> st;
+  WaveState<D> st;
   st.reset();
   const int s0 = lo + wave * kUnit;
   if (s0 < end) {  // wave-uniform
-    QK<T, D> qk;
-    qk.load_q(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + col) * D + grp * (D / 4),
-              col < a.G);
-    KRegs<T, D> kr;
-    VRegs<T, D> vr;
+    Frag<T, D> q;
+    if (hd < a.G) q.load(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + hd) * D, g);
+    else q.zero();
+    UnitRegs<T, D> u;
     const int nvalid = min(kUnit, end - s0);
-    load_unit_k<T, D>(kr, kc, logc, is_res, s0, nvalid, col, grp);
-    process_unit<T, D, GP>(kr, vr, qk, st, s_p[wave], s_alpha[wave], is_res, nvalid, a.qk_scale, a.beta_log2,
-                           col, grp, c, ph, vc, s0);
+    load_unit_k<T, D>(u, kc, logc, is_res, s0, nvalid, hd, g, -1, nullptr);
+    process_unit<T, D>(u, q, st, is_res, nvalid, a.qk_scale, a.beta_log2, hd, g, vc, s0, -1, nullptr);
   }
-  // wave state -> LDS: sum the row phases of acc, keep max and sum per head
-#pragma unroll
-  for (int msk = Regs::CPR; msk < 64; msk <<= 1)
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) st.acc[h][e] = wave_xor_add(st.acc[h][e], msk);
-  if (ph == 0) {
-#pragma unroll
-    for (int h = 0; h < GP; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s_acc[wave][h][8 * c + e] = st.acc[h][e];
-  }
-  if (col == 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int h = 4 * grp + i;
-      if (h < GP) {
-        s_m[wave][h] = st.m[i];
-        s_l[wave][h] = st.l[i];
-      }
-    }
-  }
+  store_wave_state<D, GP>(st, s_acc[wave], s_m[wave], s_l[wave], hd, g);
   __syncthreads();
   // merge the 4 waves into this block's record
   const size_t rec = ((size_t)bh * a.P + p) * GP;
@@ -408,7 +419,7 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
 }
 
 
-// One block of 16 waves per (b, kv head): streams every slot of the head,
+// One block of 8 waves per (b, kv head): streams every slot of the head,
 // merges the wave states in LDS, applies the gate and writes the G outputs;
 // optionally appends this step's token first. Used when the (b, kv head)
 // pairs alone fill the GPU, so no split-K records or second launch are needed.
@@ -420,122 +431,105 @@ constexpr int kHeadThreads = 64 * kHeadWaves;
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
-  using Regs = VRegs<T, D>;
   const int kvh = blockIdx.x, b = blockIdx.y;
   const int bh = b * a.Hkv + kvh;
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int col = lane & 15, grp = lane >> 4;
-  const int c = lane % Regs::CPR, ph = lane / Regs::CPR;
+  const int hd = lane & 15, g = lane >> 4;
   T* kc = static_cast<T*>(const_cast<void*>(a.kc)) + (size_t)bh * a.C * D;
   T* vc = static_cast<T*>(const_cast<void*>(a.vc)) + (size_t)bh * a.C * D;
   const float* logc = a.logc + (size_t)bh * a.Rcap;
 
-  // fused append of this step's token as main slot r + n (Sec. 3.1)
+  // fused append of this step's token as main slot r + n (Sec. 3.1): the
+  // row is stored into the cache for later steps, and this call reads it
+  // from k_new / v_new, so no wave waits for the store
   const bool app = a.k_new != nullptr && r + n < a.C;
+  const int app_row = app ? r + n : -1;
+  const T* kn = app ? static_cast<const T*>(a.k_new) + (size_t)bh * D : nullptr;
+  const T* vn = app ? static_cast<const T*>(a.v_new) + (size_t)bh * D : nullptr;
   if (app) {
-    const T* kn = static_cast<const T*>(a.k_new) + (size_t)bh * D;
-    const T* vn = static_cast<const T*>(a.v_new) + (size_t)bh * D;
     for (int x = tid; x < D; x += kHeadThreads) {
-      kc[(size_t)(r + n) * D + x] = kn[x];
-      vc[(size_t)(r + n) * D + x] = vn[x];
+      kc[(size_t)app_row * D + x] = kn[x];
+      vc[(size_t)app_row * D + x] = vn[x];
     }
+    n += 1;
   }
-  __syncthreads();  // the appended row is visible to every wave of the block
-  if (app) n += 1;
 
-  __shared__ float s_p[kHeadWaves][kUnit][GP];
-  __shared__ float s_alpha[kHeadWaves][GP];
-  __shared__ float s_acc[kHeadWaves][GP][D];
-  __shared__ float s_m[kHeadWaves][GP];
-  __shared__ float s_l[kHeadWaves][GP];
-  __shared__ float s_res[GP][D + 2];  // merged residual state: acc[D], m, l
+  __shared__ float s_acc[2][kHeadWaves][GP][D];  // per kind (0 residual, 1 main), per wave
+  __shared__ float s_m[2][kHeadWaves][GP];
+  __shared__ float s_l[2][kHeadWaves][GP];
 
-  QK<T, D> qk;
-  qk.load_q(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + col) * D + grp * (D / 4),
-            col < a.G);
+  Frag<T, D> q;
+  if (hd < a.G) q.load(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + hd) * D, g);
+  else q.zero();
 
-  for (int kind = 0; kind < 2; ++kind) {
-    const bool is_res = kind == 0;
-    const int base = is_res ? 0 : r;
-    const int end = is_res ? r : r + n;
-    const int U = (end - base + kUnit - 1) / kUnit;
-    WaveState<GP> st;
+  // One pass over all units of the head: residual units [0, UR) first, then
+  // main units, dealt round-robin to the waves so that every wave streams
+  // about the same number of slots whatever the split between the kinds.
+  const int UR = (r + kUnit - 1) / kUnit, UM = (n + kUnit - 1) / kUnit;
+  WaveState<D> st;
+  st.reset();
+  bool in_res = true;  // wave-uniform
+  for (int u = wave; u < UR + UM; u += kHeadWaves) {
+    const bool is_res = u < UR;
+    if (!is_res && in_res) {
+      store_wave_state<D, GP>(st, s_acc[0][wave], s_m[0][wave], s_l[0][wave], hd, g);
+      st.reset();
+      in_res = false;
+    }
+    const int s0 = is_res ? u * kUnit : r + (u - UR) * kUnit;
+    const int nvalid = min(kUnit, (is_res ? r : r + n) - s0);
+    UnitRegs<T, D> ur;
+    load_unit_k<T, D>(ur, kc, logc, is_res, s0, nvalid, hd, g, app_row, kn);
+    process_unit<T, D>(ur, q, st, is_res, nvalid, a.qk_scale, a.beta_log2, hd, g, vc, s0, app_row, vn);
+  }
+  if (in_res) {
+    store_wave_state<D, GP>(st, s_acc[0][wave], s_m[0][wave], s_l[0][wave], hd, g);
     st.reset();
-    for (int u = wave; u < U; u += kHeadWaves) {  // wave-uniform
-      const int s0 = base + u * kUnit;
-      const int nvalid = min(kUnit, end - s0);
-      KRegs<T, D> kr;
-      VRegs<T, D> vr;
-      load_unit_k<T, D>(kr, kc, logc, is_res, s0, nvalid, col, grp);
-      process_unit<T, D, GP>(kr, vr, qk, st, s_p[wave], s_alpha[wave], is_res, nvalid, a.qk_scale, a.beta_log2,
-                             col, grp, c, ph, vc, s0);
-    }
+  }
+  store_wave_state<D, GP>(st, s_acc[1][wave], s_m[1][wave], s_l[1][wave], hd, g);
+  __syncthreads();
+
+  // merge the waves per kind, then the gate and the shared denominator
+  for (int idx = tid; idx < a.G * D; idx += kHeadThreads) {
+    const int h = idx / D, d = idx % D;
+    float Mk[2], lk[2], ok[2];
 #pragma unroll
-    for (int msk = Regs::CPR; msk < 64; msk <<= 1)
+    for (int kind = 0; kind < 2; ++kind) {
+      float M = s_m[kind][0][h];
 #pragma unroll
-      for (int h = 0; h < GP; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) st.acc[h][e] = wave_xor_add(st.acc[h][e], msk);
-    if (ph == 0) {
-#pragma unroll
-      for (int h = 0; h < GP; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s_acc[wave][h][8 * c + e] = st.acc[h][e];
-    }
-    if (col == 0) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int h = 4 * grp + i;
-        if (h < GP) {
-          s_m[wave][h] = st.m[i];
-          s_l[wave][h] = st.l[i];
-        }
-      }
-    }
-    __syncthreads();
-    for (int idx = tid; idx < GP * D; idx += kHeadThreads) {
-      const int h = idx / D, d = idx % D;
-      float M = s_m[0][h];
-#pragma unroll
-      for (int w = 1; w < kHeadWaves; ++w) M = fmaxf(M, s_m[w][h]);
+      for (int w = 1; w < kHeadWaves; ++w) M = fmaxf(M, s_m[kind][w][h]);
       float o = 0.f, l = 0.f;
       if (M != kNegInf) {
 #pragma unroll
         for (int w = 0; w < kHeadWaves; ++w) {
-          const float f = exp2f(s_m[w][h] - M);
-          o = fmaf(f, s_acc[w][h][d], o);
-          l = fmaf(f, s_l[w][h], l);
+          const float f = exp2f(s_m[kind][w][h] - M);
+          o = fmaf(f, s_acc[kind][w][h][d], o);
+          l = fmaf(f, s_l[kind][w][h], l);
         }
       }
-      if (is_res) {
-        s_res[h][d] = o;
-        if (d == 0) { s_res[h][D] = M; s_res[h][D + 1] = l; }
-        continue;
-      }
-      if (h >= a.G) continue;
-      // main merged: p_max = 1 / l (the max term is exactly 1), then the gate
-      const float pmax = l > 0.f ? 1.f / l : 1.f;
-      const int qh = b * a.Hq + kvh * a.G + h;
-      const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
-      const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
-      const float lg2g = g > 0.f ? log2f(g) : kNegInf;
-      const float mR = s_res[h][D], lR = s_res[h][D + 1];
-      const float mRg = (mR == kNegInf || lg2g == kNegInf) ? kNegInf : mR + lg2g;
-      const float Mx = fmaxf(M, mRg);
-      const float fM = M != kNegInf ? exp2f(M - Mx) : 0.f;
-      const float fR = mRg != kNegInf ? exp2f(mRg - Mx) : 0.f;
-      const float den = l * fM + lR * fR;
-      const float num = o * fM + s_res[h][d] * fR;
-      a.out[(size_t)qh * D + d] = den > 0.f ? num / den : 0.f;
-      if (d == 0) {
-        if (a.dbg_lse_main) a.dbg_lse_main[qh] = l > 0.f ? (M + log2f(l)) * kLn2 : kNegInf;
-        if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
-        if (a.dbg_gate) a.dbg_gate[qh] = g;
-      }
+      Mk[kind] = M; lk[kind] = l; ok[kind] = o;
     }
-    __syncthreads();
+    const float M = Mk[1], l = lk[1], mR = Mk[0], lR = lk[0];
+    // p_max = 1 / l_main (the max term is exactly 1), then the gate
+    const float pmax = l > 0.f ? 1.f / l : 1.f;
+    const int qh = b * a.Hq + kvh * a.G + h;
+    const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
+    const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
+    const float lg2g = g > 0.f ? log2f(g) : kNegInf;
+    const float mRg = (mR == kNegInf || lg2g == kNegInf) ? kNegInf : mR + lg2g;
+    const float Mx = fmaxf(M, mRg);
+    const float fM = M != kNegInf ? exp2f(M - Mx) : 0.f;
+    const float fR = mRg != kNegInf ? exp2f(mRg - Mx) : 0.f;
+    const float den = l * fM + lR * fR;
+    const float num = ok[1] * fM + ok[0] * fR;
+    a.out[(size_t)qh * D + d] = den > 0.f ? num / den : 0.f;
+    if (d == 0) {
+      if (a.dbg_lse_main) a.dbg_lse_main[qh] = l > 0.f ? (M + log2f(l)) * kLn2 : kNegInf;
+      if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
+      if (a.dbg_gate) a.dbg_gate[qh] = g;
+    }
   }
   if (app && tid == 0) a.main_len[bh] = n;
 }
