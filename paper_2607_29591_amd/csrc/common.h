@@ -104,6 +104,10 @@ struct Frag<uint16_t, D> {        // bf16: 16x16x32 steps, 8 elements per step
 #pragma unroll
     for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const uint4*>(row + 8 * grp + 32 * i);
   }
+  __device__ __forceinline__ void store(uint16_t* row, int grp) const {
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) *reinterpret_cast<uint4*>(row + 8 * grp + 32 * i) = w[i];
+  }
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int i = 0; i < kSteps; ++i) w[i] = make_uint4(0, 0, 0, 0);
@@ -117,6 +121,10 @@ struct Frag<float, D> {           // fp32: 16x16x4 steps, 1 element per step
   __device__ __forceinline__ void load(const float* row, int grp) {
 #pragma unroll
     for (int i = 0; i < kSteps; ++i) w[i] = *reinterpret_cast<const float4*>(row + 4 * grp + 16 * i);
+  }
+  __device__ __forceinline__ void store(float* row, int grp) const {
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) *reinterpret_cast<float4*>(row + 4 * grp + 16 * i) = w[i];
   }
   __device__ __forceinline__ void zero() {
 #pragma unroll

@@ -92,6 +92,15 @@ struct VPiece {
       }
     }
   }
+  __device__ __forceinline__ void store(T* p) const {
+    if constexpr (kWords == 2) {
+      *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < kWords / 4; ++j)
+        reinterpret_cast<uint4*>(p)[j] = make_uint4(w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]);
+    }
+  }
 };
 
 // Key fragments (+ log-counts) and value pieces of one 64-slot unit.
@@ -102,44 +111,57 @@ struct UnitRegs {
   VPiece<T, D> v[16];      // v[4T + u]: piece hd of value row 16T + 4g + u
 };
 
-// Loads of unit [s0, s0 + nvalid); rows past the tail are clamped into the
-// unit (their probabilities are zero). Slot app_row (or none if -1) is taken
-// from the token being appended (kn / vn) instead of the cache: the unit that
-// holds it (wave-uniform test) reloads the lanes that read that row.
+// Key rows s0 + 16t + hd of a unit, clamped to row `last` (rows past the
+// valid range get no probability). Slot app_row (or none if -1) is taken from
+// the token being appended (kn) instead of the cache; only the unit that
+// holds it (a wave-uniform test) pays for the per-lane pointer choice.
 template <typename T, int D>
-__device__ __forceinline__ void load_unit_k(UnitRegs<T, D>& u, const T* kc, const float* logc, bool is_res,
-                                            int s0, int nvalid, int hd, int g, int app_row, const T* kn) {
+__device__ __forceinline__ void load_unit_k(UnitRegs<T, D>& u, const T* kc, int s0, int last, int hd, int g,
+                                            int app_row, const T* kn) {
+  if (app_row >= s0 && app_row < s0 + kUnit) {
 #pragma unroll
-  for (int t = 0; t < kTiles; ++t) u.k[t].load(kc + (size_t)(s0 + min(16 * t + hd, nvalid - 1)) * D, g);
-  if (app_row >= s0 && app_row < s0 + nvalid) {
+    for (int t = 0; t < kTiles; ++t) {
+      const int row = min(s0 + 16 * t + hd, last);
+      u.k[t].load(row == app_row ? kn : kc + (size_t)row * D, g);
+    }
+  } else {
 #pragma unroll
-    for (int t = 0; t < kTiles; ++t)
-      if (s0 + min(16 * t + hd, nvalid - 1) == app_row) u.k[t].load(kn, g);
+    for (int t = 0; t < kTiles; ++t) u.k[t].load(kc + (size_t)min(s0 + 16 * t + hd, last) * D, g);
   }
+}
+
+// Log-counts of the unit's residual slots s0 + j, j < nres.
+template <typename T, int D>
+__device__ __forceinline__ void load_unit_lc(UnitRegs<T, D>& u, const float* logc, int s0, int nres, int g) {
 #pragma unroll
   for (int t = 0; t < kTiles; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 16 * t + 4 * g + i;
-      u.lc[t][i] = (is_res && j < nvalid) ? logc[s0 + j] : 0.f;
+      u.lc[t][i] = j < nres ? logc[s0 + j] : 0.f;
     }
 }
 
+// Value rows of unit [s0, s0 + nvalid), clamped into the unit; slot app_row
+// from vn as for the keys.
 template <typename T, int D>
 __device__ __forceinline__ void load_unit_v(UnitRegs<T, D>& u, const T* vc, int s0, int nvalid, int hd, int g,
                                             int app_row, const T* vn) {
   constexpr int kE = VPiece<T, D>::kElems;
-#pragma unroll
-  for (int T4 = 0; T4 < 4; ++T4)
-#pragma unroll
-    for (int uu = 0; uu < 4; ++uu)
-      u.v[4 * T4 + uu].load(vc + (size_t)(s0 + min(16 * T4 + 4 * g + uu, nvalid - 1)) * D + kE * hd);
   if (app_row >= s0 && app_row < s0 + nvalid) {
 #pragma unroll
     for (int T4 = 0; T4 < 4; ++T4)
 #pragma unroll
+      for (int uu = 0; uu < 4; ++uu) {
+        const int row = s0 + min(16 * T4 + 4 * g + uu, nvalid - 1);
+        u.v[4 * T4 + uu].load((row == app_row ? vn : vc + (size_t)row * D) + kE * hd);
+      }
+  } else {
+#pragma unroll
+    for (int T4 = 0; T4 < 4; ++T4)
+#pragma unroll
       for (int uu = 0; uu < 4; ++uu)
-        if (s0 + min(16 * T4 + 4 * g + uu, nvalid - 1) == app_row) u.v[4 * T4 + uu].load(vn + kE * hd);
+        u.v[4 * T4 + uu].load(vc + (size_t)(s0 + min(16 * T4 + 4 * g + uu, nvalid - 1)) * D + kE * hd);
   }
 }
 
@@ -213,25 +235,34 @@ __device__ __forceinline__ void pv_unit(WaveState<D>& st, const UnitRegs<float, 
                                                          st.acc[e], 0, 0, 0);
 }
 
-// One unit: logits on MFMA, then (once the key fragments are consumed) the
-// value loads, the online softmax update and P.V.
+// Scaled logits of one unit in base 2: lane (hd, g) gets slot 16t + 4g + i.
 template <typename T, int D>
-__device__ __forceinline__ void process_unit(UnitRegs<T, D>& u, const Frag<T, D>& q, WaveState<D>& st,
-                                             bool is_res, int nvalid, float qk_scale, float beta_log2, int hd,
-                                             int g, const T* vc, int s0, int app_row, const T* vn) {
-  f32x4_t s[kTiles];
+__device__ __forceinline__ void unit_logits(const UnitRegs<T, D>& u, const Frag<T, D>& q, float qk_scale,
+                                            float (&s)[kTiles][4]) {
 #pragma unroll
-  for (int t = 0; t < kTiles; ++t) s[t] = mma<D>(u.k[t], q, zero4());
-  load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, app_row, vn);
+  for (int t = 0; t < kTiles; ++t) {
+    const f32x4_t c = mma<D>(u.k[t], q, zero4());
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s[t][i] = c[i] * qk_scale;
+  }
+}
+
+// Online softmax update over the unit's slots [lo, hi) of one kind (residual
+// slots add beta * log2 count; empty entries and other slots get no weight):
+// per-head max and sum over the lane's 16 slots, then across the four lane
+// groups, then P.V.
+template <typename T, int D>
+__device__ __forceinline__ void softmax_pv(WaveState<D>& st, const UnitRegs<T, D>& u, const float (&s)[kTiles][4],
+                                           int lo, int hi, bool is_res, float beta_log2, int g) {
   float p[kTiles][4];
   float mloc = kNegInf;
 #pragma unroll
   for (int t = 0; t < kTiles; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const bool live = 16 * t + 4 * g + i < nvalid && !(is_res && u.lc[t][i] == kNegInf);
-      float v = s[t][i] * qk_scale;
-      if (is_res) v = fmaf(beta_log2, u.lc[t][i], v);
+      const int j = 16 * t + 4 * g + i;
+      const bool live = j >= lo && j < hi && !(is_res && u.lc[t][i] == kNegInf);
+      const float v = is_res ? fmaf(beta_log2, u.lc[t][i], s[t][i]) : s[t][i];
       p[t][i] = live ? v : kNegInf;
       mloc = fmaxf(mloc, p[t][i]);
     }
@@ -311,8 +342,12 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
     else q.zero();
     UnitRegs<T, D> u;
     const int nvalid = min(kUnit, end - s0);
-    load_unit_k<T, D>(u, kc, logc, is_res, s0, nvalid, hd, g, -1, nullptr);
-    process_unit<T, D>(u, q, st, is_res, nvalid, a.qk_scale, a.beta_log2, hd, g, vc, s0, -1, nullptr);
+    load_unit_k<T, D>(u, kc, s0, end - 1, hd, g, -1, nullptr);
+    if (is_res) load_unit_lc<T, D>(u, logc, s0, nvalid, g);
+    float sc[kTiles][4];
+    unit_logits<T, D>(u, q, a.qk_scale, sc);
+    load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, -1, nullptr);
+    softmax_pv<T, D>(st, u, sc, 0, nvalid, is_res, a.beta_log2, g);
   }
   store_wave_state<D, GP>(st, s_acc[wave], s_m[wave], s_l[wave], hd, g);
   __syncthreads();
@@ -433,28 +468,31 @@ template <typename T, int D, int GP>
 __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   const int kvh = blockIdx.x, b = blockIdx.y;
   const int bh = b * a.Hkv + kvh;
-  int r, n;
-  cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int hd = lane & 15, g = lane >> 4;
   T* kc = static_cast<T*>(const_cast<void*>(a.kc)) + (size_t)bh * a.C * D;
   T* vc = static_cast<T*>(const_cast<void*>(a.vc)) + (size_t)bh * a.C * D;
   const float* logc = a.logc + (size_t)bh * a.Rcap;
 
-  // fused append of this step's token as main slot r + n (Sec. 3.1): the
-  // row is stored into the cache for later steps, and this call reads it
-  // from k_new / v_new, so no wave waits for the store
+  // Units: residual slots [0, r) in 64-slot chunks, then main slots [r, r+n)
+  // in 64-slot chunks, dealt round-robin to the waves so that every wave
+  // streams about the same number of slots whatever the split between the
+  // kinds. A wave's first unit is slots [64 wave, 64 wave + 64) unless it is a
+  // main unit and r is not a multiple of 64, so its keys are requested before
+  // the cache lengths are read (and requested again in that case).
+  UnitRegs<T, D> ur0;
+  load_unit_k<T, D>(ur0, kc, kUnit * wave, a.C - 1, hd, g, -1, nullptr);
+  int r, n;
+  cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+
+  // fused append of this step's token as main slot r + n (Sec. 3.1): this
+  // call reads it from k_new / v_new, and the wave whose unit holds it
+  // stores it into the cache for later steps
   const bool app = a.k_new != nullptr && r + n < a.C;
   const int app_row = app ? r + n : -1;
   const T* kn = app ? static_cast<const T*>(a.k_new) + (size_t)bh * D : nullptr;
   const T* vn = app ? static_cast<const T*>(a.v_new) + (size_t)bh * D : nullptr;
-  if (app) {
-    for (int x = tid; x < D; x += kHeadThreads) {
-      kc[(size_t)app_row * D + x] = kn[x];
-      vc[(size_t)app_row * D + x] = vn[x];
-    }
-    n += 1;
-  }
+  if (app) n += 1;
 
   __shared__ float s_acc[2][kHeadWaves][GP][D];  // per kind (0 residual, 1 main), per wave
   __shared__ float s_m[2][kHeadWaves][GP];
@@ -464,25 +502,66 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   if (hd < a.G) q.load(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + hd) * D, g);
   else q.zero();
 
-  // One pass over all units of the head: residual units [0, UR) first, then
-  // main units, dealt round-robin to the waves so that every wave streams
-  // about the same number of slots whatever the split between the kinds.
-  const int UR = (r + kUnit - 1) / kUnit, UM = (n + kUnit - 1) / kUnit;
+  const int UR = (r + kUnit - 1) / kUnit, U = UR + (n + kUnit - 1) / kUnit;
+  auto unit_range = [&](int u, bool& is_res, int& s0, int& end) {
+    is_res = u < UR;
+    s0 = is_res ? u * kUnit : r + (u - UR) * kUnit;
+    end = is_res ? r : r + n;
+  };
   WaveState<D> st;
   st.reset();
-  bool in_res = true;  // wave-uniform
-  for (int u = wave; u < UR + UM; u += kHeadWaves) {
-    const bool is_res = u < UR;
+  bool in_res = true;  // wave-uniform: the residual state is not yet stored
+  // one unit whose keys are already requested into ur.k
+  auto run_unit = [&](int u, UnitRegs<T, D>& ur) {
+    bool is_res;
+    int s0, end;
+    unit_range(u, is_res, s0, end);
+    const int nvalid = min(kUnit, end - s0);
     if (!is_res && in_res) {
       store_wave_state<D, GP>(st, s_acc[0][wave], s_m[0][wave], s_l[0][wave], hd, g);
       st.reset();
       in_res = false;
     }
-    const int s0 = is_res ? u * kUnit : r + (u - UR) * kUnit;
-    const int nvalid = min(kUnit, (is_res ? r : r + n) - s0);
+    if (is_res) load_unit_lc<T, D>(ur, logc, s0, nvalid, g);
+    const bool has_app = app_row >= s0 && app_row < s0 + nvalid;
+    if (has_app) {  // the new key row into the cache, from the registers that received it
+#pragma unroll
+      for (int t = 0; t < kTiles; ++t)
+        if (s0 + 16 * t + hd == app_row) ur.k[t].store(kc + (size_t)app_row * D, g);
+    }
+    float sc[kTiles][4];
+    unit_logits<T, D>(ur, q, a.qk_scale, sc);
+    load_unit_v<T, D>(ur, vc, s0, nvalid, hd, g, app_row, vn);
+    softmax_pv<T, D>(st, ur, sc, 0, nvalid, is_res, a.beta_log2, g);
+    if (has_app) {
+#pragma unroll
+      for (int T4 = 0; T4 < 4; ++T4)
+#pragma unroll
+        for (int uu = 0; uu < 4; ++uu)
+          if (s0 + 16 * T4 + 4 * g + uu == app_row)
+            ur.v[4 * T4 + uu].store(vc + (size_t)app_row * D + VPiece<T, D>::kElems * hd);
+    }
+  };
+  if (wave < U) {
+    bool is_res;
+    int s0, end;
+    unit_range(wave, is_res, s0, end);
+    if (s0 != kUnit * wave) {
+      load_unit_k<T, D>(ur0, kc, s0, end - 1, hd, g, app_row, kn);
+    } else if (app_row >= s0 && app_row < s0 + kUnit) {
+#pragma unroll
+      for (int t = 0; t < kTiles; ++t)
+        if (min(s0 + 16 * t + hd, a.C - 1) == app_row) ur0.k[t].load(kn, g);
+    }
+    run_unit(wave, ur0);
+  }
+  for (int u = wave + kHeadWaves; u < U; u += kHeadWaves) {
+    bool is_res;
+    int s0, end;
+    unit_range(u, is_res, s0, end);
     UnitRegs<T, D> ur;
-    load_unit_k<T, D>(ur, kc, logc, is_res, s0, nvalid, hd, g, app_row, kn);
-    process_unit<T, D>(ur, q, st, is_res, nvalid, a.qk_scale, a.beta_log2, hd, g, vc, s0, app_row, vn);
+    load_unit_k<T, D>(ur, kc, s0, end - 1, hd, g, app_row, kn);
+    run_unit(u, ur);
   }
   if (in_res) {
     store_wave_state<D, GP>(st, s_acc[0][wave], s_m[0][wave], s_l[0][wave], hd, g);
@@ -590,8 +669,10 @@ DecodePlan make_decode_plan(const reskv_shape_t& s) {
   const int rmax = s.res_cap < s.slot_cap ? s.res_cap : s.slot_cap;
   p.PR = (rmax + kChunk - 1) / kChunk;
   p.P = p.PR + (s.slot_cap + kChunk - 1) / kChunk;
-  // one block per (b, kv head) when those alone fill the chip's CUs
-  p.whole_head = p.GP <= 4 && (long long)p.B * p.Hkv >= kWholeHeadMin;
+  // one block per (b, kv head) when those alone fill the chip's CUs (fp32
+  // rows of 128 take the split kernels: the head kernel would spill)
+  p.whole_head = p.GP <= 4 && (long long)p.B * p.Hkv >= kWholeHeadMin &&
+                 (s.dtype == RESKV_BF16 || p.D == 64);
   const size_t recs = (size_t)p.B * p.Hkv * p.P * p.GP;
   p.acc_off = 0;
   p.ml_off = align_up(recs * p.D * sizeof(float), 256);

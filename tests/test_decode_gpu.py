@@ -173,8 +173,9 @@ def test_append_then_decode(dtype):
 def test_decode_fused_append(dtype, d, G, B, Hkv):
     """reskv_decode_attn with this step's K/V: the token is appended as main
     slot r + n (cache and main_len written) and attended in the same call.
-    B*Hkv >= 256 with G <= 4 takes the one-block-per-head kernel; the others
-    the split-K kernels; full caches are left unchanged."""
+    B*Hkv >= 256 with G <= 4 (bf16, or fp32 rows of 64) takes the
+    one-block-per-head kernel; the others the split-K kernels; full caches are
+    left unchanged."""
     rng = np.random.default_rng(11 + d + G)
     C, Rcap = 300, 64
     res = rng.choice([0, 16, 64], size=(B, Hkv))
@@ -208,10 +209,11 @@ def test_decode_fused_append(dtype, d, G, B, Hkv):
     assert rel_err_rows(out.double().cpu().numpy(), ref).max() <= TOL[dtype]
 
 
-@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 64), ("f32", 128)])
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 64), ("f32", 128), ("bf16", 128)])
 def test_decode_whole_head_path_shapes(dtype, d):
-    """256 (b, kv head) pairs: the one-block-per-head kernel, with ragged
-    lengths, r = 0 heads and empty entries."""
+    """256 (b, kv head) pairs (the one-block-per-head kernel; fp32 rows of 128
+    take the split kernels), with ragged lengths, r = 0 heads and empty
+    entries."""
     B, Hkv, G = 64, 4, 4
     rng = np.random.default_rng(30 + d)
     C, Rcap = 700, 130
