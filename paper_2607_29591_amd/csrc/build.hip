@@ -33,6 +33,8 @@
 
 #include <vector>
 
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -41,7 +43,12 @@ namespace reskv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kKeyChunk = 256;     // keys per scoring block (16 MFMA tiles)
+constexpr int kKeyGroups = 4;     // 256-key groups per scoring block, streamed with key prefetch
+constexpr int kKeyChunk = 256 * kKeyGroups;  // keys per scoring block
+constexpr int kRowChunk = 128;     // window rows staged in LDS per scoring step
+// s_waitcnt immediate: vector-memory count 0, export and LDS/scalar counts
+// left at their maximum (no wait on them)
+constexpr int kWaitVmcnt0 = 0x0F70;
 constexpr int kTokTiles = 4;       // 16-token MFMA tiles per wave in the assignment
 constexpr int kAssignWaves = 8;    // 2 waves per SIMD: one's argmin VALU overlaps the other's MFMAs
 constexpr int kAssignThreads = 64 * kAssignWaves;
@@ -87,23 +94,43 @@ __device__ __forceinline__ void store_elem(uint16_t* p, float x) { *p = f32_to_b
 __device__ __forceinline__ void store_elem(float* p, float x) { *p = x; }
 
 // Window row t = h*w + i of the group: query head kvh*G + h, position s-w+i.
+// Rows [r0, r0 + nrows) are copied into LDS with rows of D*sizeof(T) + 16
+// bytes (the pad keeps MFMA fragment reads free of bank conflicts); rows at
+// or past R are zero.
 template <typename T, int D>
-__device__ __forceinline__ void load_window_row(Frag<T, D>& f, const BuildArgs& a, int b, int kvh, int t, int grp) {
-  if (t < a.R) {
-    const int h = t / a.w, i = t % a.w;
-    const T* q = static_cast<const T*>(a.q_obs) + (((size_t)b * a.Hq + kvh * a.G + h) * a.w + i) * D;
-    f.load(q, grp);
-  } else {
-    f.zero();
+__device__ __forceinline__ void stage_window_rows(unsigned char* s_q, const BuildArgs& a, int b, int kvh, int r0,
+                                                  int nrows) {
+  constexpr int kPieces = D * (int)sizeof(T) / 16;
+  constexpr int kQRowB = D * (int)sizeof(T) + 16;
+  for (int x = threadIdx.x; x < nrows * kPieces; x += blockDim.x) {
+    const int rr = x / kPieces, pc = x % kPieces, t = r0 + rr;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (t < a.R) {
+      const int h = t / a.w, i = t % a.w;
+      const T* q = static_cast<const T*>(a.q_obs) + (((size_t)b * a.Hq + kvh * a.G + h) * a.w + i) * D;
+      v = reinterpret_cast<const uint4*>(q)[pc];
+    }
+    *reinterpret_cast<uint4*>(s_q + rr * kQRowB + pc * 16) = v;
   }
 }
 
 // ---------------------------------------------------------------- scoring
 
-// Each wave owns 64 keys of the block's 256-key chunk (its key fragments are
-// read once) and runs over every window row. The MFMA is oriented keys x rows,
-// C[key][row]: a lane holds 16 keys of one row, so a row's max and sum need
-// only two cross-lane steps.
+// Scoring blocks stream kKeyGroups groups of 256 keys; in each group a wave
+// owns 64 keys and runs over every window row, with the next group's key
+// fragments already requested. The window rows are staged in LDS once per
+// block (128 at a time).
+
+// Key fragments of the 64 keys from kw (clamped to the sequence).
+template <typename T, int D>
+__device__ __forceinline__ void load_score_keys(Frag<T, D> (&f)[4], const T* K, int kw, int s, int col, int grp) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) f[t].load(K + (size_t)min(kw + 16 * t + col, s - 1) * D, grp);
+}
+
+// lse pass: the MFMA is oriented keys x rows, C[key][row]: a lane holds 16
+// keys of one row, so a row's max and sum need only two cross-lane steps.
+// Each wave keeps a running (max, sum) per row over its key groups.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -113,58 +140,96 @@ __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
   if (hm.all_main || k0 >= hm.s) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  __shared__ float2 s_ml[4][1024];
+  constexpr int kQRowB = D * (int)sizeof(T) + 16;
+  constexpr int kRT = kRowChunk / 16;
+  __shared__ __align__(16) unsigned char s_q[kRowChunk * kQRowB];
+  __shared__ float2 s_ml[4][kRowChunk];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
-  const int kw = k0 + 64 * wave;  // this wave's first key
-  Frag<T, D> kf[4];
+  for (int r0 = 0; r0 < a.R; r0 += kRowChunk) {
+    const int nrt = (min(kRowChunk, a.R - r0) + 15) / 16;
+    if (r0 > 0) __syncthreads();  // the previous chunk's rows and records are consumed
+    Frag<T, D> kf[4], kn[4];
+    load_score_keys<T, D>(kf, K, k0 + 64 * wave, hm.s, col, grp);
+    stage_window_rows<T, D>(s_q, a, b, kvh, r0, 16 * nrt);
+    __syncthreads();
+    float rm[kRT], rl[kRT];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int p = min(kw + 16 * t + col, hm.s - 1);
-    kf[t].load(K + (size_t)p * D, grp);
-  }
-  const int RT = (a.R + 15) / 16;
-  for (int rt = 0; rt < RT; ++rt) {
-    const int t_row = 16 * rt + col;  // window row of this lane's column
-    Frag<T, D> qf;
-    load_window_row<T, D>(qf, a, b, kvh, t_row, grp);
-    const int pos = t_row < a.R ? hm.s - a.w + t_row % a.w : -1;
-    float v[16];
-    float m = kNegInf;
+    for (int rt = 0; rt < kRT; ++rt) { rm[rt] = kNegInf; rl[rt] = 0.f; }
+    // The first group's keys have landed; without this the compiler's wait
+    // tracking cannot tell them from the in-loop prefetch and makes the first
+    // row tile of every group wait for the prefetch.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+#pragma unroll 1
+    for (int gi = 0; gi < kKeyGroups; ++gi) {
+      const int kw = k0 + 256 * gi + 64 * wave;  // this wave's keys in group gi
+      if (gi + 1 < kKeyGroups) load_score_keys<T, D>(kn, K, kw + 256, hm.s, col, grp);
+      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of this group's work
+      // keys up to s - w are visible to every window row (and lie below s):
+      // such waves skip the per-element masks
+      auto rows = [&](auto full_tag) {
+        constexpr bool kFull = decltype(full_tag)::value;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const f32x4_t c = mma<D>(kf[t], qf, zero4());
+        for (int rt = 0; rt < kRT; ++rt) {
+          if (rt >= nrt) break;
+          const int t_row = r0 + 16 * rt + col;  // window row of this lane's column
+          Frag<T, D> qf;
+          qf.load(reinterpret_cast<const T*>(s_q + (16 * rt + col) * kQRowB), grp);
+          const int pos = t_row < a.R ? hm.s - a.w + t_row % a.w : -1;
+          // raw logits; the scale is positive, so the max commutes with it
+          float v[16];
+          float m = kNegInf;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int p = kw + 16 * t + 4 * grp + i;
-        const float x = (p < hm.s && p <= pos) ? c[i] * a.scale2 : kNegInf;
-        v[4 * t + i] = x;
-        m = fmaxf(m, x);
+          for (int t = 0; t < 4; ++t) {
+            const f32x4_t c = mma<D>(kf[t], qf, zero4());
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int p = kw + 16 * t + 4 * grp + i;
+              const float x = (kFull || (p < hm.s && p <= pos)) ? c[i] : kNegInf;
+              v[4 * t + i] = x;
+              m = fmaxf(m, x);
+            }
+          }
+          m = wave_xor_max(m, 16);
+          m = wave_xor_max(m, 32);
+          m = m == kNegInf ? kNegInf : m * a.scale2;
+          const float m_new = fmaxf(rm[rt], m);
+          if (m_new == kNegInf) continue;
+          float l = 0.f;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) l += fast_exp2(fmaf(v[j], a.scale2, -m_new));
+          l = wave_xor_add(l, 16);
+          l = wave_xor_add(l, 32);
+          rl[rt] = fmaf(rl[rt], fast_exp2(rm[rt] - m_new), l);
+          rm[rt] = m_new;
+        }
+      };
+      if (kw < hm.s) {  // wave-uniform
+        if (kw + 64 <= hm.s - a.w + 1) rows(std::true_type{});
+        else rows(std::false_type{});
+      }
+      if (gi + 1 < kKeyGroups) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) kf[t] = kn[t];
       }
     }
-    m = wave_xor_max(m, 16);
-    m = wave_xor_max(m, 32);
-    const float mu = m == kNegInf ? 0.f : m;
-    float l = 0.f;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) l += exp2f(v[j] - mu);
-    l = wave_xor_add(l, 16);
-    l = wave_xor_add(l, 32);
-    if (grp == 0 && t_row < a.R) s_ml[wave][t_row] = make_float2(m, l);
-  }
-  __syncthreads();
-  for (int t = threadIdx.x; t < a.R; t += kThreads) {
-    float M = kNegInf;
+    for (int rt = 0; rt < kRT; ++rt)
+      if (rt < nrt && grp == 0) s_ml[wave][16 * rt + col] = make_float2(rm[rt], rl[rt]);
+    __syncthreads();
+    for (int t = threadIdx.x; t < min(kRowChunk, a.R - r0); t += kThreads) {
+      float M = kNegInf;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][t].x);
-    float L = 0.f;
-    if (M != kNegInf) {
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][t].x);
+      float L = 0.f;
+      if (M != kNegInf) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float2 e = s_ml[w][t];
-        if (e.x != kNegInf) L = fmaf(e.y, exp2f(e.x - M), L);
+        for (int w = 0; w < 4; ++w) {
+          const float2 e = s_ml[w][t];
+          if (e.x != kNegInf) L = fmaf(e.y, exp2f(e.x - M), L);
+        }
       }
+      a.lse_part[((size_t)bh * a.NCH + ch) * a.R + r0 + t] = make_float2(M, L);
     }
-    a.lse_part[((size_t)bh * a.NCH + ch) * a.R + t] = make_float2(M, L);
   }
 }
 
@@ -186,9 +251,9 @@ __global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
   a.lse2[(size_t)bh * a.R + t] = M + log2f(L);
 }
 
-// Each wave owns 64 keys and runs over every window row; C[row][key]: a lane
-// holds one key of 4 rows, so the per-key sums stay in registers until two
-// final cross-lane steps, and no cross-wave merge is needed.
+// Score pass: C[row][key]: a lane holds one key of 4 rows, so the per-key
+// sums stay in registers until two final cross-lane steps, and no cross-wave
+// merge is needed.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -198,47 +263,76 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
   if (hm.all_main || k0 >= hm.n_sc) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  __shared__ float s_lse[1024];
-  for (int t = threadIdx.x; t < a.R; t += kThreads) s_lse[t] = a.lse2[(size_t)bh * a.R + t];
-  __syncthreads();
-  const int kw = k0 + 64 * wave;
-  if (kw >= hm.n_sc) return;  // wave-uniform; no barrier follows
+  constexpr int kQRowB = D * (int)sizeof(T) + 16;
+  constexpr int kRT = kRowChunk / 16;
+  __shared__ __align__(16) unsigned char s_q[kRowChunk * kQRowB];
+  __shared__ float s_lse[kRowChunk];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
-  Frag<T, D> kf[4];
+  for (int r0 = 0; r0 < a.R; r0 += kRowChunk) {
+    const int nr = min(kRowChunk, a.R - r0), nrt = (nr + 15) / 16;
+    if (r0 > 0) __syncthreads();  // the previous chunk's rows are consumed
+    Frag<T, D> kf[4], kn[4];
+    load_score_keys<T, D>(kf, K, k0 + 64 * wave, hm.s, col, grp);
+    stage_window_rows<T, D>(s_q, a, b, kvh, r0, 16 * nrt);
+    for (int t = threadIdx.x; t < nr; t += kThreads) s_lse[t] = a.lse2[(size_t)bh * a.R + r0 + t];
+    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // as in lse_partial: the first group's keys have landed
+#pragma unroll 1
+    for (int gi = 0; gi < kKeyGroups; ++gi) {
+      const int kw = k0 + 256 * gi + 64 * wave;  // this wave's keys in group gi
+      if (gi + 1 < kKeyGroups) load_score_keys<T, D>(kn, K, kw + 256, hm.s, col, grp);
+      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of this group's work
+      float ksum[4] = {0.f, 0.f, 0.f, 0.f};
+      // keys up to s - w are visible to every window row: such waves skip the
+      // per-element causal test (padded rows carry lse = +inf and add 0)
+      auto rows = [&](auto full_tag) {
+        constexpr bool kFull = decltype(full_tag)::value;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int p = min(kw + 16 * t + col, hm.s - 1);
-    kf[t].load(K + (size_t)p * D, grp);
-  }
-  float ksum[4] = {0.f, 0.f, 0.f, 0.f};
-  const int RT = (a.R + 15) / 16;
-  for (int rt = 0; rt < RT; ++rt) {
-    Frag<T, D> qf;
-    load_window_row<T, D>(qf, a, b, kvh, 16 * rt + col, grp);
-    float lse[4];
-    int pos[4];
+        for (int rt = 0; rt < kRT; ++rt) {
+          if (rt >= nrt) break;
+          Frag<T, D> qf;
+          qf.load(reinterpret_cast<const T*>(s_q + (16 * rt + col) * kQRowB), grp);
+          float lse[4];
+          int pos[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int t = 16 * rt + 4 * grp + i;
-      lse[i] = t < a.R ? s_lse[t] : 0.f;
-      pos[i] = t < a.R ? hm.s - a.w + t % a.w : -1;  // padded rows see no key
+          for (int i = 0; i < 4; ++i) {
+            const int tl = 16 * rt + 4 * grp + i, t = r0 + tl;
+            lse[i] = t < a.R ? s_lse[tl] : __builtin_huge_valf();
+            pos[i] = t < a.R ? hm.s - a.w + t % a.w : -1;  // padded rows see no key
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const f32x4_t c = mma<D>(qf, kf[t], zero4());
+            const int p = kw + 16 * t + col;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float e = fast_exp2(fmaf(c[i], a.scale2, -lse[i]));
+              ksum[t] += (kFull || p <= pos[i]) ? e : 0.f;
+            }
+          }
+        }
+      };
+      if (kw < hm.n_sc) {  // wave-uniform
+        if (kw + 64 <= hm.s - a.w + 1) rows(std::true_type{});
+        else rows(std::false_type{});
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          float v = ksum[t];
+          v = wave_xor_add(v, 16);
+          v = wave_xor_add(v, 32);
+          const int p = kw + 16 * t + col;
+          if (grp == 0 && p < hm.n_sc) {
+            float* dst = a.raw + (size_t)bh * a.S + p;
+            if (r0 == 0) *dst = v;
+            else *dst += v;  // later row chunks add to this lane's own sums
+          }
+        }
+      }
+      if (gi + 1 < kKeyGroups) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) kf[t] = kn[t];
+      }
     }
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const f32x4_t c = mma<D>(qf, kf[t], zero4());
-      const int p = kw + 16 * t + col;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (p <= pos[i]) ksum[t] += exp2f(fmaf(c[i], a.scale2, -lse[i]));
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    float v = ksum[t];
-    v = wave_xor_add(v, 16);
-    v = wave_xor_add(v, 32);
-    const int p = kw + 16 * t + col;
-    if (grp == 0 && p < hm.n_sc) a.raw[(size_t)bh * a.S + p] = v;
   }
 }
 
@@ -439,24 +533,27 @@ __global__ __launch_bounds__(kThreads) void gather_init(BuildArgs a) {
   }
 }
 
-// hi = bf16(mu), lo = bf16(mu - hi), norm = ||mu||^2 (fp64 sum, fixed order)
+// hi = bf16(mu), lo = bf16(mu - hi), norm = ||mu||^2 (fp64 sum in a fixed
+// order: a butterfly within each wave, then the waves' partials in order)
 template <int D>
 __device__ void prep_center(const BuildArgs& a, size_t ci, const float* mu, double* s_red) {
+  static_assert(D <= kThreads, "one element per thread");
   const int tid = threadIdx.x;
   double sq = 0.0;
-  for (int d = tid; d < D; d += kThreads) {
-    const float x = mu[d];
+  if (tid < D) {
+    const float x = mu[tid];
     const uint16_t h = f32_to_bf16_rne(x);
-    const uint16_t l = f32_to_bf16_rne(x - to_f32(h));
-    a.cent_hi[ci * D + d] = h;
-    a.cent_lo[ci * D + d] = l;
+    a.cent_hi[ci * D + tid] = h;
+    a.cent_lo[ci * D + tid] = f32_to_bf16_rne(x - to_f32(h));
     sq = (double)x * x;
-    s_red[d] = sq;
   }
+#pragma unroll
+  for (int msk = 1; msk < 64; msk <<= 1) sq += __shfl_xor(sq, msk, 64);
+  if ((tid & 63) == 0) s_red[tid >> 6] = sq;
   __syncthreads();
   if (tid == 0) {
     double t = 0.0;
-    for (int d = 0; d < D; ++d) t += s_red[d];
+    for (int w = 0; w < (D + 63) / 64; ++w) t += s_red[w];
     a.cnorm[ci] = (float)t;
   }
   __syncthreads();

@@ -47,7 +47,7 @@ struct HeadMeta {
 
 struct BuildPlan {
   int B, Hq, Hkv, G, D, C, Rcap, S, w, R, T, dtype;
-  int NCH;    // 256-key chunks of the longest sequence
+  int NCH;    // scoring key chunks of the longest sequence
   int NBLK;   // 256-token blocks of the largest evicted set
   int max_s, max_main, max_reff;
   size_t off_meta, off_lsep, off_lse, off_raw, off_score, off_elist, off_seeds, off_cent, off_chi,
