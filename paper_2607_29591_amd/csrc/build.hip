@@ -49,10 +49,10 @@ constexpr int kRowChunk = 128;     // window rows staged in LDS per scoring step
 // s_waitcnt immediate: vector-memory count 0, export and LDS/scalar counts
 // left at their maximum (no wait on them)
 constexpr int kWaitVmcnt0 = 0x0F70;
-constexpr int kTokTiles = 4;       // 16-token MFMA tiles per wave in the assignment
-constexpr int kAssignWaves = 8;    // 2 waves per SIMD: one's argmin VALU overlaps the other's MFMAs
+constexpr int kTokTiles = 2;       // 16-token MFMA tiles per wave in the assignment
+constexpr int kAssignWaves = 8;    // with at most 128 registers, two blocks share a CU
 constexpr int kAssignThreads = 64 * kAssignWaves;
-constexpr int kTokBlock = kAssignWaves * 16 * kTokTiles;  // evicted tokens per Lloyd block (512)
+constexpr int kTokBlock = kAssignWaves * 16 * kTokTiles;  // evicted tokens per Lloyd block (256)
 constexpr int kCenterChunk = 64;   // centres staged in LDS per step
 constexpr int kSelThreads = 1024;
 
@@ -607,7 +607,7 @@ __device__ __forceinline__ f32x4_t mma_step(const Frag<float, D>& c, const Frag<
 // the MFMA chains are independent. Centres past r' are staged with an
 // infinite norm and never win.
 template <typename T, int D>
-__global__ __launch_bounds__(kAssignThreads) void lloyd_assign(BuildArgs a, int iter) {
+__global__ __launch_bounds__(kAssignThreads, sizeof(T) == 2 ? 4 : 2) void lloyd_assign(BuildArgs a, int iter) {
   constexpr bool kBf = sizeof(T) == 2;
   constexpr int kRowB = kBf ? D * 2 + 16 : D * 4 + 16;   // padded LDS row bytes
   constexpr int kSteps = kBf ? D / 32 : D / 4;           // MFMA k-steps over the lane's share of a row
@@ -761,19 +761,34 @@ __global__ __launch_bounds__(kThreads) void lloyd_offsets(BuildArgs a) {
   int carry = 0;
   for (int j0 = 0; j0 < hm.r_eff; j0 += kThreads) {
     const int j = j0 + threadIdx.x;
+    // the column of block counts is read in batches of kBatch independent
+    // loads so the per-block walk is not a chain of memory round trips
+    constexpr int kBatch = 16;
     int tot = 0;
-    if (j < hm.r_eff)
-      for (int q = 0; q < nblk; ++q) tot += hist[(size_t)q * a.Rcap + j];
+    if (j < hm.r_eff) {
+      for (int q0 = 0; q0 < nblk; q0 += kBatch) {
+        int c[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) c[u] = q0 + u < nblk ? hist[(size_t)(q0 + u) * a.Rcap + j] : 0;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) tot += c[u];
+      }
+    }
     int all;
     const int start = carry + block_excl_scan<kThreads>(tot, s_tmp, all);
     if (j < hm.r_eff) {
       a.cstart[(size_t)bh * a.Rcap + j] = start;
       a.ccount[(size_t)bh * a.Rcap + j] = tot;
       int run = start;
-      for (int q = 0; q < nblk; ++q) {
-        const int c = hist[(size_t)q * a.Rcap + j];
-        hist[(size_t)q * a.Rcap + j] = run;
-        run += c;
+      for (int q0 = 0; q0 < nblk; q0 += kBatch) {
+        int c[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) c[u] = q0 + u < nblk ? hist[(size_t)(q0 + u) * a.Rcap + j] : 0;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          if (q0 + u < nblk) hist[(size_t)(q0 + u) * a.Rcap + j] = run;
+          run += c[u];
+        }
       }
     }
     carry += all;
@@ -787,16 +802,24 @@ __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
   const HeadMeta hm = a.meta[bh];
   const int t0 = blk * kTokBlock;
   if (hm.r_eff == 0 || t0 >= hm.nE) return;
-  __shared__ int s_a[kTokBlock];
+  __shared__ int4 s_a4[kTokBlock / 4];
+  int* s_a = reinterpret_cast<int*>(s_a4);
   const int i = t0 + threadIdx.x;
   const int g = i < hm.nE ? a.assign[(size_t)bh * a.S + i] : -1;
+  const int src = i < hm.nE ? a.elist[(size_t)bh * a.S + i] : 0;
   s_a[threadIdx.x] = g;
   __syncthreads();
   if (g < 0) return;
+  // stable rank: earlier tokens of the block in the same group, four per read
   int rank = 0;
-  for (int q = 0; q < (int)threadIdx.x; ++q) rank += (s_a[q] == g);
+  const int tid = threadIdx.x;
+  for (int q4 = 0; q4 < tid / 4; ++q4) {
+    const int4 v = s_a4[q4];
+    rank += (v.x == g) + (v.y == g) + (v.z == g) + (v.w == g);
+  }
+  for (int q = tid & ~3; q < tid; ++q) rank += (s_a[q] == g);
   const int dst = a.hist[((size_t)bh * a.NBLK + blk) * a.Rcap + g] + rank;
-  a.order[(size_t)bh * a.S + dst] = a.elist[(size_t)bh * a.S + i];
+  a.order[(size_t)bh * a.S + dst] = src;
 }
 
 // New centre of group j = fp64 mean of its members' keys, summed in a fixed
