@@ -97,6 +97,22 @@ def traffic_from_profile(src_hash):
     return rec.get("bytes_per_call")
 
 
+def construction_mfma_from_profile(src_hash):
+    """MFMA utilisation (rocprofv3 MfmaUtil, percent) of the construction's
+    MFMA kernels, if the committed measurement was taken on the current
+    construction source."""
+    path = os.path.join(ROOT, "profiles", "construction_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("build_source_sha256_16") != src_hash:
+        return None
+    ks = rec["kernels"]
+    return {k: {"mfma_util_pct": round(ks[k]["mfma_util_pct"], 1), "mfma_tflops": round(ks[k]["mfma_tflops"])}
+            for k in ("lse_partial", "score_accum", "lloyd_assign") if k in ks}
+
+
 def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
     """Time the fp64 oracle on a bounded sample of the job on the host and
     extrapolate to the whole job: one (sequence, KV head) of construction
@@ -309,6 +325,8 @@ def main():
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
     src = source_hash("paper_2607_29591_amd/csrc/decode.hip", "paper_2607_29591_amd/csrc/common.h")
     traffic = traffic_from_profile(src)
+    cmfma = construction_mfma_from_profile(
+        source_hash("paper_2607_29591_amd/csrc/build.hip", "paper_2607_29591_amd/csrc/common.h"))
 
     result = {
         "metric": "decode attn tokens/s (batch x layers)",
@@ -334,6 +352,7 @@ def main():
         "decode_gbs": dec_bytes_job / (decode_ms * 1e-3) / 1e9,
         "build_ms_per_layer": build_ms / L,
         "build_gbs": build_bytes / (build_ms * 1e-3) / 1e9,
+        "construction_mfma": cmfma,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "reskv_decode_attn (one launch per layer-step: decode_head, one block per "
