@@ -407,28 +407,57 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   const int kk[2] = {hm.k_top, hm.k_top + hm.r_eff};
   uint32_t prefix[2] = {0u, 0u}, mask = 0u;
   int krem[2] = {kk[0], kk[1]};
+  const int wave = tid >> 6, lane = tid & 63;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = tid; i < 512; i += kSelThreads) (&s_hist[0][0])[i] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += kSelThreads) {
-      const uint32_t u = key[i];
-      const int dig = (u >> shift) & 0xff;
+    // coalesced, four keys in flight per thread
+    for (int i0 = tid; i0 < n; i0 += 4 * kSelThreads) {
+      uint32_t u[4];
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
-        if (krem[q] > 0 && (u & mask) == prefix[q]) atomicAdd(&s_hist[q][dig], 1);
+      for (int v = 0; v < 4; ++v) u[v] = i0 + v * kSelThreads < n ? key[i0 + v * kSelThreads] : 0u;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        if (i0 + v * kSelThreads >= n) continue;
+        const int dig = (u[v] >> shift) & 0xff;
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          if (krem[q] > 0 && (u[v] & mask) == prefix[q]) atomicAdd(&s_hist[q][dig], 1);
+      }
     }
     __syncthreads();
-    if (tid < 2) {
-      const int q = tid;
+    // wave q finds the digit of threshold q: each lane holds 4 bins in
+    // descending digit order; an inclusive scan over lanes gives the count of
+    // keys at or above each digit
+    if (wave < 2) {
+      const int q = wave;
       if (krem[q] > 0) {
-        int acc = 0, d = 255;
-        for (; d > 0; --d) {
-          if (acc + s_hist[q][d] >= krem[q]) break;
-          acc += s_hist[q][d];
+        int c[4], own = 0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) { c[v] = s_hist[q][255 - 4 * lane - v]; own += c[v]; }
+        int incl = own;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o, 64);
+          if (lane >= o) incl += y;
         }
-        s_pref[q] = prefix[q] | ((uint32_t)d << shift);
-        s_krem[q] = krem[q] - acc;
-      } else {
+        int run = incl - own;  // keys above this lane's first digit
+        int hit_d = -1, hit_acc = 0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          if (hit_d < 0 && run + c[v] >= krem[q]) { hit_d = 255 - 4 * lane - v; hit_acc = run; }
+          run += c[v];
+        }
+        // the first lane (highest digits) that reaches krem owns the digit
+        const unsigned long long hit = __ballot(hit_d >= 0);
+        const int src = hit ? __ffsll((long long)hit) - 1 : 63;
+        int d = __shfl(hit_d, src, 64), acc = __shfl(hit_acc, src, 64);
+        if (!hit) { d = 0; acc = __shfl(incl, 63, 64) - s_hist[q][0]; }
+        if (lane == 0) {
+          s_pref[q] = prefix[q] | ((uint32_t)d << shift);
+          s_krem[q] = krem[q] - acc;
+        }
+      } else if (lane == 0) {
         s_pref[q] = prefix[q];
         s_krem[q] = krem[q];
       }
@@ -446,29 +475,61 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   const bool on1 = kk[0] > 0, on2 = kk[1] > 0;
   const int L = (n + kSelThreads - 1) / kSelThreads;
   const int lo = min(n, tid * L), hi = min(n, lo + L);
+  // Each thread owns the consecutive keys [lo, hi); up to kSegKeys of them
+  // are held in registers across the three passes below (read once, all
+  // loads in flight together); longer segments are re-read per pass.
+  constexpr int kSegKeys = 32;
+  uint32_t seg[kSegKeys];
+  const bool in_regs = L <= kSegKeys;  // block-uniform
+  if (in_regs) {
+#pragma unroll
+    for (int v = 0; v < kSegKeys; ++v) seg[v] = lo + v < hi ? key[lo + v] : 0u;
+  }
   // pass 1: equal-to-threshold counts per segment, scanned
   int e1 = 0, e2 = 0;
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t u = key[i];
-    e1 += (u == T1);
-    e2 += (u == T2);
+  if (in_regs) {
+#pragma unroll
+    for (int v = 0; v < kSegKeys; ++v)
+      if (lo + v < hi) { e1 += (seg[v] == T1); e2 += (seg[v] == T2); }
+  } else {
+    for (int i = lo; i < hi; ++i) {
+      const uint32_t u = key[i];
+      e1 += (u == T1);
+      e2 += (u == T2);
+    }
   }
   int tot;
   int eb1 = block_excl_scan<kSelThreads>(e1, s_tmp, tot);
   int eb2 = block_excl_scan<kSelThreads>(e2, s_tmp, tot);
   // pass 2: classify, count main / evicted / seed per segment
   int c_top = 0, c_ev = 0, c_seed = 0;
+  auto classify = [&](uint32_t u, int& r1, int& r2, bool& top, bool& sel2) {
+    top = on1 && (u > T1 || (u == T1 && r1 < need1));
+    sel2 = on2 && (u > T2 || (u == T2 && r2 < need2));
+    r1 += (u == T1);
+    r2 += (u == T2);
+  };
   {
     int r1 = eb1, r2 = eb2;
-    for (int i = lo; i < hi; ++i) {
-      const uint32_t u = key[i];
-      const bool top = on1 && (u > T1 || (u == T1 && r1 < need1));
-      const bool sel2 = on2 && (u > T2 || (u == T2 && r2 < need2));
-      r1 += (u == T1);
-      r2 += (u == T2);
-      c_top += top;
-      c_ev += !top;
-      c_seed += (sel2 && !top);
+    if (in_regs) {
+#pragma unroll
+      for (int v = 0; v < kSegKeys; ++v) {
+        if (lo + v < hi) {
+          bool top, sel2;
+          classify(seg[v], r1, r2, top, sel2);
+          c_top += top;
+          c_ev += !top;
+          c_seed += (sel2 && !top);
+        }
+      }
+    } else {
+      for (int i = lo; i < hi; ++i) {
+        bool top, sel2;
+        classify(key[i], r1, r2, top, sel2);
+        c_top += top;
+        c_ev += !top;
+        c_seed += (sel2 && !top);
+      }
     }
   }
   int ob_top = block_excl_scan<kSelThreads>(c_top, s_tmp, tot);
@@ -479,15 +540,19 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   int32_t* seeds = a.seeds + (size_t)bh * a.Rcap;
   {
     int r1 = eb1, r2 = eb2;
-    for (int i = lo; i < hi; ++i) {
-      const uint32_t u = key[i];
-      const bool top = on1 && (u > T1 || (u == T1 && r1 < need1));
-      const bool sel2 = on2 && (u > T2 || (u == T2 && r2 < need2));
-      r1 += (u == T1);
-      r2 += (u == T2);
+    auto emit = [&](int i, uint32_t u) {
+      bool top, sel2;
+      classify(u, r1, r2, top, sel2);
       if (top) main_idx[ob_top++] = i;
       else elist[ob_ev++] = i;
       if (sel2 && !top) seeds[ob_seed++] = i;
+    };
+    if (in_regs) {
+#pragma unroll
+      for (int v = 0; v < kSegKeys; ++v)
+        if (lo + v < hi) emit(lo + v, seg[v]);
+    } else {
+      for (int i = lo; i < hi; ++i) emit(i, key[i]);
     }
   }
   // the protected recent window follows the top-scored tokens
