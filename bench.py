@@ -85,8 +85,9 @@ def source_hash(*paths):
 
 
 def traffic_from_profile(src_hash):
-    """HBM bytes per decode call measured by rocprofv3 counters, if the
-    committed measurement was taken on the current decode source."""
+    """Measured / algorithmic HBM bytes of the decode calls profiled with
+    rocprofv3 counters, if that measurement was taken on the current decode
+    source."""
     path = os.path.join(ROOT, "profiles", "decode_traffic.json")
     if not os.path.exists(path):
         return None
@@ -94,13 +95,14 @@ def traffic_from_profile(src_hash):
         rec = json.load(f)
     if rec.get("decode_source_sha256_16") != src_hash:
         return None
-    return rec.get("bytes_per_call")
+    return rec.get("bytes_per_call") / rec.get("algorithmic_bytes_per_call")
 
 
 def construction_mfma_from_profile(src_hash):
-    """MFMA utilisation (rocprofv3 MfmaUtil, percent) of the construction's
-    MFMA kernels, if the committed measurement was taken on the current
-    construction source."""
+    """MFMA use of the construction's MFMA kernels from the committed
+    rocprofv3 counters (busy percent, executed and algorithmic TFLOP/s, and
+    algorithmic flops over the 2.5 PF/s peak), if the measurement was taken on
+    the current construction source."""
     path = os.path.join(ROOT, "profiles", "construction_counters.json")
     if not os.path.exists(path):
         return None
@@ -109,7 +111,8 @@ def construction_mfma_from_profile(src_hash):
     if rec.get("build_source_sha256_16") != src_hash:
         return None
     ks = rec["kernels"]
-    return {k: {"mfma_util_pct": round(ks[k]["mfma_util_pct"], 1), "mfma_tflops": round(ks[k]["mfma_tflops"])}
+    return {k: {"mfma_busy_pct": round(ks[k]["mfma_util_pct"], 1), "executed_tflops": round(ks[k]["mfma_tflops"]),
+                "algorithmic_tflops": round(ks[k]["alg_tflops"]), "algorithmic_util_pct": round(ks[k]["alg_util_pct"], 1)}
             for k in ("lse_partial", "score_accum", "lloyd_assign") if k in ks}
 
 
@@ -324,7 +327,9 @@ def main():
     avg_bytes = dec_bytes_job / calls
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
     src = source_hash("paper_2607_29591_amd/csrc/decode.hip", "paper_2607_29591_amd/csrc/common.h")
-    traffic = traffic_from_profile(src)
+    traffic_ratio = traffic_from_profile(src)
+    # counter bytes of the profiled calls, scaled to this job's average call
+    traffic = traffic_ratio * avg_bytes if traffic_ratio is not None else None
     cmfma = construction_mfma_from_profile(
         source_hash("paper_2607_29591_amd/csrc/build.hip", "paper_2607_29591_amd/csrc/common.h"))
 
