@@ -25,6 +25,9 @@ Paper map (section / equation / algorithm):
   shared-softmax decode ..... Sec. 5.4, residual-logit, denominator, numerator
                               and output equations; App. D, Algorithm 2
   dynamic gate .............. Sec. 5.5.2, gate equation; App. A.3
+  validation proxy .......... Sec. 5.5.1, validation-loss and margin
+                              equations; App. D, Algorithm 1; App. B.3
+                              (grid, 96 fit / 32 validation queries, delta)
 
 Readings taken where the paper is silent (each also listed in the design
 notes of the repository):
@@ -46,7 +49,16 @@ notes of the repository):
       nearest-even; log-counts are fp32;
   R12 single-token residual entries reproduce full attention only with the
       gate held at 1 (g_min = 1);
-  R13 p_max covers every main slot, including tokens appended during decode.
+  R13 p_max covers every main slot, including tokens appended during decode;
+  R19 a grid fraction f gives the candidate count r = floor(f * b + 1/2);
+  R20 the validation queries are the last `val_rows` window positions of
+      every query head of the group, the fit queries the leading ones (96/32
+      at G = 4, w = 32, val_rows = 8); the fit queries alone score the tokens;
+  R21 validation queries are evaluated like decode queries: o_S attends to
+      the whole prefix [0, s), the candidate output to the whole compressed
+      cache, with the decode gate at the scalar threshold tau;
+  R22 the loss is the mean over validation queries of the squared L2 error;
+      among r > 0 the smallest loss wins, ties to the smaller r.
 """
 
 import math
@@ -58,6 +70,7 @@ __all__ = [
     "window_raw_scores", "pool5", "scored_length", "select_main",
     "lloyd", "lloyd_objective", "assign_nearest", "residual_entries",
     "build_head", "build_cache", "gate_value", "decode_head", "decode",
+    "candidate_counts", "proxy_choice", "validation_proxy",
 ]
 
 _F64 = np.float64
@@ -143,12 +156,14 @@ def scored_length(s, m, recent_window):
     return s - p
 
 
-def window_raw_scores(K, Qw):
+def window_raw_scores(K, Qw, fit_rows=None):
     """Per-key attention mass from the observation window.
 
     K  : [s, d] prefill keys of one KV head.
     Qw : [G, w, d] window queries of the G query heads sharing that KV head;
          row i of each head sits at position s - w + i.
+    fit_rows : if given, only the leading `fit_rows` positions of each head
+         take part (the fit queries of the validation proxy, R20).
     Returns raw[s]: raw[p] = sum over window rows t that can see p (p <= pos(t))
     of softmax_t[p], where softmax_t normalises over every key row t can see
     (R1), summed over the G heads of the group (R2).
@@ -157,10 +172,11 @@ def window_raw_scores(K, Qw):
     Qw = np.asarray(Qw, _F64)
     s, d = K.shape
     G, w, _ = Qw.shape
+    nr = w if fit_rows is None else fit_rows
     raw = np.zeros(s, dtype=_F64)
     for h in range(G):
-        a = (Qw[h] @ K.T) / math.sqrt(d)              # [w, s]
-        pos = s - w + np.arange(w)
+        a = (Qw[h, :nr] @ K.T) / math.sqrt(d)         # [nr, s]
+        pos = s - w + np.arange(nr)
         visible = np.arange(s)[None, :] <= pos[:, None]
         a = np.where(visible, a, -np.inf)
         a = a - a.max(axis=1, keepdims=True)
@@ -289,11 +305,12 @@ def residual_entries(KE, VE, assign, centers, r, d):
 # construction of one (layer, KV head) (App. D, Algorithm 1 with r given)
 # --------------------------------------------------------------------------
 
-def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16"):
+def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16", fit_rows=None):
     """Construct the main + residual layout for one (layer, KV head).
 
     K, V : [s, d] prefill keys/values (values already in the storage dtype).
-    Qw   : [G, w, d] window queries.
+    Qw   : [G, w, d] window queries (only the leading `fit_rows` positions of
+           each head score the tokens when given).
     Returns a dict with the scores, selection, Lloyd record and the cache
     rows in slot order: residual entries in slots [0, r), main tokens in
     slots [r, r + main_len).
@@ -309,7 +326,7 @@ def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16"):
         out["scores"] = np.zeros(0)
     else:
         n = scored_length(s, m, recent_window)
-        raw = window_raw_scores(K, Qw)
+        raw = window_raw_scores(K, Qw, fit_rows)
         out["raw"] = raw
         scores = pool5(raw[:n])
         out["scores"] = scores
@@ -459,3 +476,64 @@ def decode(q, kc, vc, logc, res_len, main_len, tau, alpha, g_min, beta, heads=No
         lse_r[b, h] = dbg["lse_res"]
         gate[b, h] = dbg["gate"]
     return out, lse_m, lse_r, gate
+
+
+# --------------------------------------------------------------------------
+# construction-time validation proxy (Sec. 5.5.1; App. D, Algorithm 1)
+# --------------------------------------------------------------------------
+
+def candidate_counts(budget, grid):
+    """Residual counts of the budget grid: r = floor(f * b + 1/2) (R19)."""
+    return [int(math.floor(f * budget + 0.5)) for f in grid]
+
+
+def proxy_choice(losses, counts, delta):
+    """r* = argmin over r > 0 of the validation loss (ties to the smaller r,
+    R22); it is chosen only if L_{r*} < (1 - delta) L_0 (margin equation),
+    else r = 0. `losses[i]` belongs to `counts[i]`; one count must be 0."""
+    i0 = counts.index(0)
+    best = None
+    for i, r in enumerate(counts):
+        if r <= 0:
+            continue
+        if best is None or losses[i] < losses[best] or (losses[i] == losses[best] and r < counts[best]):
+            best = i
+    if best is not None and losses[best] < (1.0 - delta) * losses[i0]:
+        return counts[best], best
+    return 0, i0
+
+
+def validation_proxy(K, V, Qw, budget, grid, recent_window, lloyd_iters, val_rows, delta,
+                     tau, alpha, g_min, beta, dtype="bf16"):
+    """Algorithm 1 for one (layer, KV head).
+
+    The fit queries (leading window positions) score the tokens once; for
+    each grid count r the cache is built with m = b - r, the validation
+    queries (trailing `val_rows` positions of every head) are decoded against
+    it with the gated shared softmax, and the loss is their mean squared
+    error against full attention over the whole prefix (R21, R22). Returns the
+    chosen r, the per-candidate losses and counts, and the chosen candidate's
+    build record.
+    """
+    K = np.asarray(K, _F64)
+    V = np.asarray(V, _F64)
+    Qw = np.asarray(Qw, _F64)
+    G, w, d = Qw.shape
+    fit = w - val_rows
+    counts = candidate_counts(budget, grid)
+    vq = Qw[:, fit:].reshape(-1, d)
+    target = [full_attention(q, K, V) for q in vq]
+    losses, recs = [], []
+    for r in counts:
+        rec = build_head(K, V, Qw, budget - r, r, recent_window, lloyd_iters, dtype, fit_rows=fit)
+        n = rec["main_len"]
+        kc, vc = rec["kc"], rec["vc"]
+        err = 0.0
+        for q, o in zip(vq, target):
+            out, _ = decode_head(q, kc[r:r + n], vc[r:r + n], kc[:r], vc[:r], rec["logc"],
+                                 tau, alpha, g_min, beta)
+            err += float(((out - o) ** 2).sum())
+        losses.append(err / len(vq))
+        recs.append(rec)
+    r_star, i = proxy_choice(losses, counts, delta)
+    return dict(r=r_star, losses=losses, counts=counts, record=recs[i], records=recs)
