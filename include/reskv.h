@@ -63,6 +63,9 @@ typedef struct {
   int32_t obs_window;    /* w: observation-window queries per q head, 1..S */
   int32_t recent_window; /* |P| before clamping to m: protected last tokens */
   int32_t lloyd_iters;   /* T >= 1: (assign, update) rounds, App. B.3 uses 4 */
+  int32_t fit_rows;      /* leading window rows per q head that score, 1..w;
+                            0 = all w. The validation proxy scores with the
+                            fit part only (Sec. 5.5.1) */
 } reskv_build_params_t;
 
 typedef struct {
@@ -80,8 +83,10 @@ typedef struct {
  * Steps, per (b, kv head): observation-window scores (App. B.2.2: window
  * queries at positions s-w..s-1 attend causally, softmax per row, summed
  * over the G query heads, 5-tap zero-padded pooling over the positions
- * before the protected window); main selection M = P u Top_{m-|P|}(scores)
- * with ties to the lower position (Sec. 5.2, main-selection equation);
+ * before the protected window; with fit_rows = f > 0 only the rows at
+ * s-w..s-w+f-1 score, the fit part of Sec. 5.5.1); main selection
+ * M = P u Top_{m-|P|}(scores) with ties to the lower position (Sec. 5.2,
+ * main-selection equation);
  * Lloyd partition of the evicted set E = S \ M into r groups, seeded by the
  * evicted tokens ranked k_top..k_top+r-1 (Sec. 5.3, partition objective;
  * App. B.3); entries = (mean key, mean value, count) of the final groups
@@ -128,6 +133,71 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
                                   const int32_t* seq_len_host,
                                   const int32_t* budget_host,
                                   const int32_t* res_count_host);
+
+typedef struct {
+  const double* grid_host;  /* [n_grid] budget fractions f in [0, 1); at least
+                               one is 0 (App. B.3: 0, .05, .10, .15, .20) */
+  int32_t n_grid;           /* 1..8 */
+  int32_t val_rows;         /* trailing window rows per q head held out for
+                               validation, 1..w-1; the other w - val_rows
+                               rows are the fit part (App. B.3: 8 of 32 at
+                               G = 4, i.e. 96 fit and 32 validation queries) */
+  float delta;              /* relative margin in [0, 1] (App. B.3: 0.01) */
+} reskv_proxy_params_t;
+
+/*
+ * reskv_build_cache_proxy - construction with the residual count chosen per
+ * (b, kv head) by the validation proxy (Sec. 5.5.1, validation-loss and
+ * margin equations; App. D, Algorithm 1).
+ *
+ * The fit rows (the leading w - val_rows rows of every query head's
+ * window) score the tokens once. For each grid fraction f the candidate
+ * count is r_f = floor(f * b + 1/2) and the candidate cache is built as by
+ * reskv_build_cache with res_count = r_f and fit_rows = w - val_rows. Every
+ * validation query q (the trailing val_rows rows of the G heads of the
+ * group, at their own window positions) is decoded against each candidate
+ * with the decode rule of reskv_decode_attn (gate at gate->tau_scalar;
+ * gate->tau is not read) and against the whole prefix [0, s) without
+ * compression, o_S(q); the candidate's loss is the mean over the G *
+ * val_rows queries of ||o_f(q) - o_S(q)||^2. With r* the count of least
+ * loss among r_f > 0 (ties to the smaller count), r* is kept when
+ * L(r*) < (1 - delta) * L(0), evaluated in fp32, else r = 0; the outputs
+ * then hold that candidate's cache, exactly as reskv_build_cache writes it.
+ *
+ *   params          as for reskv_build_cache; fit_rows must be 0 or
+ *                   w - val_rows
+ *   k, v, seq_len_host, q_obs, budget_host   as for reskv_build_cache
+ *   kc, vc, logc, main_idx, res_len, main_len  out, as for
+ *                   reskv_build_cache with res_len = the chosen r
+ *   val_loss        optional (NULL) out fp32 [B*Hkv, n_grid]: the loss of
+ *                   every candidate, in grid order
+ *   workspace       device scratch of reskv_build_proxy_workspace_size()
+ *                   bytes; it holds every candidate cache
+ *
+ * Every candidate must satisfy r_f < b and r_f <= Rcap.
+ * Returns RESKV_OK or an error code before launching anything.
+ */
+reskv_status_t reskv_build_cache_proxy(const reskv_shape_t* shape,
+                                       const reskv_build_params_t* params,
+                                       const reskv_proxy_params_t* proxy,
+                                       const reskv_gate_t* gate,
+                                       const void* k, const void* v,
+                                       const int32_t* seq_len_host,
+                                       const void* q_obs,
+                                       const int32_t* budget_host,
+                                       void* kc, void* vc, float* logc,
+                                       int32_t* main_idx,
+                                       int32_t* res_len, int32_t* main_len,
+                                       float* val_loss,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* Bytes of device workspace reskv_build_cache_proxy needs (0 if invalid). */
+size_t reskv_build_proxy_workspace_size(const reskv_shape_t* shape,
+                                        const reskv_build_params_t* params,
+                                        const reskv_proxy_params_t* proxy,
+                                        const int32_t* seq_len_host,
+                                        const int32_t* budget_host);
 
 /*
  * reskv_decode_attn - one decode step of shared-softmax attention for one

@@ -128,9 +128,12 @@ static reskv_status_t check_build(const reskv_shape_t* shape, const reskv_build_
     return fail(RESKV_ERR_INVALID_ARG, "obs_window %d outside [1, %d]", p->obs_window, p->max_seq_len);
   if (p->recent_window < 0) return fail(RESKV_ERR_INVALID_ARG, "recent_window must be >= 0");
   if (p->lloyd_iters < 1 || p->lloyd_iters > 64) return fail(RESKV_ERR_INVALID_ARG, "lloyd_iters %d outside [1, 64]", p->lloyd_iters);
-  if ((long long)p->obs_window * (shape->num_q_heads / shape->num_kv_heads) > 1024)
-    return fail(RESKV_ERR_UNSUPPORTED, "observation rows per KV head (G*w = %d) above 1024",
-                p->obs_window * (shape->num_q_heads / shape->num_kv_heads));
+  if (p->fit_rows < 0 || p->fit_rows > p->obs_window)
+    return fail(RESKV_ERR_INVALID_ARG, "fit_rows %d outside [0, obs_window=%d]", p->fit_rows, p->obs_window);
+  const int rows = p->fit_rows > 0 ? p->fit_rows : p->obs_window;
+  if ((long long)rows * (shape->num_q_heads / shape->num_kv_heads) > 1024)
+    return fail(RESKV_ERR_UNSUPPORTED, "scoring rows per KV head (G*%d = %d) above 1024", rows,
+                rows * (shape->num_q_heads / shape->num_kv_heads));
   if (shape->res_cap > 4096) return fail(RESKV_ERR_UNSUPPORTED, "res_cap %d above 4096", shape->res_cap);
   const int Hkv = shape->num_kv_heads;
   for (int b = 0; b < shape->batch; ++b) {
@@ -182,6 +185,83 @@ reskv_status_t reskv_build_cache(const reskv_shape_t* shape, const reskv_build_p
                               vc, logc, main_idx, res_len, main_len, dbg_scores, dbg_assign, workspace,
                               (hipStream_t)stream);
   if (e != hipSuccess) return fail(RESKV_ERR_HIP, "build launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+// Proxy arguments, then every candidate count through the construction
+// checks with the fit rows in place.
+static reskv_status_t check_proxy(const reskv_shape_t* shape, const reskv_build_params_t* p,
+                                  const reskv_proxy_params_t* x, const int32_t* seq_len, const int32_t* budget,
+                                  reskv_build_params_t* pf) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if (!p || !x) return fail(RESKV_ERR_INVALID_ARG, "params or proxy params is NULL");
+  if (!seq_len || !budget) return fail(RESKV_ERR_INVALID_ARG, "a host length array is NULL");
+  if (!x->grid_host) return fail(RESKV_ERR_INVALID_ARG, "grid_host is NULL");
+  if (x->n_grid < 1 || x->n_grid > kProxyMaxGrid)
+    return fail(RESKV_ERR_INVALID_ARG, "n_grid %d outside [1, %d]", x->n_grid, kProxyMaxGrid);
+  bool has_zero = false;
+  for (int c = 0; c < x->n_grid; ++c) {
+    const double f = x->grid_host[c];
+    if (!(f >= 0.0 && f < 1.0)) return fail(RESKV_ERR_INVALID_ARG, "grid[%d] = %g outside [0, 1)", c, f);
+    has_zero |= f == 0.0;
+  }
+  if (!has_zero) return fail(RESKV_ERR_INVALID_ARG, "the grid must contain the fraction 0 (the pure-main cache)");
+  if (x->val_rows < 1 || x->val_rows >= p->obs_window)
+    return fail(RESKV_ERR_INVALID_ARG, "val_rows %d outside [1, obs_window - 1 = %d]", x->val_rows,
+                p->obs_window - 1);
+  if (p->fit_rows != 0 && p->fit_rows != p->obs_window - x->val_rows)
+    return fail(RESKV_ERR_INVALID_ARG, "fit_rows %d must be 0 or obs_window - val_rows = %d", p->fit_rows,
+                p->obs_window - x->val_rows);
+  if (!(x->delta >= 0.f && x->delta <= 1.f)) return fail(RESKV_ERR_INVALID_ARG, "delta %g outside [0, 1]", x->delta);
+  *pf = *p;
+  pf->fit_rows = p->obs_window - x->val_rows;
+  const int Hkv = shape->num_kv_heads;
+  std::vector<int32_t> counts((size_t)shape->batch * Hkv);
+  for (int c = 0; c < x->n_grid; ++c) {
+    for (int b = 0; b < shape->batch; ++b) {
+      const double r = floor(x->grid_host[c] * (double)budget[b] + 0.5);
+      if (budget[b] >= 1 && r >= budget[b])
+        return fail(RESKV_ERR_INVALID_ARG, "grid[%d] = %g gives r = %.0f >= budget[%d] = %d", c, x->grid_host[c],
+                    r, b, budget[b]);
+      for (int h = 0; h < Hkv; ++h) counts[(size_t)b * Hkv + h] = (int32_t)r;
+    }
+    if ((st = check_build(shape, pf, seq_len, budget, counts.data())) != RESKV_OK) return st;
+  }
+  return RESKV_OK;
+}
+
+size_t reskv_build_proxy_workspace_size(const reskv_shape_t* shape, const reskv_build_params_t* params,
+                                        const reskv_proxy_params_t* proxy, const int32_t* seq_len_host,
+                                        const int32_t* budget_host) {
+  reskv_build_params_t pf;
+  if (check_proxy(shape, params, proxy, seq_len_host, budget_host, &pf) != RESKV_OK) return 0;
+  ProxyPlan plan;
+  if (!make_proxy_plan(*shape, pf, *proxy, seq_len_host, budget_host, &plan)) return 0;
+  return plan.bytes;
+}
+
+reskv_status_t reskv_build_cache_proxy(const reskv_shape_t* shape, const reskv_build_params_t* params,
+                                       const reskv_proxy_params_t* proxy, const reskv_gate_t* gate, const void* k,
+                                       const void* v, const int32_t* seq_len_host, const void* q_obs,
+                                       const int32_t* budget_host, void* kc, void* vc, float* logc,
+                                       int32_t* main_idx, int32_t* res_len, int32_t* main_len, float* val_loss,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  reskv_build_params_t pf;
+  reskv_status_t st = check_proxy(shape, params, proxy, seq_len_host, budget_host, &pf);
+  if (st != RESKV_OK) return st;
+  if ((st = check_gate(gate)) != RESKV_OK) return st;
+  if (!k || !v || !q_obs || !kc || !vc || !logc || !main_idx || !res_len || !main_len)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  ProxyPlan plan;
+  if (!make_proxy_plan(*shape, pf, *proxy, seq_len_host, budget_host, &plan))
+    return fail(RESKV_ERR_UNSUPPORTED, "proxy plan could not be formed for these sizes");
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(RESKV_ERR_WORKSPACE, "proxy build needs %zu workspace bytes, got %zu", plan.bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  hipError_t e = launch_build_proxy(*shape, pf, *proxy, *gate, plan, k, v, seq_len_host, q_obs, budget_host, kc, vc,
+                                    logc, main_idx, res_len, main_len, val_loss, workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "proxy build launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 

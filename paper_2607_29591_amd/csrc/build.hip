@@ -85,6 +85,7 @@ struct BuildArgs {
   int32_t* ccount;     // [BH][Rcap]
   int32_t* order;      // [BH][S]   evicted positions grouped by centre
   int B, Hq, Hkv, G, C, Rcap, S, w, R, NCH, NBLK, T;
+  int wr;              // leading window rows per query head that score (R = G * wr)
   float scale2;        // log2(e) / sqrt(d)
 };
 
@@ -93,7 +94,8 @@ __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ void store_elem(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
 __device__ __forceinline__ void store_elem(float* p, float x) { *p = x; }
 
-// Window row t = h*w + i of the group: query head kvh*G + h, position s-w+i.
+// Scoring row t = h*wr + i of the group: query head kvh*G + h, window row i
+// (position s-w+i); only the leading wr rows of each head's window score.
 // Rows [r0, r0 + nrows) are copied into LDS with rows of D*sizeof(T) + 16
 // bytes (the pad keeps MFMA fragment reads free of bank conflicts); rows at
 // or past R are zero.
@@ -106,7 +108,7 @@ __device__ __forceinline__ void stage_window_rows(unsigned char* s_q, const Buil
     const int rr = x / kPieces, pc = x % kPieces, t = r0 + rr;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (t < a.R) {
-      const int h = t / a.w, i = t % a.w;
+      const int h = t / a.wr, i = t % a.wr;
       const T* q = static_cast<const T*>(a.q_obs) + (((size_t)b * a.Hq + kvh * a.G + h) * a.w + i) * D;
       v = reinterpret_cast<const uint4*>(q)[pc];
     }
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
           const int t_row = r0 + 16 * rt + col;  // window row of this lane's column
           Frag<T, D> qf;
           qf.load(reinterpret_cast<const T*>(s_q + (16 * rt + col) * kQRowB), grp);
-          const int pos = t_row < a.R ? hm.s - a.w + t_row % a.w : -1;
+          const int pos = t_row < a.R ? hm.s - a.w + t_row % a.wr : -1;
           // raw logits; the scale is positive, so the max commutes with it
           float v[16];
           float m = kNegInf;
@@ -298,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
           for (int i = 0; i < 4; ++i) {
             const int tl = 16 * rt + 4 * grp + i, t = r0 + tl;
             lse[i] = t < a.R ? s_lse[tl] : __builtin_huge_valf();
-            pos[i] = t < a.R ? hm.s - a.w + t % a.w : -1;  // padded rows see no key
+            pos[i] = t < a.R ? hm.s - a.w + t % a.wr : -1;  // padded rows see no key
           }
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
@@ -976,15 +978,6 @@ __host__ __device__ inline HeadMeta make_meta(int s, int r, int budget, int rece
   return m;
 }
 
-void head_meta(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
-               const int32_t* budget, const int32_t* res_count, std::vector<HeadMeta>& out) {
-  const int Hkv = s.num_kv_heads;
-  out.resize((size_t)s.batch * Hkv);
-  for (int b = 0; b < s.batch; ++b)
-    for (int h = 0; h < Hkv; ++h)
-      out[(size_t)b * Hkv + h] = make_meta(seq_len[b], res_count[b * Hkv + h], budget[b], p.recent_window);
-}
-
 // Per-head sizes travel as kernel arguments (copied at launch), in chunks.
 constexpr int kMetaChunk = 256;
 struct MetaChunk {
@@ -997,20 +990,62 @@ __global__ void meta_kernel(HeadMeta* meta, MetaChunk c) {
   if (i < c.count) meta[c.first + i] = make_meta(c.s[i], c.r[i], c.budget[i], c.recent);
 }
 
+// Arguments of every construction kernel; `meta` and the outputs belong to
+// the candidate being built, the scratch to the plan's workspace.
+BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const void* q_obs, const HeadMeta* meta,
+                    const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, void* workspace) {
+  char* ws = static_cast<char*>(workspace);
+  BuildArgs a{};
+  a.k = k; a.v = v; a.q_obs = q_obs;
+  a.kc = out.kc; a.vc = out.vc; a.logc = out.logc; a.main_idx = out.main_idx;
+  a.res_len = out.res_len; a.main_len = out.main_len;
+  a.dbg_scores = dbg_scores; a.dbg_assign = dbg_assign;
+  a.meta = meta;
+  a.lse_part = reinterpret_cast<float2*>(ws + pl.off_lsep);
+  a.lse2 = reinterpret_cast<float*>(ws + pl.off_lse);
+  a.raw = reinterpret_cast<float*>(ws + pl.off_raw);
+  a.score = reinterpret_cast<float*>(ws + pl.off_score);
+  a.elist = reinterpret_cast<int32_t*>(ws + pl.off_elist);
+  a.seeds = reinterpret_cast<int32_t*>(ws + pl.off_seeds);
+  a.cent = reinterpret_cast<float*>(ws + pl.off_cent);
+  a.cent_hi = reinterpret_cast<uint16_t*>(ws + pl.off_chi);
+  a.cent_lo = reinterpret_cast<uint16_t*>(ws + pl.off_clo);
+  a.cnorm = reinterpret_cast<float*>(ws + pl.off_cnorm);
+  a.assign = reinterpret_cast<int32_t*>(ws + pl.off_assign);
+  a.hist = reinterpret_cast<int32_t*>(ws + pl.off_hist);
+  a.cstart = reinterpret_cast<int32_t*>(ws + pl.off_cstart);
+  a.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
+  a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
+  a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
+  a.wr = pl.wr; a.R = pl.R; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
+  a.scale2 = kLog2e / sqrtf((float)pl.D);
+  return a;
+}
+
+#define RESKV_CHECK() do { e = hipGetLastError(); if (e != hipSuccess) return e; } while (0)
+
+// Raw window scores of every scored position (lse, then weights summed).
 template <typename T, int D>
-hipError_t launch_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
+hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
+  auto grid = [&](int x) { return dim3(x < 1 ? 1 : x, pl.Hkv, pl.B); };
+  hipError_t e;
+  hipLaunchKernelGGL((lse_partial<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  return hipSuccess;
+}
+
+// Pooling, selection, gather and the Lloyd rounds of one candidate.
+template <typename T, int D>
+hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
   const dim3 bhg(1, pl.Hkv, pl.B);
   auto grid = [&](int x) { return dim3(x < 1 ? 1 : x, pl.Hkv, pl.B); };
   hipError_t e;
-#define RESKV_CHECK() do { e = hipGetLastError(); if (e != hipSuccess) return e; } while (0)
   if (a.dbg_assign) {
     hipLaunchKernelGGL(fill_i32, dim3(1024), dim3(256), 0, st, a.dbg_assign,
                        (size_t)pl.T * pl.B * pl.Hkv * pl.S, -1);
     RESKV_CHECK();
   }
-  hipLaunchKernelGGL((lse_partial<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
-  hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
-  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
   hipLaunchKernelGGL(pool5, grid((pl.S + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
   hipLaunchKernelGGL(select_kernel, bhg, dim3(kSelThreads), 0, st, a); RESKV_CHECK();
   const int rows = pl.max_main + pl.Rcap;
@@ -1029,32 +1064,47 @@ hipError_t launch_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st)
       RESKV_CHECK();
     }
   }
-#undef RESKV_CHECK
   return hipSuccess;
 }
 
+#undef RESKV_CHECK
+
 }  // namespace
 
-bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
-                     const int32_t* budget, const int32_t* res_count, BuildPlan* plan) {
-  std::vector<HeadMeta> hm;
-  head_meta(s, p, seq_len, budget, res_count, hm);
+void head_meta(const BuildPlan& pl, const int32_t* seq_len, const int32_t* budget, const int32_t* res_count,
+               int recent, std::vector<HeadMeta>& out) {
+  out.resize((size_t)pl.B * pl.Hkv);
+  for (int b = 0; b < pl.B; ++b)
+    for (int h = 0; h < pl.Hkv; ++h)
+      out[(size_t)b * pl.Hkv + h] = make_meta(seq_len[b], res_count[b * pl.Hkv + h], budget[b], recent);
+}
+
+void init_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, BuildPlan* plan) {
   BuildPlan& pl = *plan;
   pl = BuildPlan{};
   pl.B = s.batch; pl.Hq = s.num_q_heads; pl.Hkv = s.num_kv_heads; pl.G = s.num_q_heads / s.num_kv_heads;
   pl.D = s.head_dim; pl.C = s.slot_cap; pl.Rcap = s.res_cap; pl.S = p.max_seq_len; pl.w = p.obs_window;
-  pl.R = pl.G * pl.w; pl.T = p.lloyd_iters; pl.dtype = s.dtype;
-  if (pl.R > 1024 || pl.Rcap > 4096) return false;
-  int max_E = 0;
+  pl.wr = p.fit_rows > 0 ? p.fit_rows : p.obs_window;
+  pl.R = pl.G * pl.wr; pl.T = p.lloyd_iters; pl.dtype = s.dtype;
+}
+
+bool fold_build_plan(const std::vector<HeadMeta>& hm, BuildPlan* plan) {
+  BuildPlan& pl = *plan;
   for (const HeadMeta& m : hm) {
     if (m.s > pl.max_s) pl.max_s = m.s;
     if (m.main_len > pl.max_main) pl.max_main = m.main_len;
     if (m.r_eff > pl.max_reff) pl.max_reff = m.r_eff;
-    if (m.nE > max_E) max_E = m.nE;
+    if (m.nE > pl.max_E) pl.max_E = m.nE;
     if (m.main_len + m.r > pl.C) return false;
   }
+  return true;
+}
+
+bool layout_build_plan(BuildPlan* plan) {
+  BuildPlan& pl = *plan;
+  if (pl.R > 1024 || pl.Rcap > 4096) return false;
   pl.NCH = (pl.max_s + kKeyChunk - 1) / kKeyChunk;
-  pl.NBLK = (max_E + kTokBlock - 1) / kTokBlock;
+  pl.NBLK = (pl.max_E + kTokBlock - 1) / kTokBlock;
   if (pl.NBLK < 1) pl.NBLK = 1;
   const size_t BH = (size_t)pl.B * pl.Hkv;
   size_t off = 0;
@@ -1079,20 +1129,22 @@ bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, cons
   return true;
 }
 
-hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, const BuildPlan& pl,
-                        const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
-                        const int32_t* budget, const int32_t* res_count, void* kc, void* vc,
-                        float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
-                        float* dbg_scores, int32_t* dbg_assign, void* workspace,
-                        hipStream_t stream) {
-  char* ws = static_cast<char*>(workspace);
-  HeadMeta* meta = reinterpret_cast<HeadMeta*>(ws + pl.off_meta);
+bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
+                     const int32_t* budget, const int32_t* res_count, BuildPlan* plan) {
+  init_build_plan(s, p, plan);
+  std::vector<HeadMeta> hm;
+  head_meta(*plan, seq_len, budget, res_count, p.recent_window, hm);
+  return fold_build_plan(hm, plan) && layout_build_plan(plan);
+}
+
+hipError_t upload_meta(const BuildPlan& pl, const int32_t* seq_len, const int32_t* budget,
+                       const int32_t* res_count, int recent, HeadMeta* meta, hipStream_t stream) {
   const int BH = pl.B * pl.Hkv;
   for (int first = 0; first < BH; first += kMetaChunk) {
     MetaChunk c;
     c.first = first;
     c.count = BH - first < kMetaChunk ? BH - first : kMetaChunk;
-    c.recent = p.recent_window;
+    c.recent = recent;
     for (int i = 0; i < c.count; ++i) {
       const int bh = first + i, b = bh / pl.Hkv;
       c.s[i] = seq_len[b];
@@ -1103,32 +1155,42 @@ hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, c
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  BuildArgs a{};
-  a.k = k; a.v = v; a.q_obs = q_obs; a.kc = kc; a.vc = vc; a.logc = logc; a.main_idx = main_idx;
-  a.res_len = res_len; a.main_len = main_len; a.dbg_scores = dbg_scores; a.dbg_assign = dbg_assign;
-  a.meta = meta;
-  a.lse_part = reinterpret_cast<float2*>(ws + pl.off_lsep);
-  a.lse2 = reinterpret_cast<float*>(ws + pl.off_lse);
-  a.raw = reinterpret_cast<float*>(ws + pl.off_raw);
-  a.score = reinterpret_cast<float*>(ws + pl.off_score);
-  a.elist = reinterpret_cast<int32_t*>(ws + pl.off_elist);
-  a.seeds = reinterpret_cast<int32_t*>(ws + pl.off_seeds);
-  a.cent = reinterpret_cast<float*>(ws + pl.off_cent);
-  a.cent_hi = reinterpret_cast<uint16_t*>(ws + pl.off_chi);
-  a.cent_lo = reinterpret_cast<uint16_t*>(ws + pl.off_clo);
-  a.cnorm = reinterpret_cast<float*>(ws + pl.off_cnorm);
-  a.assign = reinterpret_cast<int32_t*>(ws + pl.off_assign);
-  a.hist = reinterpret_cast<int32_t*>(ws + pl.off_hist);
-  a.cstart = reinterpret_cast<int32_t*>(ws + pl.off_cstart);
-  a.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
-  a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
-  a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
-  a.R = pl.R; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
-  a.scale2 = kLog2e / sqrtf((float)pl.D);
-  const bool bf = s.dtype == RESKV_BF16;
-  if (pl.D == 128) return bf ? launch_typed<uint16_t, 128>(pl, a, stream) : launch_typed<float, 128>(pl, a, stream);
-  if (pl.D == 64) return bf ? launch_typed<uint16_t, 64>(pl, a, stream) : launch_typed<float, 64>(pl, a, stream);
+  return hipSuccess;
+}
+
+hipError_t launch_build_scores(const BuildPlan& pl, const void* k, const void* q_obs, const HeadMeta* meta,
+                               void* workspace, hipStream_t stream) {
+  const BuildArgs a = make_args(pl, k, nullptr, q_obs, meta, BuildOut{}, nullptr, nullptr, workspace);
+  const bool bf = pl.dtype == RESKV_BF16;
+  if (pl.D == 128) return bf ? launch_scores_typed<uint16_t, 128>(pl, a, stream) : launch_scores_typed<float, 128>(pl, a, stream);
+  if (pl.D == 64) return bf ? launch_scores_typed<uint16_t, 64>(pl, a, stream) : launch_scores_typed<float, 64>(pl, a, stream);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_build_candidate(const BuildPlan& pl, const void* k, const void* v, const HeadMeta* meta,
+                                  const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                                  hipStream_t stream) {
+  const BuildArgs a = make_args(pl, k, v, nullptr, meta, out, dbg_scores, dbg_assign, workspace);
+  const bool bf = pl.dtype == RESKV_BF16;
+  if (pl.D == 128) return bf ? launch_candidate_typed<uint16_t, 128>(pl, a, stream) : launch_candidate_typed<float, 128>(pl, a, stream);
+  if (pl.D == 64) return bf ? launch_candidate_typed<uint16_t, 64>(pl, a, stream) : launch_candidate_typed<float, 64>(pl, a, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, const BuildPlan& pl,
+                        const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
+                        const int32_t* budget, const int32_t* res_count, void* kc, void* vc,
+                        float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
+                        float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                        hipStream_t stream) {
+  (void)s;
+  HeadMeta* meta = reinterpret_cast<HeadMeta*>(static_cast<char*>(workspace) + pl.off_meta);
+  hipError_t e = upload_meta(pl, seq_len, budget, res_count, p.recent_window, meta, stream);
+  if (e != hipSuccess) return e;
+  e = launch_build_scores(pl, k, q_obs, meta, workspace, stream);
+  if (e != hipSuccess) return e;
+  const BuildOut out{kc, vc, logc, main_idx, res_len, main_len};
+  return launch_build_candidate(pl, k, v, meta, out, dbg_scores, dbg_assign, workspace, stream);
 }
 
 }  // namespace reskv

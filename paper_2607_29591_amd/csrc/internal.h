@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "../../include/reskv.h"
 
 namespace reskv {
@@ -46,16 +48,48 @@ struct HeadMeta {
 };
 
 struct BuildPlan {
-  int B, Hq, Hkv, G, D, C, Rcap, S, w, R, T, dtype;
+  int B, Hq, Hkv, G, D, C, Rcap, S, w, T, dtype;
+  int wr;     // leading window rows per query head that score
+  int R;      // scoring rows per kv head, G * wr
   int NCH;    // scoring key chunks of the longest sequence
   int NBLK;   // 256-token blocks of the largest evicted set
-  int max_s, max_main, max_reff;
+  int max_s, max_main, max_reff, max_E;
   size_t off_meta, off_lsep, off_lse, off_raw, off_score, off_elist, off_seeds, off_cent, off_chi,
       off_clo, off_cnorm, off_assign, off_hist, off_cstart, off_ccount, off_order, bytes;
 };
 
+// Device buffers one construction writes.
+struct BuildOut {
+  void* kc;
+  void* vc;
+  float* logc;
+  int32_t* main_idx;
+  int32_t* res_len;
+  int32_t* main_len;
+};
+
 bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
                      const int32_t* budget, const int32_t* res_count, BuildPlan* plan);
+
+// Plan pieces: sizes from the shape, maxima over one or more sets of head
+// sizes (several candidate counts fold into one plan), workspace layout.
+void init_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, BuildPlan* plan);
+void head_meta(const BuildPlan& pl, const int32_t* seq_len, const int32_t* budget, const int32_t* res_count,
+               int recent, std::vector<HeadMeta>& out);
+bool fold_build_plan(const std::vector<HeadMeta>& hm, BuildPlan* plan);
+bool layout_build_plan(BuildPlan* plan);
+
+// Writes the head sizes of res_count[B*Hkv] to meta[B*Hkv] on the stream.
+hipError_t upload_meta(const BuildPlan& pl, const int32_t* seq_len, const int32_t* budget,
+                       const int32_t* res_count, int recent, HeadMeta* meta, hipStream_t stream);
+// Raw window scores into the workspace, for the scored positions of `meta`.
+hipError_t launch_build_scores(const BuildPlan& pl, const void* k, const void* q_obs, const HeadMeta* meta,
+                               void* workspace, hipStream_t stream);
+// Pooling, selection, gather and Lloyd rounds from the workspace's raw
+// scores, for the counts of `meta`, writing `out`.
+hipError_t launch_build_candidate(const BuildPlan& pl, const void* k, const void* v, const HeadMeta* meta,
+                                  const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                                  hipStream_t stream);
 
 hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, const BuildPlan& plan,
                         const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
@@ -63,6 +97,43 @@ hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, c
                         float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
                         float* dbg_scores, int32_t* dbg_assign, void* workspace,
                         hipStream_t stream);
+
+// Validation proxy (Sec. 5.5.1; App. D, Algorithm 1).
+constexpr int kProxyMaxGrid = 8;
+
+struct ProxyPlan {
+  BuildPlan build;          // scratch of one candidate build, sized for every candidate
+  int NG;                   // candidates
+  int val;                  // validation rows per query head
+  int GV;                   // validation queries per kv head, G * val
+  int NQC, GC;              // query chunks of at most 16 queries, queries per chunk
+  std::vector<int32_t> counts;  // [NG][B*Hkv] candidate counts
+  std::vector<int32_t> r_max;   // [B*Hkv] largest candidate count (its scored positions cover all)
+  DecodePlan dec_full, dec_cand;
+  size_t off_meta;          // [NG + 1][B*Hkv] HeadMeta (candidates, then scoring)
+  size_t off_kc, off_vc;    // [NG*B][Hkv][C][d]
+  size_t off_logc;          // [NG*B][Hkv][Rcap]
+  size_t off_midx;          // [NG*B][Hkv][C]
+  size_t off_rlen, off_mlen;    // [NG*B*Hkv]
+  size_t off_rlen0, off_mlen0, off_logc0;  // [B*Hkv] lengths of the uncompressed prefix
+  size_t off_q;             // [NQC][NG*B][Hkv*GC][d] validation queries
+  size_t off_out_full;      // [NQC][B][Hkv*GC][d] fp32
+  size_t off_out_cand;      // [NQC][NG*B][Hkv*GC][d] fp32
+  size_t off_dec;           // decode split-K scratch
+  size_t off_loss;          // [NG][B*Hkv] fp32
+  size_t off_choice;        // [B*Hkv] int32
+  size_t bytes;
+};
+
+bool make_proxy_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const reskv_proxy_params_t& x,
+                     const int32_t* seq_len, const int32_t* budget, ProxyPlan* plan);
+
+hipError_t launch_build_proxy(const reskv_shape_t& s, const reskv_build_params_t& p,
+                              const reskv_proxy_params_t& x, const reskv_gate_t& g, const ProxyPlan& pl,
+                              const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
+                              const int32_t* budget, void* kc, void* vc, float* logc, int32_t* main_idx,
+                              int32_t* res_len, int32_t* main_len, float* val_loss, void* workspace,
+                              hipStream_t stream);
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

@@ -36,7 +36,13 @@ class Shape(ctypes.Structure):
 
 class BuildParams(ctypes.Structure):
     _fields_ = [("max_seq_len", ctypes.c_int32), ("obs_window", ctypes.c_int32),
-                ("recent_window", ctypes.c_int32), ("lloyd_iters", ctypes.c_int32)]
+                ("recent_window", ctypes.c_int32), ("lloyd_iters", ctypes.c_int32),
+                ("fit_rows", ctypes.c_int32)]
+
+
+class ProxyParams(ctypes.Structure):
+    _fields_ = [("grid_host", ctypes.POINTER(ctypes.c_double)), ("n_grid", ctypes.c_int32),
+                ("val_rows", ctypes.c_int32), ("delta", ctypes.c_float)]
 
 
 class Gate(ctypes.Structure):
@@ -52,6 +58,11 @@ _SIG = {
                                          _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_build_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
                                                      _P, _P, _P]),
+    "reskv_build_cache_proxy": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
+                                               ctypes.POINTER(ProxyParams), ctypes.POINTER(Gate), _P, _P, _P, _P,
+                                               _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "reskv_build_proxy_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
+                                                           ctypes.POINTER(ProxyParams), _P, _P]),
     "reskv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
                                          _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_decode_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape)]),
@@ -128,6 +139,32 @@ def reskv_build_cache(shape, params, k, v, seq_len, q_obs, budget, res_count, kc
                                    _ptr(res_len), _ptr(main_len), _ptr(dbg_scores), _ptr(dbg_assign),
                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
                                    _stream(stream)))
+
+
+def make_proxy(grid=(0.0, 0.05, 0.10, 0.15, 0.20), val_rows=8, delta=0.01):
+    """Proxy parameters; the grid array lives on the returned object."""
+    g = (ctypes.c_double * len(grid))(*[float(f) for f in grid])
+    x = ProxyParams(ctypes.cast(g, ctypes.POINTER(ctypes.c_double)), len(grid), val_rows, delta)
+    x._grid = g  # keep the host array alive with the struct
+    return x
+
+
+def reskv_build_proxy_workspace_size(shape, params, proxy, seq_len, budget):
+    sl, slp = _host_i32(seq_len)
+    bu, bup = _host_i32(budget)
+    return lib().reskv_build_proxy_workspace_size(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(proxy),
+                                                  slp, bup)
+
+
+def reskv_build_cache_proxy(shape, params, proxy, gate, k, v, seq_len, q_obs, budget, kc, vc, logc, main_idx,
+                            res_len, main_len, workspace, val_loss=None, stream=None):
+    sl, slp = _host_i32(seq_len)
+    bu, bup = _host_i32(budget)
+    _check(lib().reskv_build_cache_proxy(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(proxy),
+                                         ctypes.byref(gate), _ptr(k), _ptr(v), slp, _ptr(q_obs), bup, _ptr(kc),
+                                         _ptr(vc), _ptr(logc), _ptr(main_idx), _ptr(res_len), _ptr(main_len),
+                                         _ptr(val_loss), _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def reskv_decode_workspace_size(shape):

@@ -42,16 +42,18 @@ class HostView:
         return self.t[idx].float().cpu().numpy().astype(np.float64)
 
 
-def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=False, host_cache=True):
+def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=False, host_cache=True, fit=0,
+              res=None):
     """Build one layer on the GPU; returns host numpy copies of the outputs
-    (and the device tensors under "dev" when keep_device is set)."""
+    (and the device tensors under "dev" when keep_device is set). `fit` > 0
+    scores with the leading `fit` window rows only; `res` overrides x["res"]."""
     B, Hkv, d = wl.batch, wl.hkv, wl.d
     S = x["K"].shape[2]
     C, Rcap = wl.slot_cap, wl.res_cap
     T = wl.lloyd_iters if iters is None else iters
     shape = rk.make_shape(B, wl.hq, Hkv, d, wl.dtype, C, Rcap)
-    params = rk.BuildParams(S, wl.window, wl.window if recent is None else recent, T)
-    res = np.asarray(x["res"], np.int32).reshape(-1)
+    params = rk.BuildParams(S, wl.window, wl.window if recent is None else recent, T, fit)
+    res = np.asarray(x["res"] if res is None else res, np.int32).reshape(-1)
     K = x["K"] if torch.is_tensor(x["K"]) else to_dev(x["K"], wl.dtype)
     V = x["V"] if torch.is_tensor(x["V"]) else to_dev(x["V"], wl.dtype)
     Q = x["q_obs"] if torch.is_tensor(x["q_obs"]) else to_dev(x["q_obs"], wl.dtype)
@@ -94,13 +96,14 @@ def ulp(x, dtype):
     return np.maximum(x, 1e-30) * 2.0 ** -23
 
 
-def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True):
-    """All construction checks for one (b, kv head). Returns a report dict."""
+def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True, fit=None, r=None):
+    """All construction checks for one (b, kv head). Returns a report dict.
+    `fit` = leading window rows that scored (None: all); `r` overrides x["res"]."""
     recent = wl.window if recent is None else recent
     T = wl.lloyd_iters if iters is None else iters
     G = wl.group
     s = int(x["seq_len"][b])
-    r = int(x["res"][b][h])
+    r = int(x["res"][b][h]) if r is None else int(r)
     m = int(x["budget"][b]) - r
     K = np.asarray(x["K_host"][b, h, :s], np.float64)
     V = np.asarray(x["V_host"][b, h, :s], np.float64)
@@ -119,7 +122,7 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
     gs = got["scores"][b, h, :n]
     # (ii) score parity
     if full_oracle:
-        raw = orc.window_raw_scores(K, Qw)
+        raw = orc.window_raw_scores(K, Qw, fit)
         ref = orc.pool5(raw[:n])
         err = np.abs(gs - ref)
         assert (err <= SCORE_RTOL * np.abs(ref) + 1e-30).all(), \

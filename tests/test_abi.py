@@ -102,3 +102,63 @@ def test_decode_rejects_small_workspace_and_bad_gate(L):
     with pytest.raises(rk.ReskvError) as ei:
         rk.reskv_decode_attn(shape(), rk.make_gate(), None, t, t, t, t, t, t, t, stream=FakeStream())
     assert ei.value.status == 1
+
+
+def build_args(**kw):
+    d = dict(S=300, w=16, recent=16, T=4, fit=0, seq=(300,), budget=(64,))
+    d.update(kw)
+    sh = rk.make_shape(1, 4, 2, 64, "f32", 64, 13)
+    return sh, rk.BuildParams(d["S"], d["w"], d["recent"], d["T"], d["fit"]), d["seq"], d["budget"]
+
+
+def test_build_workspace_and_fit_rows(L):
+    sh, p, seq, bud = build_args()
+    n_all = rk.reskv_build_workspace_size(sh, p, seq, bud, [13, 0])
+    assert n_all > 0
+    sh, p, seq, bud = build_args(fit=12)
+    n_fit = rk.reskv_build_workspace_size(sh, p, seq, bud, [13, 0])
+    assert 0 < n_fit <= n_all  # fewer scoring rows, no larger lse partials
+    for fit in (-1, 17):
+        sh, p, seq, bud = build_args(fit=fit)
+        assert rk.reskv_build_workspace_size(sh, p, seq, bud, [13, 0]) == 0
+
+
+GRID = (0.0, 0.05, 0.10, 0.15, 0.20)
+
+
+@pytest.mark.parametrize("grid,val,delta,fit", [
+    ((0.05, 0.1), 4, 0.01, 0),       # no zero fraction
+    ((0.0, 1.0), 4, 0.01, 0),        # f >= 1
+    ((0.0, float("nan")), 4, 0.01, 0),
+    ((0.0, 0.5), 4, 0.01, 0),        # r = 32 above res_cap 13
+    ((0.0, 0.1), 16, 0.01, 0),       # no fit rows left
+    ((0.0, 0.1), 0, 0.01, 0),        # no validation rows
+    ((0.0, 0.1), 4, 1.5, 0),         # delta outside [0, 1]
+    ((0.0, 0.1), 4, 0.01, 10),       # fit rows disagree with w - val_rows
+    ((0.0,) * 9, 4, 0.01, 0),        # more than 8 candidates
+])
+def test_proxy_rejects_bad_arguments(L, grid, val, delta, fit):
+    sh, p, seq, bud = build_args(fit=fit)
+    x = rk.make_proxy(grid, val, delta)
+    assert rk.reskv_build_proxy_workspace_size(sh, p, x, seq, bud) == 0
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_build_cache_proxy(sh, p, x, rk.make_gate(), t, t, seq, t, bud, t, t, t, t, t, t, t,
+                                   stream=FakeStream())
+    assert ei.value.status == 1
+    assert rk.last_error()
+
+
+def test_proxy_workspace_holds_every_candidate(L):
+    sh, p, seq, bud = build_args()
+    x = rk.make_proxy(GRID, 4, 0.01)
+    n = rk.reskv_build_proxy_workspace_size(sh, p, x, seq, bud)
+    # at least the five candidate caches (K and V, 2 heads x 64 slots x 64 fp32)
+    assert n >= 5 * 2 * 2 * 64 * 64 * 4
+    sh2, p2, _, _ = build_args(fit=12)  # the fit rows may also be given explicitly
+    assert rk.reskv_build_proxy_workspace_size(sh2, p2, x, seq, bud) == n
+    t = FakeTensor(8)
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_build_cache_proxy(sh, p, x, rk.make_gate(), t, t, seq, t, bud, t, t, t, t, t, t, t,
+                                   stream=FakeStream())
+    assert ei.value.status == 3
