@@ -13,8 +13,9 @@ which runs reskv_decode_attn for all 32 layers with that step's token
 appended inside the call.
 value = decode tokens (batch x layers x decode steps) / step time.
 
-Also reported: decode-only throughput and HBM GB/s, construction GB/s, the
-roofline of the decode kernels (algorithmic bytes per call / average call
+Also reported: decode-only throughput and HBM GB/s, construction GB/s,
+construction with the validation proxy choosing r (ms per layer, untimed
+in the job), the roofline of the decode kernels (algorithmic bytes per call / average call
 time from HIP events on the launch stream), and the fp64 oracle's throughput
 on the host cores over a bounded sample of the same job.
 
@@ -44,10 +45,12 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=25.0)
-    ap.add_argument("--mode", choices=["job", "decode"], default="job",
+    ap.add_argument("--mode", choices=["job", "decode", "proxy"], default="job",
                     help="job: the timed whole job (default); decode: build once, then only decode calls "
                          "(for rocprofv3 counter runs), preceded by one 256 MiB plain copy used to calibrate "
-                         "the byte counters")
+                         "the byte counters; proxy: only construction with the validation proxy, every layer")
+    ap.add_argument("--proxy-layers", type=int, default=2,
+                    help="layers built with the validation proxy after the timed job (0: skip)")
     return ap.parse_args()
 
 
@@ -114,6 +117,49 @@ def construction_mfma_from_profile(src_hash):
     return {k: {"mfma_busy_pct": round(ks[k]["mfma_util_pct"], 1), "executed_tflops": round(ks[k]["mfma_tflops"]),
                 "algorithmic_tflops": round(ks[k]["alg_tflops"]), "algorithmic_util_pct": round(ks[k]["alg_util_pct"], 1)}
             for k in ("lse_partial", "score_accum", "lloyd_assign") if k in ks}
+
+
+# Validation proxy settings of App. B.3: grid of budget fractions, 8 of the 32
+# window rows of every query head held out (96 fit / 32 validation queries at
+# G = 4), relative margin 0.01.
+PROXY_GRID = (0.0, 0.05, 0.10, 0.15, 0.20)
+PROXY_VAL_ROWS = 8
+PROXY_DELTA = 0.01
+
+
+def proxy_runs(rk, torch, wl, shape, layers, caches, n_layers, dev):
+    """Construction with the validation proxy for the first n_layers layers:
+    one untimed call, then every layer once between events on the launch
+    stream. Returns ms per layer and the chosen residual counts."""
+    import numpy as np
+    S = wl.max_ctx
+    params = rk.BuildParams(S, wl.window, wl.window, wl.lloyd_iters, 0)
+    xp = rk.make_proxy(PROXY_GRID, PROXY_VAL_ROWS, PROXY_DELTA)
+    gate = rk.make_gate(tau_scalar=0.25, alpha=wl.alpha, g_min=wl.g_min, beta=wl.beta)
+    nws = max(rk.reskv_build_proxy_workspace_size(shape, params, xp, layers[l]["seq_len"], layers[l]["budget"])
+              for l in range(n_layers))
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def call(l):
+        x, c = layers[l], caches[l]
+        rk.reskv_build_cache_proxy(shape, params, xp, gate, x["K"], x["V"], x["seq_len"], x["q_obs"], x["budget"],
+                                   c["kc"], c["vc"], c["logc"], c["main_idx"], c["res_len"], c["main_len"], ws)
+
+    call(0)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for l in range(n_layers):
+        call(l)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    chosen = np.concatenate([caches[l]["res_len"].cpu().numpy() for l in range(n_layers)])
+    counts = [int(np.floor(f * wl.budget[0] + 0.5)) for f in PROXY_GRID]
+    return dict(ms_per_layer=e0.elapsed_time(e1) / n_layers, layers_timed=n_layers,
+                workspace_bytes=nws, grid_counts=counts,
+                chosen_count_heads={str(r): int((chosen == r).sum()) for r in counts})
 
 
 def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
@@ -268,6 +314,11 @@ def main():
         ed.record(stream)
         return eb0, eb1, ed
 
+    if args.mode == "proxy":
+        pr = proxy_runs(rk, torch, wl, shape, layers, caches, L, dev)
+        print(json.dumps({"mode": "proxy", "layers": L, **pr}), flush=True)
+        return
+
     if args.mode == "decode":
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -366,6 +417,9 @@ def main():
                      "calls_timed": calls * args.steps},
         "setup_s": t_setup,
     }
+    if args.proxy_layers > 0:
+        # after the timed jobs: construction with the validation proxy choosing r
+        result["proxy_build"] = proxy_runs(rk, torch, wl, shape, layers, caches, min(args.proxy_layers, L), dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, layers[0], q_stage[0, 0], tau_stage[0, 0], res_layers,
                                               args.cpu_budget_s)
