@@ -28,6 +28,10 @@ Paper map (section / equation / algorithm):
   validation proxy .......... Sec. 5.5.1, validation-loss and margin
                               equations; App. D, Algorithm 1; App. B.3
                               (grid, 96 fit / 32 validation queries, delta)
+  alternative scorers ....... App. B.2.2 compared methods: H2O (accumulated
+                              attention of the observation queries, recent
+                              64) and TOVA (last-token window, recent 1),
+                              feeding the same selection and residual path
 
 Readings taken where the paper is silent (each also listed in the design
 notes of the repository):
@@ -58,7 +62,13 @@ notes of the repository):
       the whole prefix [0, s), the candidate output to the whole compressed
       cache, with the decode gate at the scalar threshold tau;
   R22 the loss is the mean over validation queries of the squared L2 error;
-      among r > 0 the smallest loss wins, ties to the smaller r.
+      among r > 0 the smallest loss wins, ties to the smaller r;
+  R23 H2O's accumulated attention of the observation queries is the raw
+      window score (R1, R2) without pooling (kernel 1), with 64 protected
+      recent tokens;
+  R24 TOVA's last-token window is w = 1 (the last prefill query of every
+      head of the group, summed by R2), without pooling, with 1 protected
+      recent token.
 """
 
 import math
@@ -67,7 +77,7 @@ import numpy as np
 
 __all__ = [
     "round_to_dtype", "full_attention", "evict_attention", "zn_stats",
-    "window_raw_scores", "pool5", "scored_length", "select_main",
+    "window_raw_scores", "pool", "pool5", "scored_length", "select_main",
     "lloyd", "lloyd_objective", "assign_nearest", "residual_entries",
     "build_head", "build_cache", "gate_value", "decode_head", "decode",
     "candidate_counts", "proxy_choice", "validation_proxy",
@@ -186,16 +196,26 @@ def window_raw_scores(K, Qw, fit_rows=None):
     return raw
 
 
-def pool5(raw):
-    """Centred 5-tap sum with zero padding (R3): out[p] = sum_{i=-2..2} raw[p+i]."""
+def pool(raw, kernel=5):
+    """Centred `kernel`-tap sum (odd kernel) with zero padding (R3):
+    out[p] = sum_{|i| <= kernel // 2} raw[p+i]; kernel 1 returns the raw
+    scores (the H2O and TOVA rules, R23, R24)."""
+    assert kernel >= 1 and kernel % 2 == 1
     raw = np.asarray(raw, _F64)
     n = raw.shape[0]
     out = np.zeros(n, dtype=_F64)
-    for off in range(-2, 3):
+    h = kernel // 2
+    for off in range(-h, h + 1):
         lo = max(0, -off)
         hi = min(n, n - off)
-        out[lo:hi] += raw[lo + off:hi + off]
+        if lo < hi:  # a shift of n or more positions leaves nothing inside
+            out[lo:hi] += raw[lo + off:hi + off]
     return out
+
+
+def pool5(raw):
+    """The SnapKV pooling of App. B.2.2: pool(raw, 5)."""
+    return pool(raw, 5)
 
 
 # --------------------------------------------------------------------------
@@ -305,12 +325,13 @@ def residual_entries(KE, VE, assign, centers, r, d):
 # construction of one (layer, KV head) (App. D, Algorithm 1 with r given)
 # --------------------------------------------------------------------------
 
-def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16", fit_rows=None):
+def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16", fit_rows=None, pool_kernel=5):
     """Construct the main + residual layout for one (layer, KV head).
 
     K, V : [s, d] prefill keys/values (values already in the storage dtype).
     Qw   : [G, w, d] window queries (only the leading `fit_rows` positions of
            each head score the tokens when given).
+    pool_kernel : taps of the score pooling (5: SnapKV; 1: H2O and TOVA).
     Returns a dict with the scores, selection, Lloyd record and the cache
     rows in slot order: residual entries in slots [0, r), main tokens in
     slots [r, r + main_len).
@@ -328,7 +349,7 @@ def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16", fit_row
         n = scored_length(s, m, recent_window)
         raw = window_raw_scores(K, Qw, fit_rows)
         out["raw"] = raw
-        scores = pool5(raw[:n])
+        scores = pool(raw[:n], pool_kernel)
         out["scores"] = scores
         main, evicted, seeds = select_main(scores, s, m, recent_window, r)
     out["main_idx"], out["evicted"], out["seeds"] = main, evicted, seeds
