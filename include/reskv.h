@@ -66,6 +66,11 @@ typedef struct {
   int32_t fit_rows;      /* leading window rows per q head that score, 1..w;
                             0 = all w. The validation proxy scores with the
                             fit part only (Sec. 5.5.1) */
+  int32_t pool_kernel;   /* taps of the centred zero-padded score pooling,
+                            odd, 1..31; 0 = 5. SnapKV (App. B.2.2) pools
+                            with 5; H2O (w window queries, recent 64) and
+                            TOVA (w = 1, recent 1) use 1 (App. B.2.2,
+                            compared methods) */
 } reskv_build_params_t;
 
 typedef struct {
@@ -82,8 +87,8 @@ typedef struct {
  *
  * Steps, per (b, kv head): observation-window scores (App. B.2.2: window
  * queries at positions s-w..s-1 attend causally, softmax per row, summed
- * over the G query heads, 5-tap zero-padded pooling over the positions
- * before the protected window; with fit_rows = f > 0 only the rows at
+ * over the G query heads, pool_kernel-tap (5 by default) zero-padded
+ * pooling over the positions before the protected window; with fit_rows = f > 0 only the rows at
  * s-w..s-w+f-1 score, the fit part of Sec. 5.5.1); main selection
  * M = P u Top_{m-|P|}(scores) with ties to the lower position (Sec. 5.2,
  * main-selection equation);

@@ -128,6 +128,8 @@ static reskv_status_t check_build(const reskv_shape_t* shape, const reskv_build_
     return fail(RESKV_ERR_INVALID_ARG, "obs_window %d outside [1, %d]", p->obs_window, p->max_seq_len);
   if (p->recent_window < 0) return fail(RESKV_ERR_INVALID_ARG, "recent_window must be >= 0");
   if (p->lloyd_iters < 1 || p->lloyd_iters > 64) return fail(RESKV_ERR_INVALID_ARG, "lloyd_iters %d outside [1, 64]", p->lloyd_iters);
+  if (p->pool_kernel < 0 || p->pool_kernel > 31 || (p->pool_kernel > 0 && p->pool_kernel % 2 == 0))
+    return fail(RESKV_ERR_INVALID_ARG, "pool_kernel %d must be 0 (= 5) or odd in [1, 31]", p->pool_kernel);
   if (p->fit_rows < 0 || p->fit_rows > p->obs_window)
     return fail(RESKV_ERR_INVALID_ARG, "fit_rows %d outside [0, obs_window=%d]", p->fit_rows, p->obs_window);
   const int rows = p->fit_rows > 0 ? p->fit_rows : p->obs_window;

@@ -9,7 +9,8 @@
 //   lse_final      merges the chunk partials into one log-sum-exp per row
 //   score_accum    recomputes the logits; raw[p] = sum over rows of the
 //                  normalised weight of key p, for the scored positions
-//   pool5          5-tap zero-padded sum over the scored positions
+//   pool_scores    centred zero-padded sum (5 taps by default) over the
+//                  scored positions
 //   select         radix select (4 x 8-bit digits of the fp32 bit pattern) of
 //                  the k_top-th and (k_top + r')-th largest score; ties at a
 //                  threshold go to the lower position. Stable compaction writes
@@ -86,6 +87,7 @@ struct BuildArgs {
   int32_t* order;      // [BH][S]   evicted positions grouped by centre
   int B, Hq, Hkv, G, C, Rcap, S, w, R, NCH, NBLK, T;
   int wr;              // leading window rows per query head that score (R = G * wr)
+  int pool_half;       // pooling taps on each side of a position
   float scale2;        // log2(e) / sqrt(d)
 };
 
@@ -338,7 +340,9 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
   }
 }
 
-__global__ __launch_bounds__(kThreads) void pool5(BuildArgs a) {
+// Centred (2 * pool_half + 1)-tap sum with zero padding over the scored
+// positions (5 taps for the SnapKV rule, 1 for H2O and TOVA).
+__global__ __launch_bounds__(kThreads) void pool_scores(BuildArgs a) {
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
@@ -349,11 +353,8 @@ __global__ __launch_bounds__(kThreads) void pool5(BuildArgs a) {
   float v = -1.f;
   if (p < n) {
     v = 0.f;
-#pragma unroll
-    for (int o = -2; o <= 2; ++o) {
-      const int q = p + o;
-      if (q >= 0 && q < n) v += raw[q];
-    }
+    const int lo = max(p - a.pool_half, 0), hi = min(p + a.pool_half, n - 1);
+    for (int q = lo; q <= hi; ++q) v += raw[q];
     a.score[(size_t)bh * a.S + p] = v;
   }
   if (a.dbg_scores) a.dbg_scores[(size_t)bh * a.S + p] = v;
@@ -1017,7 +1018,7 @@ BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const voi
   a.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
   a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
   a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
-  a.wr = pl.wr; a.R = pl.R; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
+  a.wr = pl.wr; a.pool_half = pl.pool_half; a.R = pl.R; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
   a.scale2 = kLog2e / sqrtf((float)pl.D);
   return a;
 }
@@ -1046,7 +1047,7 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
                        (size_t)pl.T * pl.B * pl.Hkv * pl.S, -1);
     RESKV_CHECK();
   }
-  hipLaunchKernelGGL(pool5, grid((pl.S + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(pool_scores, grid((pl.S + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
   hipLaunchKernelGGL(select_kernel, bhg, dim3(kSelThreads), 0, st, a); RESKV_CHECK();
   const int rows = pl.max_main + pl.Rcap;
   const int gblocks = (rows * (D * (int)sizeof(T) / 16) + kThreads - 1) / kThreads;
@@ -1085,6 +1086,7 @@ void init_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, Buil
   pl.B = s.batch; pl.Hq = s.num_q_heads; pl.Hkv = s.num_kv_heads; pl.G = s.num_q_heads / s.num_kv_heads;
   pl.D = s.head_dim; pl.C = s.slot_cap; pl.Rcap = s.res_cap; pl.S = p.max_seq_len; pl.w = p.obs_window;
   pl.wr = p.fit_rows > 0 ? p.fit_rows : p.obs_window;
+  pl.pool_half = (p.pool_kernel > 0 ? p.pool_kernel : 5) / 2;
   pl.R = pl.G * pl.wr; pl.T = p.lloyd_iters; pl.dtype = s.dtype;
 }
 

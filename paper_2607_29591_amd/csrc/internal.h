@@ -50,6 +50,7 @@ struct HeadMeta {
 struct BuildPlan {
   int B, Hq, Hkv, G, D, C, Rcap, S, w, T, dtype;
   int wr;     // leading window rows per query head that score
+  int pool_half;  // score pooling taps on each side
   int R;      // scoring rows per kv head, G * wr
   int NCH;    // scoring key chunks of the longest sequence
   int NBLK;   // 256-token blocks of the largest evicted set

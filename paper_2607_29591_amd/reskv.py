@@ -37,7 +37,7 @@ class Shape(ctypes.Structure):
 class BuildParams(ctypes.Structure):
     _fields_ = [("max_seq_len", ctypes.c_int32), ("obs_window", ctypes.c_int32),
                 ("recent_window", ctypes.c_int32), ("lloyd_iters", ctypes.c_int32),
-                ("fit_rows", ctypes.c_int32)]
+                ("fit_rows", ctypes.c_int32), ("pool_kernel", ctypes.c_int32)]
 
 
 class ProxyParams(ctypes.Structure):

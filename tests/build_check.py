@@ -43,16 +43,17 @@ class HostView:
 
 
 def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=False, host_cache=True, fit=0,
-              res=None):
+              res=None, pool=0):
     """Build one layer on the GPU; returns host numpy copies of the outputs
     (and the device tensors under "dev" when keep_device is set). `fit` > 0
-    scores with the leading `fit` window rows only; `res` overrides x["res"]."""
+    scores with the leading `fit` window rows only; `res` overrides x["res"];
+    `pool` is the pooling kernel (0: the default 5)."""
     B, Hkv, d = wl.batch, wl.hkv, wl.d
     S = x["K"].shape[2]
     C, Rcap = wl.slot_cap, wl.res_cap
     T = wl.lloyd_iters if iters is None else iters
     shape = rk.make_shape(B, wl.hq, Hkv, d, wl.dtype, C, Rcap)
-    params = rk.BuildParams(S, wl.window, wl.window if recent is None else recent, T, fit)
+    params = rk.BuildParams(S, wl.window, wl.window if recent is None else recent, T, fit, pool)
     res = np.asarray(x["res"] if res is None else res, np.int32).reshape(-1)
     K = x["K"] if torch.is_tensor(x["K"]) else to_dev(x["K"], wl.dtype)
     V = x["V"] if torch.is_tensor(x["V"]) else to_dev(x["V"], wl.dtype)
@@ -96,9 +97,10 @@ def ulp(x, dtype):
     return np.maximum(x, 1e-30) * 2.0 ** -23
 
 
-def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True, fit=None, r=None):
+def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True, fit=None, r=None, pool=5):
     """All construction checks for one (b, kv head). Returns a report dict.
-    `fit` = leading window rows that scored (None: all); `r` overrides x["res"]."""
+    `fit` = leading window rows that scored (None: all); `r` overrides
+    x["res"]; `pool` = pooling kernel."""
     recent = wl.window if recent is None else recent
     T = wl.lloyd_iters if iters is None else iters
     G = wl.group
@@ -123,7 +125,7 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
     # (ii) score parity
     if full_oracle:
         raw = orc.window_raw_scores(K, Qw, fit)
-        ref = orc.pool5(raw[:n])
+        ref = orc.pool(raw[:n], pool)
         err = np.abs(gs - ref)
         assert (err <= SCORE_RTOL * np.abs(ref) + 1e-30).all(), \
             f"score err {(err / np.maximum(np.abs(ref), 1e-30)).max():.2e}"

@@ -162,3 +162,10 @@ def test_proxy_workspace_holds_every_candidate(L):
         rk.reskv_build_cache_proxy(sh, p, x, rk.make_gate(), t, t, seq, t, bud, t, t, t, t, t, t, t,
                                    stream=FakeStream())
     assert ei.value.status == 3
+
+
+@pytest.mark.parametrize("pool,ok", [(0, True), (1, True), (3, True), (31, True), (2, False), (33, False), (-1, False)])
+def test_build_pool_kernel_range(L, pool, ok):
+    sh = rk.make_shape(1, 4, 2, 64, "f32", 64, 13)
+    p = rk.BuildParams(300, 16, 16, 4, 0, pool)
+    assert (rk.reskv_build_workspace_size(sh, p, (300,), (64,), [13, 0]) > 0) == ok

@@ -111,3 +111,21 @@ def test_build_llama_layer_sampled():
         rep = check_head(wl, x, got, 0, h, full_oracle=full, replay=full)
         ties += rep["near_ties"]
     assert ties <= 1
+
+
+@pytest.mark.parametrize("scorer", ["h2o", "tova", "pool3"])
+def test_build_alternative_scorers(scorer):
+    """The compared scorers of App. B.2.2 through the same selection and
+    residual path: H2O (accumulated window attention, no pooling, 64 recent
+    tokens), TOVA (last-token window w = 1, no pooling, 1 recent token), and
+    a 3-tap pooling; ragged lengths, G = 4, bf16, d = 128."""
+    window, recent, pool = {"h2o": (8, 64, 1), "tova": (1, 1, 1), "pool3": (8, 8, 3)}[scorer]
+    wl = synth.tiny_workload(s=900, d=128, hq=8, hkv=2, budget=160, res=0, window=window, dtype="bf16", batch=2,
+                             n_heavy=6)
+    wl.ctx = [900, 517]
+    wl.res = np.array([[[24, 0], [40, 7]]])
+    x = host_copies(synth.gen_layer(wl, 0, seed=21, n_decode=1))
+    got = run_build(wl, x, recent=recent, pool=pool)
+    for b in range(2):
+        for h in range(2):
+            check_head(wl, x, got, b, h, recent=recent, pool=pool)
