@@ -28,6 +28,10 @@ Paper map (section / equation / algorithm):
   validation proxy .......... Sec. 5.5.1, validation-loss and margin
                               equations; App. D, Algorithm 1; App. B.3
                               (grid, 96 fit / 32 validation queries, delta)
+  two-branch decode ......... Sec. 6.1 (main branch and residual branch
+                              merged through log-sum-exp statistics);
+                              Sec. 6.6 ablation table (separate
+                              normalisations, reading R25)
   alternative scorers ....... App. B.2.2 compared methods: H2O (accumulated
                               attention of the observation queries, recent
                               64) and TOVA (last-token window, recent 1),
@@ -68,7 +72,12 @@ notes of the repository):
       recent tokens;
   R24 TOVA's last-token window is w = 1 (the last prefill query of every
       head of the group, summed by R2), without pooling, with 1 protected
-      recent token.
+      recent token;
+  R25 the ablation with separate main and residual normalisations mixes the
+      two separately normalised branch outputs by the gate,
+      (1 - g) o_main + g o_res (g = 0 without populated entries); the paper
+      does not print its formula, so this variant is parity unpinned against
+      the paper and pinned only to its own limits.
 """
 
 import math
@@ -77,6 +86,7 @@ import numpy as np
 
 __all__ = [
     "round_to_dtype", "full_attention", "evict_attention", "zn_stats",
+    "decode_branches", "merge_branches",
     "window_raw_scores", "pool", "pool5", "scored_length", "select_main",
     "lloyd", "lloyd_objective", "assign_nearest", "residual_entries",
     "build_head", "build_cache", "gate_value", "decode_head", "decode",
@@ -466,6 +476,58 @@ def decode_head(q, Kmain, Vmain, Kres, Vres, logc, tau, alpha, g_min, beta):
     else:
         lse_res = -np.inf
     return out, dict(lse_main=lse_main, lse_res=lse_res, gate=g, p_max=p_max)
+
+
+def decode_branches(q, Kmain, Vmain, Kres, Vres, logc, beta):
+    """The two branches of one decode query, each under its own softmax
+    (Sec. 6.1: a fused main-branch kernel returns its output and per-query
+    log-sum-exp; the residual branch is evaluated over the entries):
+      o_main = softmax(a) V_main,  lse_main = log sum_p e^{a_p};
+      o_res  = softmax(at) Vbar,   lse_res  = log sum_j e^{at_j},
+    with at_j = <q, kbar_j>/sqrt(d) + beta log c_j (no gate). Empty entries
+    are left out; with none populated o_res = 0 and lse_res = -inf.
+    """
+    q = np.asarray(q, _F64)
+    d = q.shape[0]
+    a = (np.asarray(Kmain, _F64) @ q) / math.sqrt(d)
+    top = a.max()
+    w = np.exp(a - top)
+    o_main = (w @ np.asarray(Vmain, _F64)) / w.sum()
+    lse_main = top + math.log(w.sum())
+    logc = np.asarray(logc, _F64)
+    live = np.isfinite(logc)
+    if not live.any():
+        return o_main, lse_main, np.zeros(d), -np.inf
+    at = (np.asarray(Kres, _F64)[live] @ q) / math.sqrt(d) + beta * logc[live]
+    t = at.max()
+    u = np.exp(at - t)
+    o_res = (u @ np.asarray(Vres, _F64)[live]) / u.sum()
+    return o_main, lse_main, o_res, t + math.log(u.sum())
+
+
+def merge_branches(o_main, lse_main, o_res, lse_res, g, mode):
+    """Combine the two branches.
+
+    "shared": the log-sum-exp merge with the residual mass scaled by the
+    gate, (e^{lse_main} o_main + g e^{lse_res} o_res) / (e^{lse_main} +
+    g e^{lse_res}) -- the shared softmax of Sec. 5.4 written over branch
+    statistics (Sec. 6.1).
+    "separate": the ablation without the shared softmax (Sec. 6.6, ablation
+    table): each branch keeps its own normalisation and the gate mixes the
+    two, (1 - g) o_main + g o_res, with g taken as 0 when no entry is
+    populated (reading R25).
+    """
+    o_main = np.asarray(o_main, _F64)
+    o_res = np.asarray(o_res, _F64)
+    if mode == "separate":
+        gg = g if np.isfinite(lse_res) else 0.0
+        return (1.0 - gg) * o_main + gg * o_res
+    assert mode == "shared"
+    lr = lse_res + math.log(g) if (g > 0 and np.isfinite(lse_res)) else -np.inf
+    top = max(lse_main, lr)
+    wm = math.exp(lse_main - top)
+    wr = math.exp(lr - top) if np.isfinite(lr) else 0.0
+    return (wm * o_main + wr * o_res) / (wm + wr)
 
 
 def decode(q, kc, vc, logc, res_len, main_len, tau, alpha, g_min, beta, heads=None):
