@@ -253,6 +253,59 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
 size_t reskv_decode_workspace_size(const reskv_shape_t* shape);
 
 /*
+ * reskv_decode_branches - the two branches of one decode step, each under
+ * its own softmax: the form in which a fused main-branch attention kernel
+ * and a separately evaluated residual branch are combined through
+ * log-sum-exp statistics (Sec. 6.1 implementation notes). With a_p and the
+ * gate g as for reskv_decode_attn and at_j = <q, kbar_j>/sqrt(d) +
+ * beta * logc_j (no gate):
+ *   out_main = sum_p e^{a_p} v_p / sum_p e^{a_p},   lse_main = log sum_p e^{a_p}
+ *   out_res  = sum_j e^{at_j} vbar_j / sum_j e^{at_j}, lse_res = log sum_j e^{at_j}
+ * (out_res = 0 and lse_res = -inf when no entry is populated).
+ *
+ *   q, kc, vc, logc, res_len, main_len  as for reskv_decode_attn (no append)
+ *   out_main, out_res   [B, Hq, d] fp32
+ *   lse_main, lse_res, gate_out  [B*Hq] fp32
+ *   workspace           reskv_decode_workspace_size() bytes
+ * Returns RESKV_OK or an error code before launching anything.
+ */
+reskv_status_t reskv_decode_branches(const reskv_shape_t* shape,
+                                     const reskv_gate_t* gate,
+                                     const void* q,
+                                     const void* kc, const void* vc,
+                                     const float* logc,
+                                     const int32_t* res_len,
+                                     const int32_t* main_len,
+                                     float* out_main, float* lse_main,
+                                     float* out_res, float* lse_res,
+                                     float* gate_out,
+                                     void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
+typedef enum {
+  RESKV_MERGE_SHARED = 0,   /* log-sum-exp merge: the shared softmax */
+  RESKV_MERGE_SEPARATE = 1  /* separate normalisations mixed by the gate */
+} reskv_merge_mode_t;
+
+/*
+ * reskv_merge_branches - combine the outputs of reskv_decode_branches.
+ *   RESKV_MERGE_SHARED: out = (e^{lse_main} out_main + g e^{lse_res} out_res)
+ *     / (e^{lse_main} + g e^{lse_res}), which is reskv_decode_attn's output
+ *     (Sec. 5.4 output equation over branch statistics, Sec. 6.1).
+ *   RESKV_MERGE_SEPARATE: out = (1 - g) out_main + g out_res, g taken as 0
+ *     where lse_res = -inf: the ablation without the shared softmax
+ *     (Sec. 6.6 ablation table; the paper gives no formula, this mixture is
+ *     this library's reading of it).
+ * All arrays fp32 on the device, shapes as for reskv_decode_branches; out
+ * [B, Hq, d] may alias neither input.
+ */
+reskv_status_t reskv_merge_branches(const reskv_shape_t* shape, int32_t mode,
+                                    const float* out_main, const float* lse_main,
+                                    const float* out_res, const float* lse_res,
+                                    const float* gate, float* out,
+                                    void* stream);
+
+/*
  * reskv_append_kv - append one decode token per (b, kv head) as a main slot
  * (Sec. 3.1: each decode step appends the new token's key and value).
  * Writes k_new/v_new [B, Hkv, d] into slot res_len + main_len and increments

@@ -106,6 +106,45 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t*
   return ok();
 }
 
+reskv_status_t reskv_decode_branches(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
+                                     const void* kc, const void* vc, const float* logc, const int32_t* res_len,
+                                     const int32_t* main_len, float* out_main, float* lse_main, float* out_res,
+                                     float* lse_res, float* gate_out, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if ((st = check_gate(gate)) != RESKV_OK) return st;
+  if (!q || !kc || !vc || !logc || !res_len || !main_len || !out_main || !lse_main || !out_res || !lse_res ||
+      !gate_out)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  const DecodePlan plan = make_decode_plan(*shape);
+  if ((size_t)plan.GP * plan.P * sizeof(float) > decode_max_lds_weights())
+    return fail(RESKV_ERR_UNSUPPORTED, "%d split-K records per head do not fit the combine", plan.P);
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(RESKV_ERR_WORKSPACE, "decode needs %zu workspace bytes, got %zu", plan.bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  hipError_t e = launch_decode_branches(*shape, *gate, plan, q, kc, vc, logc, res_len, main_len, out_main, lse_main,
+                                        out_res, lse_res, gate_out, workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+reskv_status_t reskv_merge_branches(const reskv_shape_t* shape, int32_t mode, const float* out_main,
+                                    const float* lse_main, const float* out_res, const float* lse_res,
+                                    const float* gate, float* out, void* stream) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if (mode != RESKV_MERGE_SHARED && mode != RESKV_MERGE_SEPARATE)
+    return fail(RESKV_ERR_INVALID_ARG, "merge mode %d is neither SHARED (0) nor SEPARATE (1)", mode);
+  if (!out_main || !lse_main || !out_res || !lse_res || !gate || !out)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  if (out == out_main || out == out_res) return fail(RESKV_ERR_INVALID_ARG, "out must not alias a branch output");
+  hipError_t e = launch_merge_branches(*shape, mode, out_main, lse_main, out_res, lse_res, gate, out,
+                                       (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "merge launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 reskv_status_t reskv_append_kv(const reskv_shape_t* shape, const void* k_new, const void* v_new, void* kc,
                                void* vc, const int32_t* res_len, int32_t* main_len, void* stream) {
   reskv_status_t st = check_shape(shape);

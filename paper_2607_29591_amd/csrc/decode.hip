@@ -62,6 +62,7 @@ struct DecodeArgs {
   float* dbg_lse_main;
   float* dbg_lse_res;
   float* dbg_gate;
+  float* out_res;   // two-branch mode: the residual branch's own output (out = the main branch's)
   int Hq, Hkv, G, C, Rcap, PR, P;
   float qk_scale;   // log2(e) / sqrt(d)
   float beta_log2;  // beta * log2(e)
@@ -454,6 +455,97 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
 }
 
 
+// Two-branch combine: the split records of each kind are merged under that
+// kind's own softmax. out = main-branch output, out_res = residual-branch
+// output (0 without populated entries), dbg_lse_main / dbg_lse_res their
+// natural log-sum-exp (the residual one without the gate), dbg_gate the gate.
+template <int D, int GP>
+__global__ __launch_bounds__(kThreads) void decode_branches(DecodeArgs a) {
+  extern __shared__ float s_w[];  // [GP][P] weights of the records
+  const int kvh = blockIdx.x, b = blockIdx.y;
+  const int bh = b * a.Hkv + kvh;
+  int r, n;
+  cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  const int nRC = (r + kChunk - 1) / kChunk, nMC = (n + kChunk - 1) / kChunk;
+  const float* ml = a.part_ml + (size_t)bh * a.P * GP * 2;
+  const float* pacc = a.part_acc + (size_t)bh * a.P * GP * D;
+  const int tid = threadIdx.x, lane16 = tid & 15, h = tid >> 4;
+  if (h < a.G) {
+    float mM = kNegInf, mR = kNegInf;
+    for (int q = lane16; q < nMC; q += 16) mM = fmaxf(mM, ml[((a.PR + q) * GP + h) * 2]);
+    for (int q = lane16; q < nRC; q += 16) mR = fmaxf(mR, ml[(q * GP + h) * 2]);
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) { mM = wave_xor_max(mM, msk); mR = wave_xor_max(mR, msk); }
+    float lM = 0.f, lR = 0.f;
+    for (int q = lane16; q < nMC; q += 16) {
+      const float* e = ml + ((a.PR + q) * GP + h) * 2;
+      if (e[0] != kNegInf) lM = fmaf(e[1], exp2f(e[0] - mM), lM);
+    }
+    for (int q = lane16; q < nRC; q += 16) {
+      const float* e = ml + (q * GP + h) * 2;
+      if (e[0] != kNegInf) lR = fmaf(e[1], exp2f(e[0] - mR), lR);
+    }
+#pragma unroll
+    for (int msk = 1; msk < 16; msk <<= 1) { lM = wave_xor_add(lM, msk); lR = wave_xor_add(lR, msk); }
+    const float pmax = lM > 0.f ? 1.f / lM : 1.f;
+    const int qh = b * a.Hq + kvh * a.G + h;
+    const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
+    const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
+    const float invM = lM > 0.f ? 1.f / lM : 0.f, invR = lR > 0.f ? 1.f / lR : 0.f;
+    for (int q = lane16; q < nMC; q += 16) {
+      const float m = ml[((a.PR + q) * GP + h) * 2];
+      s_w[h * a.P + a.PR + q] = m != kNegInf ? exp2f(m - mM) * invM : 0.f;
+    }
+    for (int q = lane16; q < nRC; q += 16) {
+      const float m = ml[(q * GP + h) * 2];
+      s_w[h * a.P + q] = m != kNegInf ? exp2f(m - mR) * invR : 0.f;
+    }
+    if (lane16 == 0) {
+      a.dbg_lse_main[qh] = lM > 0.f ? (mM + log2f(lM)) * kLn2 : kNegInf;
+      a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
+      a.dbg_gate[qh] = g;
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < a.G * D; idx += kThreads) {
+    const int hh = idx / D, d = idx % D;
+    const float* w = s_w + hh * a.P;
+    float oR = 0.f, oM = 0.f;
+    for (int q = 0; q < nRC; ++q) oR = fmaf(w[q], pacc[(q * GP + hh) * D + d], oR);
+    for (int q = 0; q < nMC; ++q) oM = fmaf(w[a.PR + q], pacc[((a.PR + q) * GP + hh) * D + d], oM);
+    const size_t o = ((size_t)b * a.Hq + kvh * a.G + hh) * D + d;
+    a.out[o] = oM;
+    a.out_res[o] = oR;
+  }
+}
+
+// Merge of the two branches, one thread per output element: the
+// log-sum-exp merge with the gated residual mass (mode 0), or the gate
+// mixture of the separately normalised branches (mode 1).
+__global__ __launch_bounds__(kThreads) void merge_branches_kernel(const float* o_main, const float* lse_main,
+                                                                  const float* o_res, const float* lse_res,
+                                                                  const float* gate, float* out, int mode,
+                                                                  size_t rows, int D) {
+  const size_t i = blockIdx.x * (size_t)kThreads + threadIdx.x;
+  if (i >= rows * D) return;
+  const size_t row = i / D;
+  const float g = gate[row], lm = lse_main[row], lr = lse_res[row];
+  const bool has_res = lr != kNegInf;
+  float v;
+  if (mode == 1) {
+    const float gg = has_res ? g : 0.f;
+    v = (1.f - gg) * o_main[i] + gg * o_res[i];
+  } else {
+    const float lrg = (has_res && g > 0.f) ? lr + logf(g) : kNegInf;
+    const float top = fmaxf(lm, lrg);
+    const float wm = lm != kNegInf ? expf(lm - top) : 0.f;
+    const float wr = lrg != kNegInf ? expf(lrg - top) : 0.f;
+    const float den = wm + wr;
+    v = den > 0.f ? (wm * o_main[i] + wr * o_res[i]) / den : 0.f;
+  }
+  out[i] = v;
+}
+
 // One block of 8 waves per (b, kv head): streams every slot of the head,
 // merges the wave states in LDS, applies the gate and writes the G outputs;
 // optionally appends this step's token first. Used when the (b, kv head)
@@ -633,7 +725,7 @@ __global__ void append_kernel(const T* k_new, const T* v_new, T* kc, T* vc, cons
 template <typename T, int D, int GP>
 hipError_t launch_typed(const DecodePlan& pl, const DecodeArgs& da, hipStream_t stream) {
   if constexpr (GP <= 4) {
-    if (pl.whole_head) {
+    if (pl.whole_head && !da.out_res) {
       hipLaunchKernelGGL((decode_head<T, D, GP>), dim3(pl.Hkv, pl.B), dim3(kHeadThreads), 0, stream, da);
       return hipGetLastError();
     }
@@ -642,7 +734,10 @@ hipError_t launch_typed(const DecodePlan& pl, const DecodeArgs& da, hipStream_t 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)GP * pl.P * sizeof(float);
-  hipLaunchKernelGGL((decode_combine<D, GP>), dim3(pl.Hkv, pl.B), dim3(kThreads), lds, stream, da);
+  if (da.out_res)
+    hipLaunchKernelGGL((decode_branches<D, GP>), dim3(pl.Hkv, pl.B), dim3(kThreads), lds, stream, da);
+  else
+    hipLaunchKernelGGL((decode_combine<D, GP>), dim3(pl.Hkv, pl.B), dim3(kThreads), lds, stream, da);
   return hipGetLastError();
 }
 
@@ -708,6 +803,39 @@ hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const De
   if (pl.D == 128) return bf ? launch_gp<uint16_t, 128>(pl, da, stream) : launch_gp<float, 128>(pl, da, stream);
   if (pl.D == 64) return bf ? launch_gp<uint16_t, 64>(pl, da, stream) : launch_gp<float, 64>(pl, da, stream);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_decode_branches(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& pl,
+                                  const void* q, const void* kc, const void* vc, const float* logc,
+                                  const int32_t* res_len, const int32_t* main_len, float* out_main,
+                                  float* lse_main, float* out_res, float* lse_res, float* gate_out,
+                                  void* workspace, hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  DecodeArgs da{};
+  da.q = q; da.kc = kc; da.vc = vc; da.logc = logc;
+  da.res_len = res_len; da.main_len = const_cast<int32_t*>(main_len);  // not written without an append
+  da.part_acc = reinterpret_cast<float*>(ws + pl.acc_off);
+  da.part_ml = reinterpret_cast<float*>(ws + pl.ml_off);
+  da.tau = g.tau; da.out = out_main; da.out_res = out_res;
+  da.dbg_lse_main = lse_main; da.dbg_lse_res = lse_res; da.dbg_gate = gate_out;
+  da.Hq = pl.Hq; da.Hkv = pl.Hkv; da.G = pl.G; da.C = pl.C; da.Rcap = pl.Rcap; da.PR = pl.PR; da.P = pl.P;
+  da.qk_scale = kLog2e / sqrtf((float)pl.D);
+  da.beta_log2 = g.beta * kLog2e;
+  da.tau_scalar = g.tau_scalar; da.alpha = g.alpha; da.g_min = g.g_min;
+  const bool bf = s.dtype == RESKV_BF16;
+  if (pl.D == 128) return bf ? launch_gp<uint16_t, 128>(pl, da, stream) : launch_gp<float, 128>(pl, da, stream);
+  if (pl.D == 64) return bf ? launch_gp<uint16_t, 64>(pl, da, stream) : launch_gp<float, 64>(pl, da, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_merge_branches(const reskv_shape_t& s, int mode, const float* out_main, const float* lse_main,
+                                 const float* out_res, const float* lse_res, const float* gate, float* out,
+                                 hipStream_t stream) {
+  const size_t rows = (size_t)s.batch * s.num_q_heads;
+  const size_t n = rows * s.head_dim;
+  hipLaunchKernelGGL(merge_branches_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                     stream, out_main, lse_main, out_res, lse_res, gate, out, mode, rows, s.head_dim);
+  return hipGetLastError();
 }
 
 hipError_t launch_append(const reskv_shape_t& s, const void* k_new, const void* v_new, void* kc,

@@ -29,6 +29,17 @@ hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const De
                          float* out, float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
                          void* workspace, hipStream_t stream);
 
+// The two branches of one decode step under their own softmax (split path).
+hipError_t launch_decode_branches(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& pl,
+                                  const void* q, const void* kc, const void* vc, const float* logc,
+                                  const int32_t* res_len, const int32_t* main_len, float* out_main,
+                                  float* lse_main, float* out_res, float* lse_res, float* gate_out,
+                                  void* workspace, hipStream_t stream);
+
+hipError_t launch_merge_branches(const reskv_shape_t& s, int mode, const float* out_main, const float* lse_main,
+                                 const float* out_res, const float* lse_res, const float* gate, float* out,
+                                 hipStream_t stream);
+
 hipError_t launch_append(const reskv_shape_t& s, const void* k_new, const void* v_new, void* kc,
                          void* vc, const int32_t* res_len, int32_t* main_len, hipStream_t stream);
 

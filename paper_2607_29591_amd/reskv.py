@@ -66,6 +66,9 @@ _SIG = {
     "reskv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
                                          _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_decode_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape)]),
+    "reskv_decode_branches": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
+                                             _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "reskv_merge_branches": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P]),
     "reskv_append_kv": (ctypes.c_int, [ctypes.POINTER(Shape), _P, _P, _P, _P, _P, _P, _P]),
     "reskv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "reskv_last_error": (ctypes.c_char_p, []),
@@ -177,6 +180,22 @@ def reskv_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, work
                                    _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(k_new), _ptr(v_new), _ptr(out),
                                    _ptr(dbg_lse_main), _ptr(dbg_lse_res), _ptr(dbg_gate), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+RESKV_MERGE_SHARED, RESKV_MERGE_SEPARATE = 0, 1
+
+
+def reskv_decode_branches(shape, gate, q, kc, vc, logc, res_len, main_len, out_main, lse_main, out_res, lse_res,
+                          gate_out, workspace, stream=None):
+    _check(lib().reskv_decode_branches(ctypes.byref(shape), ctypes.byref(gate), _ptr(q), _ptr(kc), _ptr(vc),
+                                       _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(out_main), _ptr(lse_main),
+                                       _ptr(out_res), _ptr(lse_res), _ptr(gate_out), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def reskv_merge_branches(shape, mode, out_main, lse_main, out_res, lse_res, gate, out, stream=None):
+    _check(lib().reskv_merge_branches(ctypes.byref(shape), int(mode), _ptr(out_main), _ptr(lse_main), _ptr(out_res),
+                                      _ptr(lse_res), _ptr(gate), _ptr(out), _stream(stream)))
 
 
 def reskv_append_kv(shape, k_new, v_new, kc, vc, res_len, main_len, stream=None):

@@ -169,3 +169,18 @@ def test_build_pool_kernel_range(L, pool, ok):
     sh = rk.make_shape(1, 4, 2, 64, "f32", 64, 13)
     p = rk.BuildParams(300, 16, 16, 4, 0, pool)
     assert (rk.reskv_build_workspace_size(sh, p, (300,), (64,), [13, 0]) > 0) == ok
+
+
+def test_merge_branches_rejects_bad_mode_and_alias(L):
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_merge_branches(shape(), 2, t, t, t, t, t, FakeTensor(), stream=FakeStream())
+    assert ei.value.status == 1
+
+
+def test_decode_branches_rejects_small_workspace(L):
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_decode_branches(shape(), rk.make_gate(), t, t, t, t, t, t, t, t, t, t, t, FakeTensor(8),
+                                 stream=FakeStream())
+    assert ei.value.status == 3

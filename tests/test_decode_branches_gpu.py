@@ -1,0 +1,103 @@
+"""GPU parity of reskv_decode_branches and reskv_merge_branches against the
+fp64 oracle: the two branches under their own softmax (Sec. 6.1: a fused
+main-branch kernel plus a residual branch, merged through log-sum-exp
+statistics), the log-sum-exp merge (which must reproduce reskv_decode_attn,
+Sec. 5.4) and the separate-normalisation ablation (Sec. 6.6 ablation table;
+reading R25).
+
+Bar: branch outputs and merges per (batch, query head) within the decode
+tolerance (1e-5 fp32 caches, 2e-3 bf16 caches, max relative error per row);
+log-sum-exps and the gate to 1e-5; the SHARED merge against
+reskv_decode_attn's own output on the same inputs within the same bar.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import reskv_oracle as orc
+from paper_2607_29591_amd import reskv as rk
+from tests.helpers import TOL, random_cache, rel_err_rows, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def run_case(seed, B, Hq, Hkv, d, dtype, C, Rcap, res, main, tau_kind="scalar", g_min=0.0):
+    rng = np.random.default_rng(seed)
+    kc, vc, logc = random_cache(rng, B, Hkv, C, Rcap, d, dtype, res, main)
+    q = rng.normal(size=(B, Hq, d)) * 1.5
+    q = torch.as_tensor(q, dtype=torch.float32)
+    q = (q.to(torch.bfloat16) if dtype == "bf16" else q).double().numpy()
+    tau = rng.normal(0.0, 0.5, size=(B, Hq)) if tau_kind == "normal" else None
+    gate_kw = dict(tau_scalar=0.25, alpha=12.0, g_min=g_min, beta=1.0)
+    shape = rk.make_shape(B, Hq, Hkv, d, dtype, C, Rcap)
+    qd, kcd, vcd = to_dev(q, dtype), to_dev(kc, dtype), to_dev(vc, dtype)
+    lcd = torch.as_tensor(np.asarray(logc, np.float32)).cuda()
+    rl = torch.as_tensor(np.asarray(res, np.int32).reshape(-1)).cuda()
+    ml = torch.as_tensor(np.asarray(main, np.int32).reshape(-1)).cuda()
+    taud = None if tau is None else torch.as_tensor(tau.astype(np.float32).reshape(-1)).cuda()
+    gate = rk.make_gate(tau=taud, **gate_kw)
+    ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    f = lambda *s: torch.full(s, float("nan"), device="cuda")
+    om, orr, lm, lr, gt = f(B, Hq, d), f(B, Hq, d), f(B * Hq), f(B * Hq), f(B * Hq)
+    rk.reskv_decode_branches(shape, gate, qd, kcd, vcd, lcd, rl, ml, om, lm, orr, lr, gt, ws)
+    shared, sep, direct = f(B, Hq, d), f(B, Hq, d), f(B, Hq, d)
+    rk.reskv_merge_branches(shape, rk.RESKV_MERGE_SHARED, om, lm, orr, lr, gt, shared)
+    rk.reskv_merge_branches(shape, rk.RESKV_MERGE_SEPARATE, om, lm, orr, lr, gt, sep)
+    rk.reskv_decode_attn(shape, gate, qd, kcd, vcd, lcd, rl, ml, direct, ws)
+    torch.cuda.synchronize()
+    got = {k: v.double().cpu().numpy() for k, v in
+           dict(om=om, orr=orr, lm=lm, lr=lr, g=gt, shared=shared, sep=sep, direct=direct).items()}
+    G = Hq // Hkv
+    tol = TOL[dtype]
+    worst = 0.0
+    for b in range(B):
+        for h in range(Hq):
+            kv = h // G
+            r, n = int(res[b][kv]), int(main[b][kv])
+            Km, Vm = kc[b, kv, r:r + n], vc[b, kv, r:r + n]
+            Kr, Vr, lc = kc[b, kv, :r], vc[b, kv, :r], logc[b, kv, :r]
+            t = 0.25 if tau is None else tau[b, h]
+            ref, dbg = orc.decode_head(q[b, h], Km, Vm, Kr, Vr, lc, t, 12.0, g_min, 1.0)
+            o_m, l_m, o_r, l_r = orc.decode_branches(q[b, h], Km, Vm, Kr, Vr, lc, 1.0)
+            i = b * Hq + h
+            e = [rel_err_rows(got["om"][b, h][None], o_m[None]).max(),
+                 rel_err_rows(got["shared"][b, h][None], ref[None]).max(),
+                 rel_err_rows(got["shared"][b, h][None], got["direct"][b, h][None]).max(),
+                 rel_err_rows(got["sep"][b, h][None],
+                              orc.merge_branches(o_m, l_m, o_r, l_r, dbg["gate"], "separate")[None]).max()]
+            if np.isfinite(l_r):
+                e.append(rel_err_rows(got["orr"][b, h][None], o_r[None]).max())
+                assert abs(got["lr"][i] - l_r) <= 1e-5 * max(1.0, abs(l_r))
+            else:
+                assert got["lr"][i] == -np.inf and not got["orr"][b, h].any()
+            assert abs(got["lm"][i] - l_m) <= 1e-5 * max(1.0, abs(l_m))
+            assert abs(got["g"][i] - dbg["gate"]) <= 1e-5
+            assert max(e) <= tol, f"(b={b}, h={h}) errors {e}"
+            worst = max(worst, max(e))
+    return worst
+
+
+@pytest.mark.parametrize("dtype,d,G", [("bf16", 128, 4), ("f32", 64, 7), ("bf16", 64, 16), ("f32", 128, 1)])
+def test_branches_ragged(dtype, d, G):
+    """Ragged lengths across 256-slot blocks, r = 0 heads, empty entries."""
+    Hkv, B = 3, 2
+    C, Rcap = 700, 300
+    res = [[0, 17, 300], [255, 1, 64]]
+    main = [[400, 683, 1], [445, 5, 636]]
+    run_case(3, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+
+
+def test_branches_per_query_tau_and_gate_floor():
+    run_case(4, 2, 8, 2, 128, "bf16", 600, 128, [[128, 40], [0, 3]], [[400, 500], [600, 90]], tau_kind="normal")
+    run_case(5, 1, 8, 2, 64, "f32", 300, 64, [[64, 10]], [[200, 31]], g_min=0.4)
+
+
+def test_branches_whole_head_shape():
+    """B * Hkv = 256 pairs: reskv_decode_attn takes its one-block-per-head
+    kernel, the branches the split path; the shared merge agrees with it."""
+    B, Hkv, G = 64, 4, 4
+    rng = np.random.default_rng(6)
+    res = rng.choice([0, 64, 128], size=(B, Hkv))
+    main = rng.integers(100, 384, size=(B, Hkv))
+    run_case(6, B, G * Hkv, Hkv, 128, "bf16", 512, 128, res, main)
