@@ -32,6 +32,9 @@ Paper map (section / equation / algorithm):
                               merged through log-sum-exp statistics);
                               Sec. 6.6 ablation table (separate
                               normalisations, reading R25)
+  AdaKV allocation .......... App. B.2.2 compared methods (cross-head budget
+                              allocation from SnapKV scores, safeguard 0.2;
+                              reading R26)
   alternative scorers ....... App. B.2.2 compared methods: H2O (accumulated
                               attention of the observation queries, recent
                               64) and TOVA (last-token window, recent 1),
@@ -77,7 +80,13 @@ notes of the repository):
       two separately normalised branch outputs by the gate,
       (1 - g) o_main + g o_res (g = 0 without populated entries); the paper
       does not print its formula, so this variant is parity unpinned against
-      the paper and pinned only to its own limits.
+      the paper and pinned only to its own limits;
+  R26 AdaKV reallocates the top-k (scored) part of the main budgets of the KV
+      heads of one (layer, sequence): every head keeps floor(alpha * k) of
+      its own best tokens (alpha = the safeguard), the remaining slots follow
+      one ranking of all heads' other tokens (score, then head, then
+      position), each head capped by its slot capacity; recent protection
+      and residual counts stay per head as in the uniform split.
 """
 
 import math
@@ -86,7 +95,7 @@ import numpy as np
 
 __all__ = [
     "round_to_dtype", "full_attention", "evict_attention", "zn_stats",
-    "decode_branches", "merge_branches",
+    "decode_branches", "merge_branches", "adakv_allocate", "build_heads_adakv",
     "window_raw_scores", "pool", "pool5", "scored_length", "select_main",
     "lloyd", "lloyd_objective", "assign_nearest", "residual_entries",
     "build_head", "build_cache", "gate_value", "decode_head", "decode",
@@ -362,6 +371,12 @@ def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16", fit_row
         scores = pool(raw[:n], pool_kernel)
         out["scores"] = scores
         main, evicted, seeds = select_main(scores, s, m, recent_window, r)
+    return _residual_layout(out, K, V, main, evicted, seeds, r, lloyd_iters, dtype)
+
+
+def _residual_layout(out, K, V, main, evicted, seeds, r, lloyd_iters, dtype):
+    """Lloyd partition of the evicted rows, the r entries and the cache rows
+    in slot order (shared by the uniform and the AdaKV construction)."""
     out["main_idx"], out["evicted"], out["seeds"] = main, evicted, seeds
     KE, VE = K[evicted], V[evicted]
     centers0 = K[seeds]
@@ -380,6 +395,87 @@ def build_head(K, V, Qw, m, r, recent_window, lloyd_iters, dtype="bf16", fit_row
     out["res_len"] = r
     out["main_len"] = main.size
     return out
+
+
+# --------------------------------------------------------------------------
+# AdaKV cross-head budget allocation (App. B.2.2 compared methods; R26)
+# --------------------------------------------------------------------------
+
+def adakv_allocate(scores, k_top, safeguard, cap):
+    """Top-k budgets of the KV heads of one (layer, sequence) under AdaKV.
+
+    scores    : per head, the pooled scores of its scored positions;
+    k_top     : per head, its top-k budget under the uniform split;
+    safeguard : alpha; head h keeps at least floor(alpha * k_top[h]) of its
+                own best tokens;
+    cap       : per head, the most top-k tokens it may hold.
+    The other sum(k_top) - sum(floors) slots go down one ranking of every
+    head's remaining tokens, by score descending, then head, then position
+    ascending; a head takes its next token only while under its cap.
+    Returns the per-head top-k counts.
+    """
+    H = len(scores)
+    floors = [int(math.floor(safeguard * k)) for k in k_top]
+    total = sum(k_top)
+    kk = list(floors)
+    ranking = []
+    for h in range(H):
+        sc = np.asarray(scores[h], _F64)
+        order = np.lexsort((np.arange(sc.size), -sc))
+        for p in order[floors[h]:]:
+            ranking.append((-sc[p], h, int(p)))
+    ranking.sort()
+    taken = sum(floors)
+    for _, h, _ in ranking:
+        if taken >= total:
+            break
+        if kk[h] < cap[h]:
+            kk[h] += 1
+            taken += 1
+    return kk
+
+
+def build_heads_adakv(Ks, Vs, Qws, budget, res, recent_window, lloyd_iters, safeguard, slot_cap,
+                      dtype="bf16", pool_kernel=5):
+    """AdaKV allocation followed by ResKV construction for the KV heads of
+    one (layer, sequence). Per head the uniform split gives m = b - r, the
+    protected |P| = min(recent_window, m, s) and the scored range [0, s-|P|);
+    heads with s <= m keep every token and take no part. The others share
+    their top-k budgets through adakv_allocate with cap = min(s - |P|,
+    slot_cap - r - |P|); each keeps its |P| recent tokens and its top-k'
+    scored tokens, and builds its r residual entries from the rest as in
+    build_head. Returns one record per head.
+    """
+    H = len(Ks)
+    s = np.asarray(Ks[0]).shape[0]
+    recs, live, sc, kt, cap, prot = [None] * H, [], [], [], [], []
+    for h in range(H):
+        m = budget - res[h]
+        if s <= m:
+            recs[h] = build_head(Ks[h], Vs[h], Qws[h], m, res[h], recent_window, lloyd_iters, dtype,
+                                 pool_kernel=pool_kernel)
+            continue
+        P = min(recent_window, m, s)
+        n = s - P
+        raw = window_raw_scores(np.asarray(Ks[h], _F64), Qws[h])
+        live.append(h)
+        sc.append(pool(raw[:n], pool_kernel))
+        kt.append(m - P)
+        cap.append(min(n, slot_cap - res[h] - P))
+        prot.append(P)
+    kk = adakv_allocate(sc, kt, safeguard, cap)
+    for i, h in enumerate(live):
+        K = np.asarray(Ks[h], _F64)
+        V = np.asarray(Vs[h], _F64)
+        n = s - prot[i]
+        order = np.lexsort((np.arange(n), -sc[i]))
+        k = kk[i]
+        main = np.sort(np.concatenate([order[:k], np.arange(n, s)]))
+        evicted = np.sort(order[k:])
+        seeds = np.sort(order[k:k + res[h]])
+        out = {"scores": sc[i], "k_top": k, "protected": prot[i]}
+        recs[h] = _residual_layout(out, K, V, main, evicted, seeds, res[h], lloyd_iters, dtype)
+    return recs
 
 
 def build_cache(K, V, Qobs, seq_len, budget, res_count, recent_window,
