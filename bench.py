@@ -14,8 +14,8 @@ appended inside the call.
 value = decode tokens (batch x layers x decode steps) / step time.
 
 Also reported: decode-only throughput and HBM GB/s, construction GB/s,
-construction with the validation proxy choosing r (ms per layer, untimed
-in the job), the roofline of the decode kernels (algorithmic bytes per call / average call
+construction with the validation proxy choosing r and with AdaKV's
+cross-head allocation (ms per layer, untimed in the job), the roofline of the decode kernels (algorithmic bytes per call / average call
 time from HIP events on the launch stream), and the fp64 oracle's throughput
 on the host cores over a bounded sample of the same job.
 
@@ -51,6 +51,8 @@ def parse():
                          "the byte counters; proxy: only construction with the validation proxy, every layer")
     ap.add_argument("--proxy-layers", type=int, default=2,
                     help="layers built with the validation proxy after the timed job (0: skip)")
+    ap.add_argument("--adakv-layers", type=int, default=2,
+                    help="layers built with AdaKV's cross-head allocation after the timed job (0: skip)")
     return ap.parse_args()
 
 
@@ -160,6 +162,44 @@ def proxy_runs(rk, torch, wl, shape, layers, caches, n_layers, dev):
     return dict(ms_per_layer=e0.elapsed_time(e1) / n_layers, layers_timed=n_layers,
                 workspace_bytes=nws, grid_counts=counts,
                 chosen_count_heads={str(r): int((chosen == r).sum()) for r in counts})
+
+
+# AdaKV's safeguard coefficient (App. B.2.2).
+ADAKV_SAFEGUARD = 0.2
+
+
+def adakv_runs(rk, torch, wl, shape, layers, caches, res_layers, n_layers, dev):
+    """Construction with AdaKV's cross-head allocation for the first n_layers
+    layers (slot capacity of the decode caches): one untimed call, then every
+    layer once between events on the launch stream. Returns ms per layer and
+    the spread of the allocated main lengths."""
+    import numpy as np
+    S = wl.max_ctx
+    params = rk.BuildParams(S, wl.window, wl.window, wl.lloyd_iters, 0)
+    nws = max(rk.reskv_build_adakv_workspace_size(shape, params, ADAKV_SAFEGUARD, layers[l]["seq_len"],
+                                                  layers[l]["budget"], res_layers[l].reshape(-1))
+              for l in range(n_layers))
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def call(l):
+        x, c = layers[l], caches[l]
+        rk.reskv_build_cache_adakv(shape, params, ADAKV_SAFEGUARD, x["K"], x["V"], x["seq_len"], x["q_obs"],
+                                   x["budget"], res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"],
+                                   c["main_idx"], c["res_len"], c["main_len"], ws)
+
+    call(0)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for l in range(n_layers):
+        call(l)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ml = np.concatenate([caches[l]["main_len"].cpu().numpy() for l in range(n_layers)])
+    return dict(ms_per_layer=e0.elapsed_time(e1) / n_layers, layers_timed=n_layers, safeguard=ADAKV_SAFEGUARD,
+                main_len_min=int(ml.min()), main_len_mean=float(ml.mean()), main_len_max=int(ml.max()))
 
 
 def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
@@ -420,6 +460,9 @@ def main():
     if args.proxy_layers > 0:
         # after the timed jobs: construction with the validation proxy choosing r
         result["proxy_build"] = proxy_runs(rk, torch, wl, shape, layers, caches, min(args.proxy_layers, L), dev)
+    if args.adakv_layers > 0:
+        result["adakv_build"] = adakv_runs(rk, torch, wl, shape, layers, caches, res_layers,
+                                           min(args.adakv_layers, L), dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, layers[0], q_stage[0, 0], tau_stage[0, 0], res_layers,
                                               args.cpu_budget_s)

@@ -139,6 +139,62 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
                                   const int32_t* budget_host,
                                   const int32_t* res_count_host);
 
+/*
+ * reskv_build_cache_adakv - construction with the top-k budget shared
+ * across the KV heads of each sequence by AdaKV's cross-head allocation
+ * (App. B.2.2, compared methods: AdaKV allocates the retained budget across
+ * KV heads from the SnapKV scores, safeguard coefficient 0.2), followed by
+ * the residual construction of reskv_build_cache.
+ *
+ * Per (b, kv head) the uniform split gives m = b - r, the protected window
+ * |P| = min(recent_window, m, s) and the scored positions [0, s - |P|) with
+ * k_top = m - |P|, exactly as reskv_build_cache. Heads with s <= m keep every
+ * token and take no part. Among the others of sequence b:
+ *   - head h keeps floor(safeguard * k_top_h) of its best-scored tokens
+ *     (floor of the double product);
+ *   - the remaining sum(k_top_h) - sum(floor) slots go down one ranking of
+ *     every head's other scored tokens, by score descending, then KV head
+ *     ascending, then position ascending; a head takes its next token only
+ *     while it holds fewer than cap_h = min(s - |P|, C - r_h - |P|) top-k
+ *     tokens (a head can hold more than k_top_h, so slot_cap above the
+ *     budget leaves room to grow).
+ * Head h then keeps its |P| recent tokens and its k'_h best-scored tokens
+ * (ties to the lower position), and its r residual entries summarise the
+ * rest as in reskv_build_cache (seeds: the evicted tokens of rank
+ * k'_h .. k'_h + r - 1). safeguard = 1 gives the uniform split of
+ * reskv_build_cache; safeguard = 0 is one top-k over all heads of a sequence.
+ *
+ *   safeguard       in [0, 1] (App. B.2.2: 0.2); Hkv <= 32
+ *   other arguments as for reskv_build_cache, except:
+ *   main_len        out int32 [B*Hkv]: |P| + k'_h (min(m, s) for heads with
+ *                   s <= m); main_idx holds that many positions
+ *   workspace       device scratch of reskv_build_adakv_workspace_size()
+ *                   bytes (sized for the widest allocation of every head)
+ * Returns RESKV_OK or an error code before launching anything.
+ */
+reskv_status_t reskv_build_cache_adakv(const reskv_shape_t* shape,
+                                       const reskv_build_params_t* params,
+                                       double safeguard,
+                                       const void* k, const void* v,
+                                       const int32_t* seq_len_host,
+                                       const void* q_obs,
+                                       const int32_t* budget_host,
+                                       const int32_t* res_count_host,
+                                       void* kc, void* vc, float* logc,
+                                       int32_t* main_idx,
+                                       int32_t* res_len, int32_t* main_len,
+                                       float* dbg_scores, int32_t* dbg_assign,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* Bytes of device workspace reskv_build_cache_adakv needs (0 if invalid). */
+size_t reskv_build_adakv_workspace_size(const reskv_shape_t* shape,
+                                        const reskv_build_params_t* params,
+                                        double safeguard,
+                                        const int32_t* seq_len_host,
+                                        const int32_t* budget_host,
+                                        const int32_t* res_count_host);
+
 typedef struct {
   const double* grid_host;  /* [n_grid] budget fractions f in [0, 1); at least
                                one is 0 (App. B.3: 0, .05, .10, .15, .20) */

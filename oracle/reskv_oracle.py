@@ -96,7 +96,7 @@ import numpy as np
 __all__ = [
     "round_to_dtype", "full_attention", "evict_attention", "zn_stats",
     "decode_branches", "merge_branches", "adakv_allocate", "build_heads_adakv",
-    "window_raw_scores", "pool", "pool5", "scored_length", "select_main",
+    "window_raw_scores", "pool", "pool5", "scored_length", "select_main", "select_top",
     "lloyd", "lloyd_objective", "assign_nearest", "residual_entries",
     "build_head", "build_cache", "gate_value", "decode_head", "decode",
     "candidate_counts", "proxy_choice", "validation_proxy",
@@ -251,11 +251,16 @@ def select_main(scores, s, m, recent_window, r):
     if s <= m:
         return np.arange(s), np.zeros(0, np.int64), np.zeros(0, np.int64)
     p = min(recent_window, m, s)
-    n = s - p
-    k_top = m - p
+    return select_top(scores, s, s - p, m - p, r)
+
+
+def select_top(scores, s, n, k_top, r):
+    """The k_top best of the scored positions [0, n) (score descending, then
+    position ascending), plus the protected positions [n, s), are main; the
+    rest is evicted; the next r in that order seed the Lloyd groups.
+    Returns (main_idx ascending, evicted ascending, seeds ascending)."""
     scores = np.asarray(scores, _F64)
     assert scores.shape[0] == n
-    # order: score descending, then position ascending
     order = np.lexsort((np.arange(n), -scores))
     top = order[:k_top]
     main = np.sort(np.concatenate([top, np.arange(n, s)]))
@@ -467,12 +472,8 @@ def build_heads_adakv(Ks, Vs, Qws, budget, res, recent_window, lloyd_iters, safe
     for i, h in enumerate(live):
         K = np.asarray(Ks[h], _F64)
         V = np.asarray(Vs[h], _F64)
-        n = s - prot[i]
-        order = np.lexsort((np.arange(n), -sc[i]))
         k = kk[i]
-        main = np.sort(np.concatenate([order[:k], np.arange(n, s)]))
-        evicted = np.sort(order[k:])
-        seeds = np.sort(order[k:k + res[h]])
+        main, evicted, seeds = select_top(sc[i], s, s - prot[i], k, res[h])
         out = {"scores": sc[i], "k_top": k, "protected": prot[i]}
         recs[h] = _residual_layout(out, K, V, main, evicted, seeds, res[h], lloyd_iters, dtype)
     return recs

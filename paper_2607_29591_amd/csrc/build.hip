@@ -11,6 +11,10 @@
 //                  normalised weight of key p, for the scored positions
 //   pool_scores    centred zero-padded sum (5 taps by default) over the
 //                  scored positions
+//   [adakv_alloc]  with cross-head allocation only: moves top-k budget
+//                  between the KV heads of a sequence (one ranking of all
+//                  heads' scores, per-head safeguard floor and slot cap) and
+//                  rewrites each head's sizes before the selection
 //   select         radix select (4 x 8-bit digits of the fp32 bit pattern) of
 //                  the k_top-th and (k_top + r')-th largest score; ties at a
 //                  threshold go to the lower position. Stable compaction writes
@@ -56,6 +60,7 @@ constexpr int kAssignThreads = 64 * kAssignWaves;
 constexpr int kTokBlock = kAssignWaves * 16 * kTokTiles;  // evicted tokens per Lloyd block (256)
 constexpr int kCenterChunk = 64;   // centres staged in LDS per step
 constexpr int kSelThreads = 1024;
+constexpr int kAdaThreads = 1024;
 
 struct BuildArgs {
   const void* k;
@@ -562,6 +567,150 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   for (int i = tid; i < hm.P; i += kSelThreads) main_idx[hm.k_top + i] = hm.n_sc + i;
 }
 
+// ------------------------------------- AdaKV cross-head budget allocation
+
+// Per sequence b (one block): the KV heads that are not all-main share their
+// top-k budgets (the compared method AdaKV of App. B.2.2, which allocates
+// the kept budget across heads from SnapKV scores with a safeguard
+// coefficient). Head h keeps floor(safeguard * k_top_h) of its own best
+// tokens; the other sum(k_top) - sum(floor) slots follow one ranking of every
+// head's remaining tokens (score descending, then head, then position), a
+// head taking tokens only while it holds fewer than
+// cap_h = min(n_sc_h, C - r_h - P_h). A head's tokens in that ranking come
+// in its own (score, position) order, so its final set is its own top-k'_h:
+// only the counts k'_h are found here, and the selection then takes each
+// head's top k'_h exactly as for a uniform split.
+//
+// With N_h(x) = the head's scored tokens above x, the ranking reaches head
+// h's tokens above x after taking min(room_h, max(0, N_h(x) - floor_h)) of
+// them (room_h = cap_h - floor_h). A radix search over the fp32 bit pattern
+// (non-negative floats order as unsigned integers) finds the score x* of the
+// last slot handed out from per-head digit histograms; the tokens tied at
+// x* then go to the heads in ascending order.
+__global__ __launch_bounds__(kAdaThreads) void adakv_alloc(BuildArgs a, HeadMeta* meta, double safeguard) {
+  const int b = blockIdx.x, H = a.Hkv, tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  __shared__ int s_hist[kAdaMaxHeads][256];  // digit counts, then suffix sums
+  __shared__ int s_floor[kAdaMaxHeads], s_room[kAdaMaxHeads], s_n[kAdaMaxHeads], s_above[kAdaMaxHeads];
+  __shared__ int s_extra, s_total_room, s_digit;
+  if (tid < H) {
+    const HeadMeta hm = meta[b * H + tid];
+    const bool live = !hm.all_main;
+    const int fl = live ? (int)floor(safeguard * (double)hm.k_top) : 0;
+    const int cap = live ? min(hm.n_sc, a.C - hm.r - hm.P) : 0;
+    s_floor[tid] = fl;
+    s_room[tid] = live ? cap - fl : 0;
+    s_n[tid] = live ? hm.n_sc : 0;
+    s_above[tid] = 0;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int extra = 0, room = 0;
+    for (int h = 0; h < H; ++h) {
+      const HeadMeta hm = meta[b * H + h];
+      if (!hm.all_main) extra += hm.k_top - s_floor[h];
+      room += s_room[h];
+    }
+    s_extra = extra;
+    s_total_room = room;
+    s_digit = 0;
+  }
+  __syncthreads();
+  const int extra = s_extra;
+  const bool search = extra > 0 && s_total_room > extra;  // block-uniform
+  uint32_t prefix = 0u, mask = 0u;
+  int digit = 0;
+  for (int shift = 24; search && shift >= 0; shift -= 8) {
+    for (int i = tid; i < H * 256; i += kAdaThreads) (&s_hist[0][0])[i] = 0;
+    __syncthreads();
+    for (int h = 0; h < H; ++h) {
+      const int n = s_n[h];
+      const uint32_t* key = reinterpret_cast<const uint32_t*>(a.score + ((size_t)b * H + h) * a.S);
+      for (int i0 = tid; i0 < n; i0 += 4 * kAdaThreads) {
+        uint32_t u[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) u[v] = i0 + v * kAdaThreads < n ? key[i0 + v * kAdaThreads] : 0u;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (i0 + v * kAdaThreads < n && (u[v] & mask) == prefix) atomicAdd(&s_hist[h][(u[v] >> shift) & 0xff], 1);
+      }
+    }
+    __syncthreads();
+    // per head, suffix sums over digits: S_h[d] = tokens of the current
+    // prefix range whose digit is >= d (lane l holds digits 4l .. 4l+3)
+    for (int h = wave; h < H; h += kAdaThreads / 64) {
+      int c[4], own = 0;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) { c[v] = s_hist[h][4 * lane + v]; own += c[v]; }
+      int incl = own;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_down(incl, o, 64);
+        if (lane + o < 64) incl += y;
+      }
+      int run = incl - own;  // digits above this lane's four
+#pragma unroll
+      for (int v = 3; v >= 0; --v) { run += c[v]; s_hist[h][4 * lane + v] = run; }
+    }
+    __syncthreads();
+    // slots handed out down to digit d: non-increasing in d, so the digits
+    // reaching `extra` are a prefix 0 .. d*; their count gives d*
+    bool reach = false;
+    if (tid < 256) {
+      long long f = 0;
+      for (int h = 0; h < H; ++h) {
+        const int above = s_above[h] + s_hist[h][tid] - s_floor[h];
+        f += min(s_room[h], max(0, above));
+      }
+      reach = f >= extra;
+    }
+    const int cnt = __syncthreads_count(reach);
+    digit = cnt > 0 ? cnt - 1 : 0;
+    if (tid < H) {
+      const int higher = digit < 255 ? s_hist[tid][digit + 1] : 0;
+      if (shift > 0) s_above[tid] += higher;
+    }
+    if (tid == 0) s_digit = digit;
+    prefix |= (uint32_t)digit << shift;
+    mask |= 0xffu << shift;
+    __syncthreads();
+  }
+  if (tid != 0) return;
+  // counts: slots above x*, then the tokens tied at x* to the heads in order
+  // (s_above counts the tokens above the last digit's range, s_hist holds
+  // the last digit's suffix sums)
+  int rem = extra;
+  int take[kAdaMaxHeads];
+  const int d = s_digit;
+  for (int h = 0; h < H; ++h) {
+    if (!search) {
+      take[h] = extra == 0 ? 0 : s_room[h];
+      continue;
+    }
+    const int gt = s_above[h] + (d < 255 ? s_hist[h][d + 1] : 0);  // tokens > x*
+    take[h] = min(s_room[h], max(0, gt - s_floor[h]));
+    rem -= take[h];
+  }
+  for (int h = 0; search && h < H; ++h) {
+    const int ge = s_above[h] + s_hist[h][d];                      // tokens >= x*
+    const int gt = s_above[h] + (d < 255 ? s_hist[h][d + 1] : 0);
+    const int tied = max(0, ge - s_floor[h]) - max(0, gt - s_floor[h]);
+    const int t = min(min(s_room[h] - take[h], tied), rem);
+    take[h] += t;
+    rem -= t;
+  }
+  for (int h = 0; h < H; ++h) {
+    HeadMeta hm = meta[b * H + h];
+    if (hm.all_main) continue;
+    hm.k_top = s_floor[h] + take[h];
+    hm.m = hm.P + hm.k_top;
+    hm.main_len = hm.m;
+    hm.nE = hm.s - hm.m;
+    hm.r_eff = hm.r < hm.nE ? hm.r : hm.nE;
+    meta[b * H + h] = hm;
+  }
+}
+
 // ------------------------------------------------ gather + centre seeding
 
 template <typename T, int D>
@@ -1038,7 +1187,8 @@ hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStrea
 
 // Pooling, selection, gather and the Lloyd rounds of one candidate.
 template <typename T, int D>
-hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
+hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st,
+                                  HeadMeta* alloc_meta = nullptr, double safeguard = 1.0) {
   const dim3 bhg(1, pl.Hkv, pl.B);
   auto grid = [&](int x) { return dim3(x < 1 ? 1 : x, pl.Hkv, pl.B); };
   hipError_t e;
@@ -1048,6 +1198,10 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
     RESKV_CHECK();
   }
   hipLaunchKernelGGL(pool_scores, grid((pl.S + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  if (alloc_meta) {
+    hipLaunchKernelGGL(adakv_alloc, dim3(pl.B), dim3(kAdaThreads), 0, st, a, alloc_meta, safeguard);
+    RESKV_CHECK();
+  }
   hipLaunchKernelGGL(select_kernel, bhg, dim3(kSelThreads), 0, st, a); RESKV_CHECK();
   const int rows = pl.max_main + pl.Rcap;
   const int gblocks = (rows * (D * (int)sizeof(T) / 16) + kThreads - 1) / kThreads;
@@ -1131,6 +1285,23 @@ bool layout_build_plan(BuildPlan* plan) {
   return true;
 }
 
+bool make_build_plan_adakv(const reskv_shape_t& s, const reskv_build_params_t& p, double safeguard,
+                           const int32_t* seq_len, const int32_t* budget, const int32_t* res_count,
+                           BuildPlan* plan) {
+  init_build_plan(s, p, plan);
+  std::vector<HeadMeta> hm;
+  head_meta(*plan, seq_len, budget, res_count, p.recent_window, hm);
+  for (HeadMeta& m : hm) {  // widest sizes the allocation can give each head
+    if (m.all_main) continue;
+    const int fl = (int)floor(safeguard * (double)m.k_top);
+    const int cap = m.n_sc < s.slot_cap - m.r - m.P ? m.n_sc : s.slot_cap - m.r - m.P;
+    m.main_len = m.P + cap;
+    m.nE = m.s - m.P - fl;
+    m.r_eff = m.r < m.nE ? m.r : m.nE;
+  }
+  return fold_build_plan(hm, plan) && layout_build_plan(plan);
+}
+
 bool make_build_plan(const reskv_shape_t& s, const reskv_build_params_t& p, const int32_t* seq_len,
                      const int32_t* budget, const int32_t* res_count, BuildPlan* plan) {
   init_build_plan(s, p, plan);
@@ -1166,6 +1337,29 @@ hipError_t launch_build_scores(const BuildPlan& pl, const void* k, const void* q
   const bool bf = pl.dtype == RESKV_BF16;
   if (pl.D == 128) return bf ? launch_scores_typed<uint16_t, 128>(pl, a, stream) : launch_scores_typed<float, 128>(pl, a, stream);
   if (pl.D == 64) return bf ? launch_scores_typed<uint16_t, 64>(pl, a, stream) : launch_scores_typed<float, 64>(pl, a, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_build_adakv(const reskv_shape_t& s, const reskv_build_params_t& p, double safeguard,
+                              const BuildPlan& pl, const void* k, const void* v, const int32_t* seq_len,
+                              const void* q_obs, const int32_t* budget, const int32_t* res_count, void* kc,
+                              void* vc, float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
+                              float* dbg_scores, int32_t* dbg_assign, void* workspace, hipStream_t stream) {
+  (void)s;
+  HeadMeta* meta = reinterpret_cast<HeadMeta*>(static_cast<char*>(workspace) + pl.off_meta);
+  hipError_t e = upload_meta(pl, seq_len, budget, res_count, p.recent_window, meta, stream);
+  if (e != hipSuccess) return e;
+  e = launch_build_scores(pl, k, q_obs, meta, workspace, stream);
+  if (e != hipSuccess) return e;
+  const BuildOut out{kc, vc, logc, main_idx, res_len, main_len};
+  const BuildArgs a = make_args(pl, k, v, nullptr, meta, out, dbg_scores, dbg_assign, workspace);
+  const bool bf = pl.dtype == RESKV_BF16;
+  if (pl.D == 128)
+    return bf ? launch_candidate_typed<uint16_t, 128>(pl, a, stream, meta, safeguard)
+              : launch_candidate_typed<float, 128>(pl, a, stream, meta, safeguard);
+  if (pl.D == 64)
+    return bf ? launch_candidate_typed<uint16_t, 64>(pl, a, stream, meta, safeguard)
+              : launch_candidate_typed<float, 64>(pl, a, stream, meta, safeguard);
   return hipErrorInvalidValue;
 }
 

@@ -43,14 +43,15 @@ class HostView:
 
 
 def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=False, host_cache=True, fit=0,
-              res=None, pool=0):
+              res=None, pool=0, adakv=None, slot_cap=None):
     """Build one layer on the GPU; returns host numpy copies of the outputs
     (and the device tensors under "dev" when keep_device is set). `fit` > 0
     scores with the leading `fit` window rows only; `res` overrides x["res"];
-    `pool` is the pooling kernel (0: the default 5)."""
+    `pool` is the pooling kernel (0: the default 5); `adakv` = a safeguard
+    builds through reskv_build_cache_adakv; `slot_cap` overrides C."""
     B, Hkv, d = wl.batch, wl.hkv, wl.d
     S = x["K"].shape[2]
-    C, Rcap = wl.slot_cap, wl.res_cap
+    C, Rcap = wl.slot_cap if slot_cap is None else slot_cap, wl.res_cap
     T = wl.lloyd_iters if iters is None else iters
     shape = rk.make_shape(B, wl.hq, Hkv, d, wl.dtype, C, Rcap)
     params = rk.BuildParams(S, wl.window, wl.window if recent is None else recent, T, fit, pool)
@@ -67,11 +68,18 @@ def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=Fal
     main_len = torch.full((B * Hkv,), -7, dtype=torch.int32, device="cuda")
     dbg_s = torch.empty((B, Hkv, S), device="cuda") if dbg else None
     dbg_a = torch.empty((T, B, Hkv, S), dtype=torch.int32, device="cuda") if dbg else None
-    nws = rk.reskv_build_workspace_size(shape, params, x["seq_len"], x["budget"], res)
+    if adakv is None:
+        nws = rk.reskv_build_workspace_size(shape, params, x["seq_len"], x["budget"], res)
+    else:
+        nws = rk.reskv_build_adakv_workspace_size(shape, params, adakv, x["seq_len"], x["budget"], res)
     assert nws > 0
     ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
-    rk.reskv_build_cache(shape, params, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc, main_idx,
-                         res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
+    if adakv is None:
+        rk.reskv_build_cache(shape, params, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc, main_idx,
+                             res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
+    else:
+        rk.reskv_build_cache_adakv(shape, params, adakv, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc,
+                                   main_idx, res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
     torch.cuda.synchronize()
     out = dict(logc=logc.cpu().numpy().astype(np.float64), main_idx=main_idx.cpu().numpy(),
                res_len=res_len.cpu().numpy().reshape(B, Hkv), main_len=main_len.cpu().numpy().reshape(B, Hkv))
@@ -97,10 +105,12 @@ def ulp(x, dtype):
     return np.maximum(x, 1e-30) * 2.0 ** -23
 
 
-def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True, fit=None, r=None, pool=5):
+def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True, fit=None, r=None, pool=5,
+               k_top=None):
     """All construction checks for one (b, kv head). Returns a report dict.
     `fit` = leading window rows that scored (None: all); `r` overrides
-    x["res"]; `pool` = pooling kernel."""
+    x["res"]; `pool` = pooling kernel; `k_top` = the head's top-k count when
+    a cross-head allocation set it (None: the uniform m - |P|)."""
     recent = wl.window if recent is None else recent
     T = wl.lloyd_iters if iters is None else iters
     G = wl.group
@@ -113,7 +123,9 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
     rep = dict(near_ties=0, lloyd_agree=None)
     assert got["res_len"][b, h] == r
     ml = int(got["main_len"][b, h])
-    assert ml == min(m, s)
+    P = min(recent, m, s)
+    kt = m - P if (k_top is None or s <= m) else int(k_top)
+    assert ml == (s if s <= m else P + kt)
     midx = got["main_idx"][b, h, :ml].astype(np.int64)
     if s <= m:
         assert (midx == np.arange(s)).all()
@@ -130,17 +142,16 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
         assert (err <= SCORE_RTOL * np.abs(ref) + 1e-30).all(), \
             f"score err {(err / np.maximum(np.abs(ref), 1e-30)).max():.2e}"
     # (i) exact selection on the GPU's own scores
-    main_g, ev_g, seeds_g = orc.select_main(gs, s, m, recent, r)
+    main_g, ev_g, seeds_g = orc.select_top(gs, s, n, kt, r)
     np.testing.assert_array_equal(midx, main_g)
     # (iii) end-to-end selection against the oracle's fp64 scores, with
     # certified near-ties at the k_top boundary
     if full_oracle:
-        main_o, _, _ = orc.select_main(ref, s, m, recent, r)
+        main_o, _, _ = orc.select_top(ref, s, n, kt, r)
         if not np.array_equal(main_o, main_g):
-            k_top = m - min(recent, m, s)
             srt = np.sort(ref)[::-1]
-            gap = abs(srt[k_top - 1] - srt[k_top]) if 0 < k_top < n else 0.0
-            assert gap <= 2 * SCORE_RTOL * srt[max(k_top - 1, 0)], "selection differs outside a near-tie"
+            gap = abs(srt[kt - 1] - srt[kt]) if 0 < kt < n else 0.0
+            assert gap <= 2 * SCORE_RTOL * srt[max(kt - 1, 0)], "selection differs outside a near-tie"
             rep["near_ties"] += 1
     # cache main rows are exact copies
     np.testing.assert_array_equal(got["kc"][b, h, r:r + ml], K[midx])

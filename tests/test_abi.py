@@ -184,3 +184,39 @@ def test_decode_branches_rejects_small_workspace(L):
         rk.reskv_decode_branches(shape(), rk.make_gate(), t, t, t, t, t, t, t, t, t, t, t, FakeTensor(8),
                                  stream=FakeStream())
     assert ei.value.status == 3
+
+
+def test_adakv_workspace_covers_the_widest_allocation(L):
+    """The cross-head build sizes its grids for every head holding up to
+    min(s, C - r) main slots, so its workspace is at least the uniform one;
+    safeguard 1 (the uniform split) keeps the evicted sets, and the main
+    slots may still widen to the slot capacity."""
+    sh = rk.make_shape(1, 4, 2, 64, "f32", 128, 13)
+    p = rk.BuildParams(300, 16, 16, 4, 0, 0)
+    uni = rk.reskv_build_workspace_size(sh, p, (300,), (64,), [13, 0])
+    for g in (0.0, 0.2, 1.0):
+        assert rk.reskv_build_adakv_workspace_size(sh, p, g, (300,), (64,), [13, 0]) >= uni > 0
+
+
+@pytest.mark.parametrize("safeguard,hkv,code", [(-0.1, 2, 1), (1.5, 2, 1), (float("nan"), 2, 1), (0.2, 33, 2)])
+def test_adakv_rejects_bad_arguments(L, safeguard, hkv, code):
+    sh = rk.make_shape(1, hkv, hkv, 64, "f32", 64, 13)
+    p = rk.BuildParams(300, 16, 16, 4, 0, 0)
+    res = [0] * hkv
+    assert rk.reskv_build_adakv_workspace_size(sh, p, safeguard, (300,), (64,), res) == 0
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_build_cache_adakv(sh, p, safeguard, t, t, (300,), t, (64,), res, t, t, t, t, t, t, t,
+                                   stream=FakeStream())
+    assert ei.value.status == code
+    assert rk.last_error()
+
+
+def test_adakv_rejects_small_workspace(L):
+    sh = rk.make_shape(1, 4, 2, 64, "f32", 128, 13)
+    p = rk.BuildParams(300, 16, 16, 4, 0, 0)
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_build_cache_adakv(sh, p, 0.2, t, t, (300,), t, (64,), [13, 0], t, t, t, t, t, t, FakeTensor(8),
+                                   stream=FakeStream())
+    assert ei.value.status == 3
