@@ -54,11 +54,7 @@ constexpr int kRowChunk = 128;     // window rows staged in LDS per scoring step
 // s_waitcnt immediate: vector-memory count 0, export and LDS/scalar counts
 // left at their maximum (no wait on them)
 constexpr int kWaitVmcnt0 = 0x0F70;
-constexpr int kTokTiles = 2;       // 16-token MFMA tiles per wave in the assignment
-constexpr int kAssignWaves = 8;    // with at most 128 registers, two blocks share a CU
-constexpr int kAssignThreads = 64 * kAssignWaves;
-constexpr int kTokBlock = kAssignWaves * 16 * kTokTiles;  // evicted tokens per Lloyd block (256)
-constexpr int kCenterChunk = 64;   // centres staged in LDS per step
+constexpr int kTokBlock = 256;     // evicted tokens per counting-sort block (histograms, scatter)
 constexpr int kSelThreads = 1024;
 constexpr int kAdaThreads = 1024;
 
@@ -817,58 +813,81 @@ __device__ __forceinline__ f32x4_t mma_step(const Frag<float, D>& c, const Frag<
                                               e == 0 ? y.x : e == 1 ? y.y : e == 2 ? y.z : y.w, acc, 0, 0, 0);
 }
 
-// Assignment of kTokBlock evicted tokens (8 waves x kTokTiles x 16) to the
-// nearest centre: C[centre][token] = mu.k on MFMA with mu = hi + lo (bf16
-// pair) or fp32, dist = ||mu||^2 - 2 mu.k, argmin with ties to the lower
-// centre. The token tiles of a wave advance through each k-step together so
-// the MFMA chains are independent. Centres past r' are staged with an
-// infinite norm and never win.
+// Tiling of the assignment. Each wave holds kTiles 16-token tiles of keys in
+// registers and streams the centres from LDS; every centre fragment read from
+// LDS feeds 2 * kTiles MFMAs (hi and lo parts for bf16), so LDS traffic per
+// MFMA falls as 1 / kTiles. bf16: 8 tiles (128 tokens per wave) at two waves
+// per SIMD, in blocks of 4 waves so that two blocks share a CU and one
+// block's key loads overlap the other's MFMAs; fp32 (twice the key
+// registers): 2 tiles, 8 waves, four waves per SIMD. Histograms stay per
+// 256-token block of the evicted list.
+template <typename T>
+struct AssignShape {
+  static constexpr int kTiles = sizeof(T) == 2 ? 8 : 2;
+  static constexpr int kWaves = sizeof(T) == 2 ? 4 : 8;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kWavesPerSimd = sizeof(T) == 2 ? 2 : 4;
+  static constexpr int kCenters = sizeof(T) == 2 ? 32 : 64;  // centres staged in LDS per step
+  static constexpr int kTokens = kWaves * 16 * kTiles;       // evicted tokens per block
+  static constexpr int kSubs = kTokens / kTokBlock;          // histogram blocks per block
+  static_assert(kTokens % kTokBlock == 0, "assignment tiling");
+};
+
+// Assignment of AssignShape<T>::kTokens evicted tokens to the nearest centre:
+// C[centre][token] = mu.k on MFMA with mu = hi + lo (bf16 pair) or fp32,
+// dist = ||mu||^2 - 2 mu.k, argmin with ties to the lower centre. All token
+// tiles of a wave advance through each k-step together, so the MFMA chains
+// are independent. Centres past r' are staged with an infinite norm and
+// never win.
 template <typename T, int D>
-__global__ __launch_bounds__(kAssignThreads, sizeof(T) == 2 ? 4 : 2) void lloyd_assign(BuildArgs a, int iter) {
+__global__ __launch_bounds__(AssignShape<T>::kThreads, AssignShape<T>::kWavesPerSimd) void lloyd_assign(BuildArgs a, int iter) {
   constexpr bool kBf = sizeof(T) == 2;
+  constexpr int kTT = AssignShape<T>::kTiles;
+  constexpr int kSubs = AssignShape<T>::kSubs;
+  constexpr int kNT = AssignShape<T>::kThreads;
+  constexpr int kCC = AssignShape<T>::kCenters;
   constexpr int kRowB = kBf ? D * 2 + 16 : D * 4 + 16;   // padded LDS row bytes
   constexpr int kSteps = kBf ? D / 32 : D / 4;           // MFMA k-steps over the lane's share of a row
   const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
-  const int t0 = blk * kTokBlock;
+  const int t0 = blk * AssignShape<T>::kTokens;
   if (hm.r_eff == 0 || t0 >= hm.nE) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 15, grp = lane >> 4;
-  __shared__ __align__(16) unsigned char s_c[kCenterChunk * kRowB * (kBf ? 2 : 1)];
-  __shared__ float s_norm[kCenterChunk];
-  extern __shared__ int s_hist[];  // [r_eff]
-  for (int j = tid; j < hm.r_eff; j += kAssignThreads) s_hist[j] = 0;
+  __shared__ __align__(16) unsigned char s_c[kCC * kRowB * (kBf ? 2 : 1)];
+  __shared__ float s_norm[kCC];
+  extern __shared__ int s_hist[];  // [r_eff]: one 256-token histogram block at a time
 
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
   const int32_t* elist = a.elist + (size_t)bh * a.S;
-  const int tw = t0 + wave * 16 * kTokTiles;  // this wave's first token
-  Frag<T, D> tk[kTokTiles];
+  const int tw = t0 + wave * 16 * kTT;  // this wave's first token
+  Frag<T, D> tk[kTT];
 #pragma unroll
-  for (int tt = 0; tt < kTokTiles; ++tt) {
+  for (int tt = 0; tt < kTT; ++tt) {
     const int i = min(tw + 16 * tt + col, hm.nE - 1);
     tk[tt].load(K + (size_t)elist[i] * D, grp);
   }
-  float best[kTokTiles][4];
-  int bidx[kTokTiles][4];
+  // per token tile: the lane's best distance and centre (over the centres of
+  // its lane group, merged across the groups at the end)
+  float best[kTT];
+  int bidx[kTT];
 #pragma unroll
-  for (int tt = 0; tt < kTokTiles; ++tt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { best[tt][i] = __builtin_huge_valf(); bidx[tt][i] = 0x7fffffff; }
+  for (int tt = 0; tt < kTT; ++tt) { best[tt] = __builtin_huge_valf(); bidx[tt] = 0x7fffffff; }
 
   const size_t cbase = (size_t)bh * a.Rcap;
   // centre chunks are staged through one LDS buffer; the next chunk's global
   // loads are issued before this chunk's MFMAs and written after a barrier
   constexpr int kPieces = (kBf ? D * 2 : D * 4) / 16;       // 16-byte pieces per row
-  constexpr int kPer = kCenterChunk * kPieces / kAssignThreads;   // pieces per thread
-  static_assert(kCenterChunk * kPieces % kAssignThreads == 0, "staging split");
+  constexpr int kPer = kCC * kPieces / kNT;   // pieces per thread
+  static_assert(kCC * kPieces % kNT == 0, "staging split");
   uint4 ph[kPer], pl[kPer];
   float pn = 0.f;
   auto fetch = [&](int j0) {
-    const int nj = min(kCenterChunk, hm.r_eff - j0);
+    const int nj = min(kCC, hm.r_eff - j0);
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
-      const int x = tid + u * kAssignThreads, jj = x / kPieces, pc = x % kPieces;
+      const int x = tid + u * kNT, jj = x / kPieces, pc = x % kPieces;
       ph[u] = pl[u] = make_uint4(0, 0, 0, 0);
       if (jj < nj) {
         if (kBf) {
@@ -879,73 +898,83 @@ __global__ __launch_bounds__(kAssignThreads, sizeof(T) == 2 ? 4 : 2) void lloyd_
         }
       }
     }
-    if (tid < kCenterChunk) pn = tid < nj ? a.cnorm[cbase + j0 + tid] : __builtin_huge_valf();
+    if (tid < kCC) pn = tid < nj ? a.cnorm[cbase + j0 + tid] : __builtin_huge_valf();
   };
   auto commit = [&]() {
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
-      const int x = tid + u * kAssignThreads, jj = x / kPieces, pc = x % kPieces;
+      const int x = tid + u * kNT, jj = x / kPieces, pc = x % kPieces;
       *reinterpret_cast<uint4*>(s_c + jj * kRowB + pc * 16) = ph[u];
-      if (kBf) *reinterpret_cast<uint4*>(s_c + (kCenterChunk + jj) * kRowB + pc * 16) = pl[u];
+      if (kBf) *reinterpret_cast<uint4*>(s_c + (kCC + jj) * kRowB + pc * 16) = pl[u];
     }
-    if (tid < kCenterChunk) s_norm[tid] = pn;
+    if (tid < kCC) s_norm[tid] = pn;
   };
   fetch(0);
   commit();
-  for (int j0 = 0; j0 < hm.r_eff; j0 += kCenterChunk) {
-    const int nj = min(kCenterChunk, hm.r_eff - j0);
+  for (int j0 = 0; j0 < hm.r_eff; j0 += kCC) {
+    const int nj = min(kCC, hm.r_eff - j0);
     __syncthreads();  // the chunk in LDS is complete
-    if (j0 + kCenterChunk < hm.r_eff) fetch(j0 + kCenterChunk);
+    if (j0 + kCC < hm.r_eff) fetch(j0 + kCC);
     const int nct = (nj + 15) / 16;
     for (int ct = 0; ct < nct; ++ct) {  // block-uniform
       const int crow = 16 * ct + col;
-      Frag<T, D> ch, cl;
+      f32x4_t acc[kTT];
+#pragma unroll
+      for (int tt = 0; tt < kTT; ++tt) acc[tt] = zero4();
       if constexpr (kBf) {
-        ch.load(reinterpret_cast<const uint16_t*>(s_c + crow * kRowB), grp);
-        cl.load(reinterpret_cast<const uint16_t*>(s_c + (kCenterChunk + crow) * kRowB), grp);
+        // one k-step of the hi and lo centre rows at a time: 8 elements per
+        // lane, the same pieces as the token fragments (Frag layout)
+        const unsigned char* rh = s_c + crow * kRowB + 16 * grp;
+        const unsigned char* rl = s_c + (kCC + crow) * kRowB + 16 * grp;
+#pragma unroll
+        for (int k = 0; k < kSteps; ++k) {
+          const uint4 ch = *reinterpret_cast<const uint4*>(rh + 64 * k);
+          const uint4 cl = *reinterpret_cast<const uint4*>(rl + 64 * k);
+#pragma unroll
+          for (int tt = 0; tt < kTT; ++tt)
+            acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ch), as_bf16x8(tk[tt].w[k]), acc[tt], 0, 0, 0);
+#pragma unroll
+          for (int tt = 0; tt < kTT; ++tt)
+            acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cl), as_bf16x8(tk[tt].w[k]), acc[tt], 0, 0, 0);
+        }
       } else {
-        ch.load(reinterpret_cast<const float*>(s_c + crow * kRowB), grp);
-      }
-      f32x4_t acc[kTokTiles];
-#pragma unroll
-      for (int tt = 0; tt < kTokTiles; ++tt) acc[tt] = zero4();
-#pragma unroll
-      for (int k = 0; k < kSteps; ++k)
-#pragma unroll
-        for (int tt = 0; tt < kTokTiles; ++tt) acc[tt] = mma_step<D>(ch, tk[tt], k, acc[tt]);
-      if constexpr (kBf) {
+        Frag<T, D> ch;
+        ch.load(reinterpret_cast<const T*>(s_c + crow * kRowB), grp);
 #pragma unroll
         for (int k = 0; k < kSteps; ++k)
 #pragma unroll
-          for (int tt = 0; tt < kTokTiles; ++tt) acc[tt] = mma_step<D>(cl, tk[tt], k, acc[tt]);
+          for (int tt = 0; tt < kTT; ++tt) acc[tt] = mma_step<D>(ch, tk[tt], k, acc[tt]);
       }
       float nrm[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) nrm[i] = s_norm[16 * ct + 4 * grp + i];
       const int jb = j0 + 16 * ct + 4 * grp;
 #pragma unroll
-      for (int tt = 0; tt < kTokTiles; ++tt)
+      for (int tt = 0; tt < kTT; ++tt) {
+        // the lane's 4 centres in ascending order, then against earlier tiles
+        float bv = fmaf(-2.f, acc[tt][0], nrm[0]);
+        int bi = jb;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 1; i < 4; ++i) {
           const float dist = fmaf(-2.f, acc[tt][i], nrm[i]);
-          const bool win = dist < best[tt][i];
-          best[tt][i] = win ? dist : best[tt][i];
-          bidx[tt][i] = win ? jb + i : bidx[tt][i];
+          bi = dist < bv ? jb + i : bi;
+          bv = dist < bv ? dist : bv;
         }
+        bidx[tt] = bv < best[tt] ? bi : bidx[tt];
+        best[tt] = bv < best[tt] ? bv : best[tt];
+      }
     }
-    if (j0 + kCenterChunk < hm.r_eff) {  // block-uniform
+    if (j0 + kCC < hm.r_eff) {  // block-uniform
       __syncthreads();  // every wave is done with this chunk
       commit();
     }
   }
-  // argmin over the 16 centres of a lane (4 rows x 4 lane groups): ties to lower index
+  // argmin across the 4 lane groups (centres interleave across them): ties
+  // to the lower index
 #pragma unroll
-  for (int tt = 0; tt < kTokTiles; ++tt) {
-    float bv = best[tt][0];
-    int bi = bidx[tt][0];
-#pragma unroll
-    for (int i = 1; i < 4; ++i)
-      if (best[tt][i] < bv || (best[tt][i] == bv && bidx[tt][i] < bi)) { bv = best[tt][i]; bi = bidx[tt][i]; }
+  for (int tt = 0; tt < kTT; ++tt) {
+    float bv = best[tt];
+    int bi = bidx[tt];
 #pragma unroll
     for (int msk = 16; msk < 64; msk <<= 1) {
       const float ov = __shfl_xor(bv, msk, 64);
@@ -953,16 +982,28 @@ __global__ __launch_bounds__(kAssignThreads, sizeof(T) == 2 ? 4 : 2) void lloyd_
       if (ov < bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
     }
     if (bi >= hm.r_eff) bi = 0;  // only reachable with non-finite keys
+    bidx[tt] = bi;
     const int i = tw + 16 * tt + col;
     if (grp == 0 && i < hm.nE) {
       a.assign[(size_t)bh * a.S + i] = bi;
-      atomicAdd(&s_hist[bi], 1);
       if (a.dbg_assign) a.dbg_assign[((size_t)iter * a.B * a.Hkv + bh) * a.S + elist[i]] = bi;
     }
   }
-  __syncthreads();
-  int32_t* hist = a.hist + ((size_t)bh * a.NBLK + blk) * a.Rcap;
-  for (int j = tid; j < hm.r_eff; j += kAssignThreads) hist[j] = s_hist[j];
+  // group histograms of the 256-token blocks of the evicted list that this
+  // block covers and that hold tokens, one at a time through LDS
+  for (int q = 0; q < kSubs && t0 + q * kTokBlock < hm.nE; ++q) {  // block-uniform
+    for (int j = tid; j < hm.r_eff; j += kNT) s_hist[j] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < kTT; ++tt) {
+      const int i = tw + 16 * tt + col;
+      if (grp == 0 && i < hm.nE && (i - t0) / kTokBlock == q) atomicAdd(&s_hist[bidx[tt]], 1);
+    }
+    __syncthreads();
+    int32_t* hist = a.hist + ((size_t)bh * a.NBLK + blk * kSubs + q) * a.Rcap;
+    for (int j = tid; j < hm.r_eff; j += kNT) hist[j] = s_hist[j];
+    __syncthreads();
+  }
 }
 
 // Group sizes and counting-sort offsets: hist[blk][j] becomes the first
@@ -1210,8 +1251,9 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
   if (pl.max_reff > 0) {
     hipLaunchKernelGGL((center_prep<D>), grid(pl.max_reff), dim3(kThreads), 0, st, a); RESKV_CHECK();
     const size_t hist_lds = (size_t)pl.max_reff * sizeof(int);
+    const int ablk = (pl.max_E + AssignShape<T>::kTokens - 1) / AssignShape<T>::kTokens;
     for (int it = 0; it < pl.T; ++it) {
-      hipLaunchKernelGGL((lloyd_assign<T, D>), grid(pl.NBLK), dim3(kAssignThreads), hist_lds, st, a, it);
+      hipLaunchKernelGGL((lloyd_assign<T, D>), grid(ablk), dim3(AssignShape<T>::kThreads), hist_lds, st, a, it);
       RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), 0, st, a); RESKV_CHECK();
