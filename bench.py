@@ -273,6 +273,21 @@ def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
                 seconds_measured=t_score + t_lloyd + t_dec)
 
 
+def workload_text(wl, L):
+    """What one timed step covers, with the workload's sizes."""
+    import numpy as np
+    ctx = (f"context {wl.ctx[0]}" if min(wl.ctx) == max(wl.ctx)
+           else f"contexts {min(wl.ctx)}-{max(wl.ctx)} (ragged)")
+    bud = (f"budget {wl.budget[0]}" if min(wl.budget) == max(wl.budget)
+           else f"budgets {sorted(set(int(b) for b in wl.budget))}")
+    rs = sorted(set(int(x) for x in np.unique(wl.res[:L])))
+    rtxt = f"residual r per (layer, head) in {{{','.join(map(str, rs))}}}" if len(rs) <= 6 else \
+        f"residual r per (layer, head) from {rs[0]} to {rs[-1]}"
+    return (f"{wl.name}: {L} layers x (Hq {wl.hq} / Hkv {wl.hkv}, head_dim {wl.d}), batch {wl.batch}, {ctx} -> "
+            f"{bud} per KV head, {rtxt}, {wl.steps} decode steps with appends; "
+            f"step = construction of all layers + all decode steps")
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -437,12 +452,8 @@ def main():
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded; LLM-shaped keys with outlier channels and heavy tokens)",
-        "config": {"workload": (f"batched decode: {L} layers x (Hq {Hq} / Hkv {Hkv}, head_dim {d}), batch {B}, "
-                                f"context {wl.ctx[0]} -> budget {wl.budget[0]} per KV head, residual r per "
-                                f"(layer, head) in {{0,64,128,256,512}}, {wl.steps} decode steps with appends; "
-                                f"step = construction of all layers + all decode steps"),
-                   "global_batch": B, "seq_len": wl.ctx[0], "layers": L, "decode_steps": wl.steps,
-                   "budget": wl.budget[0], "parallelism": "single GPU"},
+        "config": {"workload": workload_text(wl, L), "global_batch": B, "seq_len": int(max(wl.ctx)), "layers": L,
+                   "decode_steps": wl.steps, "budget": int(max(wl.budget)), "parallelism": "single GPU"},
         "decode_tokens_per_s": tokens / (decode_ms * 1e-3),
         "decode_ms_per_job": decode_ms,
         "decode_gbs": dec_bytes_job / (decode_ms * 1e-3) / 1e9,
@@ -451,8 +462,10 @@ def main():
         "construction_mfma": cmfma,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "reskv_decode_attn (one launch per layer-step: decode_head, one block per "
-                               "(sequence, KV head), append fused)",
+                     "kernel": ("reskv_decode_attn (one launch per layer-step: decode_head, one block per "
+                                "(sequence, KV head), append fused)" if B * Hkv >= 256 and (elem == 2 or d == 64) else
+                                "reskv_decode_attn (per layer-step: append, decode_split over 256-slot blocks, "
+                                "decode_combine with the gate)"),
                      "bytes_per_call": avg_bytes, "us_per_call": avg_ms * 1e3,
                      "calls_timed": calls * args.steps},
         "setup_s": t_setup,

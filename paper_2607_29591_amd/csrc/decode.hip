@@ -586,8 +586,10 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   const T* vn = app ? static_cast<const T*>(a.v_new) + (size_t)bh * D : nullptr;
   if (app) n += 1;
 
-  __shared__ float s_acc[2][kHeadWaves][GP][D];  // per kind (0 residual, 1 main), per wave
-  __shared__ float s_m[2][kHeadWaves][GP];
+  // one accumulator row per wave and query head, used for the residual
+  // states first and then for the main states (64 KB at 16 query heads)
+  __shared__ float s_acc[kHeadWaves][GP][D];
+  __shared__ float s_m[2][kHeadWaves][GP];  // per kind (0 residual, 1 main), per wave
   __shared__ float s_l[2][kHeadWaves][GP];
 
   Frag<T, D> q;
@@ -610,7 +612,7 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
     unit_range(u, is_res, s0, end);
     const int nvalid = min(kUnit, end - s0);
     if (!is_res && in_res) {
-      store_wave_state<D, GP>(st, s_acc[0][wave], s_m[0][wave], s_l[0][wave], hd, g);
+      store_wave_state<D, GP>(st, s_acc[wave], s_m[0][wave], s_l[0][wave], hd, g);
       st.reset();
       in_res = false;
     }
@@ -656,49 +658,64 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
     run_unit(u, ur);
   }
   if (in_res) {
-    store_wave_state<D, GP>(st, s_acc[0][wave], s_m[0][wave], s_l[0][wave], hd, g);
+    store_wave_state<D, GP>(st, s_acc[wave], s_m[0][wave], s_l[0][wave], hd, g);
     st.reset();
   }
-  store_wave_state<D, GP>(st, s_acc[1][wave], s_m[1][wave], s_l[1][wave], hd, g);
   __syncthreads();
 
-  // merge the waves per kind, then the gate and the shared denominator
-  for (int idx = tid; idx < a.G * D; idx += kHeadThreads) {
+  // merge the waves' states of one kind for the outputs this thread owns:
+  // max, sum and accumulator of (head h, column d) over the 8 waves
+  constexpr int kPer = (GP * D + kHeadThreads - 1) / kHeadThreads;
+  auto merge = [&](int kind, int idx, float& M, float& l, float& o) {
     const int h = idx / D, d = idx % D;
-    float Mk[2], lk[2], ok[2];
+    M = s_m[kind][0][h];
 #pragma unroll
-    for (int kind = 0; kind < 2; ++kind) {
-      float M = s_m[kind][0][h];
+    for (int w = 1; w < kHeadWaves; ++w) M = fmaxf(M, s_m[kind][w][h]);
+    o = 0.f;
+    l = 0.f;
+    if (M != kNegInf) {
 #pragma unroll
-      for (int w = 1; w < kHeadWaves; ++w) M = fmaxf(M, s_m[kind][w][h]);
-      float o = 0.f, l = 0.f;
-      if (M != kNegInf) {
-#pragma unroll
-        for (int w = 0; w < kHeadWaves; ++w) {
-          const float f = exp2f(s_m[kind][w][h] - M);
-          o = fmaf(f, s_acc[kind][w][h][d], o);
-          l = fmaf(f, s_l[kind][w][h], l);
-        }
+      for (int w = 0; w < kHeadWaves; ++w) {
+        const float f = exp2f(s_m[kind][w][h] - M);
+        o = fmaf(f, s_acc[w][h][d], o);
+        l = fmaf(f, s_l[kind][w][h], l);
       }
-      Mk[kind] = M; lk[kind] = l; ok[kind] = o;
     }
-    const float M = Mk[1], l = lk[1], mR = Mk[0], lR = lk[0];
+  };
+  float mR[kPer], lR[kPer], oR[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int idx = tid + k * kHeadThreads;
+    if (idx < a.G * D) merge(0, idx, mR[k], lR[k], oR[k]);
+  }
+  __syncthreads();  // the residual rows are merged: the buffer takes the main states
+  store_wave_state<D, GP>(st, s_acc[wave], s_m[1][wave], s_l[1][wave], hd, g);
+  __syncthreads();
+
+  // main states, then the gate and the shared denominator
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int idx = tid + k * kHeadThreads;
+    if (idx >= a.G * D) continue;
+    const int h = idx / D, d = idx % D;
+    float M, l, oM;
+    merge(1, idx, M, l, oM);
     // p_max = 1 / l_main (the max term is exactly 1), then the gate
     const float pmax = l > 0.f ? 1.f / l : 1.f;
     const int qh = b * a.Hq + kvh * a.G + h;
     const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
     const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
     const float lg2g = g > 0.f ? log2f(g) : kNegInf;
-    const float mRg = (mR == kNegInf || lg2g == kNegInf) ? kNegInf : mR + lg2g;
+    const float mRg = (mR[k] == kNegInf || lg2g == kNegInf) ? kNegInf : mR[k] + lg2g;
     const float Mx = fmaxf(M, mRg);
     const float fM = M != kNegInf ? exp2f(M - Mx) : 0.f;
     const float fR = mRg != kNegInf ? exp2f(mRg - Mx) : 0.f;
-    const float den = l * fM + lR * fR;
-    const float num = ok[1] * fM + ok[0] * fR;
+    const float den = l * fM + lR[k] * fR;
+    const float num = oM * fM + oR[k] * fR;
     a.out[(size_t)qh * D + d] = den > 0.f ? num / den : 0.f;
     if (d == 0) {
       if (a.dbg_lse_main) a.dbg_lse_main[qh] = l > 0.f ? (M + log2f(l)) * kLn2 : kNegInf;
-      if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR > 0.f ? (mR + log2f(lR)) * kLn2 : kNegInf;
+      if (a.dbg_lse_res) a.dbg_lse_res[qh] = lR[k] > 0.f ? (mR[k] + log2f(lR[k])) * kLn2 : kNegInf;
       if (a.dbg_gate) a.dbg_gate[qh] = g;
     }
   }
@@ -724,7 +741,7 @@ __global__ void append_kernel(const T* k_new, const T* v_new, T* kc, T* vc, cons
 
 template <typename T, int D, int GP>
 hipError_t launch_typed(const DecodePlan& pl, const DecodeArgs& da, hipStream_t stream) {
-  if constexpr (GP <= 4) {
+  if constexpr (sizeof(T) == 2 || D == 64) {  // the shapes make_decode_plan sends here
     if (pl.whole_head && !da.out_res) {
       hipLaunchKernelGGL((decode_head<T, D, GP>), dim3(pl.Hkv, pl.B), dim3(kHeadThreads), 0, stream, da);
       return hipGetLastError();
@@ -766,8 +783,7 @@ DecodePlan make_decode_plan(const reskv_shape_t& s) {
   p.P = p.PR + (s.slot_cap + kChunk - 1) / kChunk;
   // one block per (b, kv head) when those alone fill the chip's CUs (fp32
   // rows of 128 take the split kernels: the head kernel would spill)
-  p.whole_head = p.GP <= 4 && (long long)p.B * p.Hkv >= kWholeHeadMin &&
-                 (s.dtype == RESKV_BF16 || p.D == 64);
+  p.whole_head = (long long)p.B * p.Hkv >= kWholeHeadMin && (s.dtype == RESKV_BF16 || p.D == 64);
   const size_t recs = (size_t)p.B * p.Hkv * p.P * p.GP;
   p.acc_off = 0;
   p.ml_off = align_up(recs * p.D * sizeof(float), 256);

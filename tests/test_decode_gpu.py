@@ -169,13 +169,14 @@ def test_append_then_decode(dtype):
 
 
 @pytest.mark.parametrize("dtype,d,G,B,Hkv", [("bf16", 128, 4, 32, 8), ("f32", 64, 2, 64, 4), ("bf16", 64, 1, 16, 16),
-                                             ("bf16", 128, 4, 2, 2), ("f32", 128, 7, 2, 2)])
+                                             ("bf16", 128, 4, 2, 2), ("f32", 128, 7, 2, 2), ("bf16", 128, 7, 64, 4),
+                                             ("bf16", 64, 16, 32, 8)])
 def test_decode_fused_append(dtype, d, G, B, Hkv):
     """reskv_decode_attn with this step's K/V: the token is appended as main
     slot r + n (cache and main_len written) and attended in the same call.
-    B*Hkv >= 256 with G <= 4 (bf16, or fp32 rows of 64) takes the
-    one-block-per-head kernel; the others the split-K kernels; full caches are
-    left unchanged."""
+    B*Hkv >= 256 (bf16, or fp32 rows of 64) takes the one-block-per-head
+    kernel, for any group size up to 16; the others the split-K kernels;
+    full caches are left unchanged."""
     rng = np.random.default_rng(11 + d + G)
     C, Rcap = 300, 64
     res = rng.choice([0, 16, 64], size=(B, Hkv))
@@ -222,3 +223,22 @@ def test_decode_whole_head_path_shapes(dtype, d):
     shape, q, kc, vc, logc = cache_case(40 + d, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
     heads = [(int(b), int(h)) for b, h in zip(rng.integers(0, B, 40), rng.integers(0, G * Hkv, 40))]
     check(dtype, shape, q, kc, vc, logc, res, main, heads=heads)
+
+
+@pytest.mark.parametrize("dtype,d,G", [("bf16", 128, 7), ("bf16", 128, 8), ("bf16", 64, 16), ("f32", 64, 7),
+                                       ("bf16", 128, 16)])
+def test_decode_whole_head_wide_groups(dtype, d, G):
+    """256 (b, kv head) pairs with more than 4 query heads per KV head (the
+    ragged GQA-7 workload's group, 8 and 16): the one-block-per-head kernel,
+    whose waves merge the residual states and then the main states through
+    one LDS buffer; ragged lengths, r = 0 heads, empty entries, per-query
+    thresholds."""
+    B, Hkv = 64, 4
+    rng = np.random.default_rng(50 + d + G)
+    C, Rcap = 640, 130
+    res = rng.choice([0, 1, 63, 130], size=(B, Hkv))
+    main = rng.integers(1, C - 130, size=(B, Hkv))
+    shape, q, kc, vc, logc = cache_case(60 + d + G, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+    heads = [(int(b), int(h)) for b, h in zip(rng.integers(0, B, 48), rng.integers(0, G * Hkv, 48))]
+    tau = rng.normal(0.0, 0.5, size=(B, G * Hkv))
+    check(dtype, shape, q, kc, vc, logc, res, main, heads=heads, tau=tau)
