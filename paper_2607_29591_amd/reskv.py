@@ -207,6 +207,26 @@ def reskv_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, work
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
+def prepare_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, workspace,
+                        dbg_lse_main=None, dbg_lse_res=None, dbg_gate=None, k_new=None, v_new=None, stream=None):
+    """Marshal the arguments of one reskv_decode_attn call once and return a
+    function that issues it (for loops that launch the same calls many
+    times). The caller keeps the tensors alive and unchanged in place."""
+    fn = lib().reskv_decode_attn
+    args = (ctypes.byref(shape), ctypes.byref(gate), _ptr(q), _ptr(kc), _ptr(vc), _ptr(logc), _ptr(res_len),
+            _ptr(main_len), _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(dbg_lse_main), _ptr(dbg_lse_res),
+            _ptr(dbg_gate), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    keep = (shape, gate)
+
+    def call():
+        status = fn(*args)
+        if status != 0:
+            _check(status)
+
+    call.keep = keep
+    return call
+
+
 RESKV_MERGE_SHARED, RESKV_MERGE_SEPARATE = 0, 1
 
 

@@ -220,3 +220,13 @@ def test_adakv_rejects_small_workspace(L):
         rk.reskv_build_cache_adakv(sh, p, 0.2, t, t, (300,), t, (64,), [13, 0], t, t, t, t, t, t, FakeTensor(8),
                                    stream=FakeStream())
     assert ei.value.status == 3
+
+
+def test_prepared_decode_call_reports_errors(L):
+    """A prepared call validates like the direct call: a bad shape raises
+    when it is issued, before anything is launched."""
+    t = FakeTensor()
+    call = rk.prepare_decode_attn(shape(head_dim=96), rk.make_gate(), t, t, t, t, t, t, t, t, stream=FakeStream())
+    with pytest.raises(rk.ReskvError) as ei:
+        call()
+    assert ei.value.status == 2

@@ -242,3 +242,37 @@ def test_decode_whole_head_wide_groups(dtype, d, G):
     heads = [(int(b), int(h)) for b, h in zip(rng.integers(0, B, 48), rng.integers(0, G * Hkv, 48))]
     tau = rng.normal(0.0, 0.5, size=(B, G * Hkv))
     check(dtype, shape, q, kc, vc, logc, res, main, heads=heads, tau=tau)
+
+
+def test_prepared_decode_call_matches_direct_call():
+    """prepare_decode_attn marshals the arguments once; issuing it twice
+    (each call appends a token) gives the same caches, lengths and outputs,
+    bit for bit, as two reskv_decode_attn calls."""
+    B, Hkv, G, d, dtype = 4, 2, 4, 128, "bf16"
+    rng = np.random.default_rng(77)
+    C, Rcap = 200, 32
+    res = rng.choice([0, 16, 32], size=(B, Hkv))
+    main = rng.integers(1, C - 40, size=(B, Hkv))
+    shape, q, kc, vc, logc = cache_case(77, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+    kn, vn = to_dev(rng.normal(size=(B, Hkv, d)), dtype), to_dev(rng.normal(size=(B, Hkv, d)), dtype)
+    qd = to_dev(q, dtype)
+    runs = []
+    for prepared in (False, True):
+        kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
+        lcd = torch.as_tensor(logc.astype(np.float32)).cuda()
+        rl = torch.as_tensor(res.astype(np.int32).reshape(-1)).cuda()
+        ml = torch.as_tensor(main.astype(np.int32).reshape(-1)).cuda()
+        out = torch.empty((B, G * Hkv, d), device="cuda")
+        ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+        gate = rk.make_gate()
+        if prepared:
+            call = rk.prepare_decode_attn(shape, gate, qd, kcd, vcd, lcd, rl, ml, out, ws, k_new=kn, v_new=vn)
+            call()
+            call()
+        else:
+            for _ in range(2):
+                rk.reskv_decode_attn(shape, gate, qd, kcd, vcd, lcd, rl, ml, out, ws, k_new=kn, v_new=vn)
+        torch.cuda.synchronize()
+        runs.append([t.cpu() for t in (kcd, vcd, ml, out)])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
