@@ -292,7 +292,9 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "bench.py measures one GPU: the ResKV hot path here is built and timed on a "
-                                   "single MI355X; multi-GPU runs are not part of this build", "n_gpus": args.gpus}))
+                                   "single MI355X and has no multi-GPU mode (every (sequence, KV head) is "
+                                   "independent, so sharding by sequence or KV head needs no communication)",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
     import numpy as np
     import torch
