@@ -92,6 +92,17 @@ struct BuildArgs {
   float scale2;        // log2(e) / sqrt(d)
 };
 
+// (b, kv head) of a block from blockIdx.y / .z; with rev set the heads are
+// walked in the opposite order, so a kernel that re-reads the keys of the
+// kernel before it starts with the heads that kernel read last (still in the
+// memory-side cache) instead of the ones it read first.
+__device__ __forceinline__ void block_head(const BuildArgs& a, int rev, int& b, int& kvh, int& bh) {
+  bh = blockIdx.z * a.Hkv + blockIdx.y;
+  if (rev) bh = a.B * a.Hkv - 1 - bh;
+  b = bh / a.Hkv;
+  kvh = bh - b * a.Hkv;
+}
+
 __device__ __forceinline__ float to_f32(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ void store_elem(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
@@ -260,9 +271,10 @@ __global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
 // sums stay in registers until two final cross-lane steps, and no cross-wave
 // merge is needed.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a) {
-  const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int bh = b * a.Hkv + kvh;
+__global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a, int rev) {
+  const int ch = blockIdx.x;
+  int b, kvh, bh;
+  block_head(a, rev, b, kvh, bh);
   const HeadMeta hm = a.meta[bh];
   const int k0 = ch * kKeyChunk;
   if (hm.all_main || k0 >= hm.n_sc) return;
@@ -1084,9 +1096,10 @@ __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
 // order; an empty group keeps its centre. The last round also writes the
 // entry: mean key and mean value in the cache dtype, and log c_j.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void lloyd_update(BuildArgs a, int last) {
-  const int j = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int bh = b * a.Hkv + kvh;
+__global__ __launch_bounds__(kThreads) void lloyd_update(BuildArgs a, int last, int rev) {
+  const int j = blockIdx.x;
+  int b, kvh, bh;
+  block_head(a, rev, b, kvh, bh);
   const HeadMeta hm = a.meta[bh];
   if (j >= hm.r_eff) return;
   constexpr int CPR = D / 8;            // lanes per row, 8 elements each
@@ -1222,7 +1235,8 @@ hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStrea
   hipError_t e;
   hipLaunchKernelGGL((lse_partial<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
   hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
-  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  // the second pass over the keys walks the heads in reverse (cache reuse)
+  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a, 1); RESKV_CHECK();
   return hipSuccess;
 }
 
@@ -1257,7 +1271,9 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
       RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), 0, st, a); RESKV_CHECK();
-      hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, it == pl.T - 1 ? 1 : 0);
+      // the update walks the heads in reverse of the assignment before and
+      // after it, so each starts on the keys the other read last
+      hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, it == pl.T - 1 ? 1 : 0, 1);
       RESKV_CHECK();
     }
   }
