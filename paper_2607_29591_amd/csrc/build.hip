@@ -399,6 +399,25 @@ __device__ __forceinline__ int block_excl_scan(int v, int* s_tmp, int& total) {
   return off + x - v;
 }
 
+// Histogram increment of bin `dig` by the lanes with `act` set. Scores share
+// their leading digits (sign and exponent), so the lanes of a wave often hit
+// one bin: up to two leader rounds count the lanes that share the leader's
+// bin with one atomic each; the remaining lanes add their own. Called by
+// every lane of the wave (act false where a lane has nothing to count).
+__device__ __forceinline__ void wave_hist_add(int* hist, int dig, bool act, int lane) {
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const unsigned long long m = __ballot(act);
+    if (m == 0ull) return;  // wave-uniform
+    const int leader = __ffsll((long long)m) - 1;
+    const int d = __shfl(dig, leader, 64);
+    const unsigned long long same = __ballot(act && dig == d);
+    if (lane == leader) atomicAdd(&hist[d], __popcll(same));
+    act = act && dig != d;
+  }
+  if (act) atomicAdd(&hist[dig], 1);
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
@@ -427,18 +446,19 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = tid; i < 512; i += kSelThreads) (&s_hist[0][0])[i] = 0;
     __syncthreads();
-    // coalesced, four keys in flight per thread
-    for (int i0 = tid; i0 < n; i0 += 4 * kSelThreads) {
-      uint32_t u[4];
+    // coalesced, kHistBatch keys in flight per thread
+    constexpr int kHistBatch = 16;
+    for (int i0 = tid; i0 < n; i0 += kHistBatch * kSelThreads) {
+      uint32_t u[kHistBatch];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) u[v] = i0 + v * kSelThreads < n ? key[i0 + v * kSelThreads] : 0u;
+      for (int v = 0; v < kHistBatch; ++v) u[v] = i0 + v * kSelThreads < n ? key[i0 + v * kSelThreads] : 0u;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        if (i0 + v * kSelThreads >= n) continue;
+      for (int v = 0; v < kHistBatch; ++v) {
         const int dig = (u[v] >> shift) & 0xff;
+        const bool in = i0 + v * kSelThreads < n;
 #pragma unroll
         for (int q = 0; q < 2; ++q)
-          if (krem[q] > 0 && (u[v] & mask) == prefix[q]) atomicAdd(&s_hist[q][dig], 1);
+          wave_hist_add(s_hist[q], dig, in && krem[q] > 0 && (u[v] & mask) == prefix[q], lane);
       }
     }
     __syncthreads();
@@ -497,6 +517,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   constexpr int kSegKeys = 32;
   uint32_t seg[kSegKeys];
   const bool in_regs = L <= kSegKeys;  // block-uniform
+  // longer segments: the keys of [lo, hi) in order, read kSegKeys at a time
+  // with every load of a batch in flight together
+  auto for_segment = [&](int lo_, int hi_, auto&& f) {
+    for (int i0 = lo_; i0 < hi_; i0 += kSegKeys) {
+      uint32_t b[kSegKeys];
+#pragma unroll
+      for (int v = 0; v < kSegKeys; ++v) b[v] = i0 + v < hi_ ? key[i0 + v] : 0u;
+#pragma unroll
+      for (int v = 0; v < kSegKeys; ++v)
+        if (i0 + v < hi_) f(i0 + v, b[v]);
+    }
+  };
   if (in_regs) {
 #pragma unroll
     for (int v = 0; v < kSegKeys; ++v) seg[v] = lo + v < hi ? key[lo + v] : 0u;
@@ -508,11 +540,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
     for (int v = 0; v < kSegKeys; ++v)
       if (lo + v < hi) { e1 += (seg[v] == T1); e2 += (seg[v] == T2); }
   } else {
-    for (int i = lo; i < hi; ++i) {
-      const uint32_t u = key[i];
+    for_segment(lo, hi, [&](int, uint32_t u) {
       e1 += (u == T1);
       e2 += (u == T2);
-    }
+    });
   }
   int tot;
   int eb1 = block_excl_scan<kSelThreads>(e1, s_tmp, tot);
@@ -539,13 +570,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
         }
       }
     } else {
-      for (int i = lo; i < hi; ++i) {
+      for_segment(lo, hi, [&](int, uint32_t u) {
         bool top, sel2;
-        classify(key[i], r1, r2, top, sel2);
+        classify(u, r1, r2, top, sel2);
         c_top += top;
         c_ev += !top;
         c_seed += (sel2 && !top);
-      }
+      });
     }
   }
   int ob_top = block_excl_scan<kSelThreads>(c_top, s_tmp, tot);
@@ -568,7 +599,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
       for (int v = 0; v < kSegKeys; ++v)
         if (lo + v < hi) emit(lo + v, seg[v]);
     } else {
-      for (int i = lo; i < hi; ++i) emit(i, key[i]);
+      for_segment(lo, hi, emit);
     }
   }
   // the protected recent window follows the top-scored tokens
