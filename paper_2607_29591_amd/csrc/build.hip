@@ -671,7 +671,7 @@ __global__ __launch_bounds__(kAdaThreads) void adakv_alloc(BuildArgs a, HeadMeta
         for (int v = 0; v < 4; ++v) u[v] = i0 + v * kAdaThreads < n ? key[i0 + v * kAdaThreads] : 0u;
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-          if (i0 + v * kAdaThreads < n && (u[v] & mask) == prefix) atomicAdd(&s_hist[h][(u[v] >> shift) & 0xff], 1);
+          wave_hist_add(s_hist[h], (u[v] >> shift) & 0xff, i0 + v * kAdaThreads < n && (u[v] & mask) == prefix, lane);
       }
     }
     __syncthreads();
