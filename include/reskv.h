@@ -15,6 +15,10 @@
  * hipStream_t; NULL is the null stream). Calls are asynchronous: argument
  * errors are reported by the return value before anything is launched;
  * faults inside a kernel surface at the caller's next synchronisation.
+ * A call enqueues kernel launches only (no memset, copy, allocation or
+ * synchronisation), and decode reads the cache lengths on the device, so
+ * calls can be captured into a HIP graph and replayed; host arrays (_host)
+ * are read when the call is made, i.e. at capture.
  *
  * Shapes: B = batch, Hq / Hkv = query / KV heads with Hq % Hkv == 0 and
  * G = Hq / Hkv <= 16 (grouped-query attention: query head h reads KV head
