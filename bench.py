@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--decode-steps", type=int, default=None, help="override decode steps per job (testing only)")
     ap.add_argument("--layers", type=int, default=None, help="override layer count (testing only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager-decode", action="store_true",
+                    help="issue the decode calls one by one instead of replaying them as one HIP graph")
     ap.add_argument("--cpu-budget-s", type=float, default=25.0)
     ap.add_argument("--mode", choices=["job", "decode", "proxy"], default="job",
                     help="job: the timed whole job (default); decode: build once, then only decode calls "
@@ -356,6 +358,8 @@ def main():
                                          dec_ws, k_new=kn_stage[l, t], v_new=vn_stage[l, t], stream=stream)
                   for l in range(L)] for t in range(wl.steps)]
 
+    dec_graph = None
+
     def job(record):
         eb0 = torch.cuda.Event(enable_timing=True)
         eb1 = torch.cuda.Event(enable_timing=True)
@@ -366,12 +370,32 @@ def main():
                                  res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"], c["main_idx"],
                                  c["res_len"], c["main_len"], build_ws)
         eb1.record(stream)
-        for calls in dec_calls:
-            for call in calls:  # this step's token is appended inside each decode call
-                call()
+        if dec_graph is not None:
+            dec_graph.replay()
+        else:
+            for calls in dec_calls:
+                for call in calls:  # this step's token is appended inside each decode call
+                    call()
         ed = torch.cuda.Event(enable_timing=True)
         ed.record(stream)
         return eb0, eb1, ed
+
+    def capture_decode():
+        """All decode calls of a job as one HIP graph (the library enqueues
+        kernel launches only), captured on a stream of its own after the
+        kernels have run once eagerly."""
+        cap = torch.cuda.Stream()
+        calls = [[rk.prepare_decode_attn(shape, gates[l][t], q_stage[l, t], caches[l]["kc"], caches[l]["vc"],
+                                         caches[l]["logc"], caches[l]["res_len"], caches[l]["main_len"], out,
+                                         dec_ws, k_new=kn_stage[l, t], v_new=vn_stage[l, t], stream=cap)
+                  for l in range(L)] for t in range(wl.steps)]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            for step in calls:
+                for call in step:
+                    call()
+        torch.cuda.synchronize()
+        return g
 
     if args.mode == "proxy":
         pr = proxy_runs(rk, torch, wl, shape, layers, caches, L, dev)
@@ -408,6 +432,18 @@ def main():
 
     for _ in range(args.warmup):
         job(False)
+    decode_launch = "eager"
+    if not args.eager_decode:
+        if args.warmup == 0:
+            for call in dec_calls[0]:  # every decode kernel runs once before the capture
+                call()
+        torch.cuda.synchronize()
+        try:
+            dec_graph = capture_decode()
+            decode_launch = "hip_graph"
+        except Exception as exc:  # keep the eager calls
+            dec_graph = None
+            decode_launch = f"eager (graph capture failed: {exc})"
     torch.cuda.synchronize()
     phase = []
     t0 = time.perf_counter()
@@ -416,6 +452,14 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1000 / args.steps
+    graph_check = None
+    if dec_graph is not None:
+        # the replayed job's last output against the same job issued call by call
+        out_graph = out.clone()
+        dec_graph = None
+        job(False)
+        torch.cuda.synchronize()
+        graph_check = "bitwise equal to eager calls" if torch.equal(out, out_graph) else "MISMATCH with eager calls"
     build_ms = sum(a.elapsed_time(b) for a, b, _ in phase) / args.steps
     decode_ms = sum(b.elapsed_time(c) for _, b, c in phase) / args.steps
 
@@ -473,6 +517,8 @@ def main():
                      "bytes_per_call": avg_bytes, "us_per_call": avg_ms * 1e3,
                      "calls_timed": calls * args.steps},
         "setup_s": t_setup,
+        "decode_launch": decode_launch,
+        "decode_graph_check": graph_check,
     }
     if args.proxy_layers > 0:
         # after the timed jobs: construction with the validation proxy choosing r
