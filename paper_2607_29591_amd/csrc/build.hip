@@ -881,8 +881,10 @@ struct AssignShape {
 // dist = ||mu||^2 - 2 mu.k, argmin with ties to the lower centre. All token
 // tiles of a wave advance through each k-step together, so the MFMA chains
 // are independent. Centres past r' are staged with an infinite norm and
-// never win.
-template <typename T, int D>
+// never win. kLo = false drops the lo part: the first round's centres are
+// bf16 key rows, so for finite keys lo is exactly zero there and the
+// distances are the same bit for bit with half the MFMAs.
+template <typename T, int D, bool kLo = true>
 __global__ __launch_bounds__(AssignShape<T>::kThreads, AssignShape<T>::kWavesPerSimd) void lloyd_assign(BuildArgs a, int iter) {
   constexpr bool kBf = sizeof(T) == 2;
   constexpr int kTT = AssignShape<T>::kTiles;
@@ -935,7 +937,7 @@ __global__ __launch_bounds__(AssignShape<T>::kThreads, AssignShape<T>::kWavesPer
       if (jj < nj) {
         if (kBf) {
           ph[u] = reinterpret_cast<const uint4*>(a.cent_hi + (cbase + j0 + jj) * D)[pc];
-          pl[u] = reinterpret_cast<const uint4*>(a.cent_lo + (cbase + j0 + jj) * D)[pc];
+          if (kLo) pl[u] = reinterpret_cast<const uint4*>(a.cent_lo + (cbase + j0 + jj) * D)[pc];
         } else {
           ph[u] = reinterpret_cast<const uint4*>(a.cent + (cbase + j0 + jj) * D)[pc];
         }
@@ -948,7 +950,7 @@ __global__ __launch_bounds__(AssignShape<T>::kThreads, AssignShape<T>::kWavesPer
     for (int u = 0; u < kPer; ++u) {
       const int x = tid + u * kNT, jj = x / kPieces, pc = x % kPieces;
       *reinterpret_cast<uint4*>(s_c + jj * kRowB + pc * 16) = ph[u];
-      if (kBf) *reinterpret_cast<uint4*>(s_c + (kCC + jj) * kRowB + pc * 16) = pl[u];
+      if (kBf && kLo) *reinterpret_cast<uint4*>(s_c + (kCC + jj) * kRowB + pc * 16) = pl[u];
     }
     if (tid < kCC) s_norm[tid] = pn;
   };
@@ -972,13 +974,15 @@ __global__ __launch_bounds__(AssignShape<T>::kThreads, AssignShape<T>::kWavesPer
 #pragma unroll
         for (int k = 0; k < kSteps; ++k) {
           const uint4 ch = *reinterpret_cast<const uint4*>(rh + 64 * k);
-          const uint4 cl = *reinterpret_cast<const uint4*>(rl + 64 * k);
+          const uint4 cl = kLo ? *reinterpret_cast<const uint4*>(rl + 64 * k) : make_uint4(0, 0, 0, 0);
 #pragma unroll
           for (int tt = 0; tt < kTT; ++tt)
             acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ch), as_bf16x8(tk[tt].w[k]), acc[tt], 0, 0, 0);
+          if constexpr (kLo) {
 #pragma unroll
-          for (int tt = 0; tt < kTT; ++tt)
-            acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cl), as_bf16x8(tk[tt].w[k]), acc[tt], 0, 0, 0);
+            for (int tt = 0; tt < kTT; ++tt)
+              acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cl), as_bf16x8(tk[tt].w[k]), acc[tt], 0, 0, 0);
+          }
         }
       } else {
         Frag<T, D> ch;
@@ -1298,7 +1302,10 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
     const size_t hist_lds = (size_t)pl.max_reff * sizeof(int);
     const int ablk = (pl.max_E + AssignShape<T>::kTokens - 1) / AssignShape<T>::kTokens;
     for (int it = 0; it < pl.T; ++it) {
-      hipLaunchKernelGGL((lloyd_assign<T, D>), grid(ablk), dim3(AssignShape<T>::kThreads), hist_lds, st, a, it);
+      if (sizeof(T) == 2 && it == 0)  // centres are the seeds' bf16 keys: lo = 0
+        hipLaunchKernelGGL((lloyd_assign<T, D, false>), grid(ablk), dim3(AssignShape<T>::kThreads), hist_lds, st, a, it);
+      else
+        hipLaunchKernelGGL((lloyd_assign<T, D>), grid(ablk), dim3(AssignShape<T>::kThreads), hist_lds, st, a, it);
       RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), 0, st, a); RESKV_CHECK();
