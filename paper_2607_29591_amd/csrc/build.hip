@@ -48,7 +48,7 @@ namespace reskv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kKeyGroups = 4;     // 256-key groups per scoring block, streamed with key prefetch
+constexpr int kKeyGroups = 4;     // 256-key groups per scoring block, one after the other
 constexpr int kKeyChunk = 256 * kKeyGroups;  // keys per scoring block
 constexpr int kRowChunk = 128;     // window rows staged in LDS per scoring step
 // s_waitcnt immediate: vector-memory count 0, export and LDS/scalar counts
@@ -146,9 +146,11 @@ __device__ __forceinline__ void load_score_keys(Frag<T, D> (&f)[4], const T* K, 
 
 // lse pass: the MFMA is oriented keys x rows, C[key][row]: a lane holds 16
 // keys of one row, so a row's max and sum need only two cross-lane steps.
-// Each wave keeps a running (max, sum) per row over its key groups.
+// Each wave keeps a running (max, sum) per row over its key groups. A wave
+// holds one 64-key group at a time (no second key buffer): at three waves
+// per SIMD (bf16) the other blocks on the CU cover its load latency.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
+__global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 3 : 2)) void lse_partial(BuildArgs a) {
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
@@ -157,36 +159,32 @@ __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   constexpr int kQRowB = D * (int)sizeof(T) + 16;
-  constexpr int kRT = kRowChunk / 16;
   __shared__ __align__(16) unsigned char s_q[kRowChunk * kQRowB];
   __shared__ float2 s_ml[4][kRowChunk];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
   for (int r0 = 0; r0 < a.R; r0 += kRowChunk) {
     const int nrt = (min(kRowChunk, a.R - r0) + 15) / 16;
     if (r0 > 0) __syncthreads();  // the previous chunk's rows and records are consumed
-    Frag<T, D> kf[4], kn[4];
+    Frag<T, D> kf[4];
     load_score_keys<T, D>(kf, K, k0 + 64 * wave, hm.s, col, grp);
     stage_window_rows<T, D>(s_q, a, b, kvh, r0, 16 * nrt);
     __syncthreads();
-    float rm[kRT], rl[kRT];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) { rm[rt] = kNegInf; rl[rt] = 0.f; }
-    // The first group's keys have landed; without this the compiler's wait
-    // tracking cannot tell them from the in-loop prefetch and makes the first
-    // row tile of every group wait for the prefetch.
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    // running (max, sum) of row 16 rt + col over this wave's keys, kept in
+    // LDS so the row-tile loop need not be unrolled; the four lane groups
+    // hold the same reduced values and each lane reads back its own writes
+    for (int rt = 0; rt < nrt; ++rt) s_ml[wave][16 * rt + col] = make_float2(kNegInf, 0.f);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // the first group's keys have landed
 #pragma unroll 1
     for (int gi = 0; gi < kKeyGroups; ++gi) {
       const int kw = k0 + 256 * gi + 64 * wave;  // this wave's keys in group gi
-      if (gi + 1 < kKeyGroups) load_score_keys<T, D>(kn, K, kw + 256, hm.s, col, grp);
-      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of this group's work
+      if (gi > 0) load_score_keys<T, D>(kf, K, kw, hm.s, col, grp);
+      __builtin_amdgcn_sched_barrier(0);  // the group's key loads go out before its work
       // keys up to s - w are visible to every window row (and lie below s):
       // such waves skip the per-element masks
       auto rows = [&](auto full_tag) {
         constexpr bool kFull = decltype(full_tag)::value;
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-          if (rt >= nrt) break;
+#pragma unroll 1
+        for (int rt = 0; rt < nrt; ++rt) {
           const int t_row = r0 + 16 * rt + col;  // window row of this lane's column
           Frag<T, D> qf;
           qf.load(reinterpret_cast<const T*>(s_q + (16 * rt + col) * kQRowB), grp);
@@ -208,29 +206,23 @@ __global__ __launch_bounds__(kThreads) void lse_partial(BuildArgs a) {
           m = wave_xor_max(m, 16);
           m = wave_xor_max(m, 32);
           m = m == kNegInf ? kNegInf : m * a.scale2;
-          const float m_new = fmaxf(rm[rt], m);
+          const float2 st = s_ml[wave][16 * rt + col];
+          const float m_new = fmaxf(st.x, m);
           if (m_new == kNegInf) continue;
           float l = 0.f;
 #pragma unroll
           for (int j = 0; j < 16; ++j) l += fast_exp2(fmaf(v[j], a.scale2, -m_new));
           l = wave_xor_add(l, 16);
           l = wave_xor_add(l, 32);
-          rl[rt] = fmaf(rl[rt], fast_exp2(rm[rt] - m_new), l);
-          rm[rt] = m_new;
+          s_ml[wave][16 * rt + col] = make_float2(m_new, fmaf(st.y, fast_exp2(st.x - m_new), l));
         }
       };
       if (kw < hm.s) {  // wave-uniform
         if (kw + 64 <= hm.s - a.w + 1) rows(std::true_type{});
         else rows(std::false_type{});
       }
-      if (gi + 1 < kKeyGroups) {
-#pragma unroll
-        for (int t = 0; t < 4; ++t) kf[t] = kn[t];
-      }
+
     }
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt)
-      if (rt < nrt && grp == 0) s_ml[wave][16 * rt + col] = make_float2(rm[rt], rl[rt]);
     __syncthreads();
     for (int t = threadIdx.x; t < min(kRowChunk, a.R - r0); t += kThreads) {
       float M = kNegInf;
@@ -269,9 +261,10 @@ __global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
 
 // Score pass: C[row][key]: a lane holds one key of 4 rows, so the per-key
 // sums stay in registers until two final cross-lane steps, and no cross-wave
-// merge is needed.
+// merge is needed. One key group per wave at a time and a rolled row-tile
+// loop keep it at four waves per SIMD (bf16).
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a, int rev) {
+__global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 4 : 2)) void score_accum(BuildArgs a, int rev) {
   const int ch = blockIdx.x;
   int b, kvh, bh;
   block_head(a, rev, b, kvh, bh);
@@ -288,23 +281,23 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a, int rev) {
   for (int r0 = 0; r0 < a.R; r0 += kRowChunk) {
     const int nr = min(kRowChunk, a.R - r0), nrt = (nr + 15) / 16;
     if (r0 > 0) __syncthreads();  // the previous chunk's rows are consumed
-    Frag<T, D> kf[4], kn[4];
+    Frag<T, D> kf[4];
     load_score_keys<T, D>(kf, K, k0 + 64 * wave, hm.s, col, grp);
     stage_window_rows<T, D>(s_q, a, b, kvh, r0, 16 * nrt);
     for (int t = threadIdx.x; t < nr; t += kThreads) s_lse[t] = a.lse2[(size_t)bh * a.R + r0 + t];
     __syncthreads();
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // as in lse_partial: the first group's keys have landed
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // the first group's keys have landed
 #pragma unroll 1
     for (int gi = 0; gi < kKeyGroups; ++gi) {
       const int kw = k0 + 256 * gi + 64 * wave;  // this wave's keys in group gi
-      if (gi + 1 < kKeyGroups) load_score_keys<T, D>(kn, K, kw + 256, hm.s, col, grp);
-      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of this group's work
+      if (gi > 0) load_score_keys<T, D>(kf, K, kw, hm.s, col, grp);
+      __builtin_amdgcn_sched_barrier(0);  // the group's key loads go out before its work
       float ksum[4] = {0.f, 0.f, 0.f, 0.f};
       // keys up to s - w are visible to every window row: such waves skip the
       // per-element causal test (padded rows carry lse = +inf and add 0)
       auto rows = [&](auto full_tag) {
         constexpr bool kFull = decltype(full_tag)::value;
-#pragma unroll
+#pragma unroll 1
         for (int rt = 0; rt < kRT; ++rt) {
           if (rt >= nrt) break;
           Frag<T, D> qf;
@@ -345,10 +338,7 @@ __global__ __launch_bounds__(kThreads) void score_accum(BuildArgs a, int rev) {
           }
         }
       }
-      if (gi + 1 < kKeyGroups) {
-#pragma unroll
-        for (int t = 0; t < 4; ++t) kf[t] = kn[t];
-      }
+
     }
   }
 }
@@ -858,25 +848,28 @@ __device__ __forceinline__ f32x4_t mma_step(const Frag<float, D>& c, const Frag<
 
 // Tiling of the assignment. Each wave holds kTiles 16-token tiles of keys in
 // registers and streams the centres from LDS; every centre fragment read from
-// LDS feeds 2 * kTiles MFMAs (hi and lo parts for bf16), so LDS traffic per
-// MFMA falls as 1 / kTiles. bf16: 8 tiles (128 tokens per wave) at two waves
-// per SIMD, in blocks of 4 waves so that two blocks share a CU and one
-// block's key loads overlap the other's MFMAs; fp32 (twice the key
-// registers): 2 tiles, 8 waves, four waves per SIMD. Histograms stay per
-// 256-token block of the evicted list.
-template <typename T>
+// LDS feeds kTiles MFMAs per part (hi and lo for bf16), so LDS traffic per
+// MFMA falls as 1 / kTiles. bf16: 4 tiles (64 tokens per wave) in blocks of 4
+// waves at four waves per SIMD, so four blocks share a CU and drift out of
+// step: some load keys while others run MFMAs. At d = 128 the kernel with the
+// lo part stages 16 centres at a time, which keeps it within the 128
+// registers of that occupancy. fp32 (twice the key registers): 2 tiles,
+// 8 waves, four waves per SIMD. Histograms stay per 256-token block of the
+// evicted list.
+template <typename T, int D, bool kLo>
 struct AssignShape {
-  static constexpr int kTiles = sizeof(T) == 2 ? 8 : 2;
-  static constexpr int kWaves = sizeof(T) == 2 ? 4 : 8;
+  static constexpr bool kBf = sizeof(T) == 2;
+  static constexpr int kTiles = kBf ? 4 : 2;
+  static constexpr int kWaves = kBf ? 4 : 8;
   static constexpr int kThreads = 64 * kWaves;
-  static constexpr int kWavesPerSimd = sizeof(T) == 2 ? 2 : 4;
-  static constexpr int kCenters = sizeof(T) == 2 ? 32 : 64;  // centres staged in LDS per step
-  static constexpr int kTokens = kWaves * 16 * kTiles;       // evicted tokens per block
-  static constexpr int kSubs = kTokens / kTokBlock;          // histogram blocks per block
+  static constexpr int kWavesPerSimd = 4;
+  static constexpr int kCenters = kBf ? (kLo && D == 128 ? 16 : 32) : 64;  // centres staged in LDS per step
+  static constexpr int kTokens = kWaves * 16 * kTiles;                    // evicted tokens per block
+  static constexpr int kSubs = kTokens / kTokBlock;                       // histogram blocks per block
   static_assert(kTokens % kTokBlock == 0, "assignment tiling");
 };
 
-// Assignment of AssignShape<T>::kTokens evicted tokens to the nearest centre:
+// Assignment of AssignShape::kTokens evicted tokens to the nearest centre:
 // C[centre][token] = mu.k on MFMA with mu = hi + lo (bf16 pair) or fp32,
 // dist = ||mu||^2 - 2 mu.k, argmin with ties to the lower centre. All token
 // tiles of a wave advance through each k-step together, so the MFMA chains
@@ -885,18 +878,19 @@ struct AssignShape {
 // bf16 key rows, so for finite keys lo is exactly zero there and the
 // distances are the same bit for bit with half the MFMAs.
 template <typename T, int D, bool kLo = true>
-__global__ __launch_bounds__(AssignShape<T>::kThreads, AssignShape<T>::kWavesPerSimd) void lloyd_assign(BuildArgs a, int iter) {
+__global__ __launch_bounds__((AssignShape<T, D, kLo>::kThreads), (AssignShape<T, D, kLo>::kWavesPerSimd)) void lloyd_assign(BuildArgs a, int iter) {
+  using Shape = AssignShape<T, D, kLo>;
   constexpr bool kBf = sizeof(T) == 2;
-  constexpr int kTT = AssignShape<T>::kTiles;
-  constexpr int kSubs = AssignShape<T>::kSubs;
-  constexpr int kNT = AssignShape<T>::kThreads;
-  constexpr int kCC = AssignShape<T>::kCenters;
+  constexpr int kTT = Shape::kTiles;
+  constexpr int kSubs = Shape::kSubs;
+  constexpr int kNT = Shape::kThreads;
+  constexpr int kCC = Shape::kCenters;
   constexpr int kRowB = kBf ? D * 2 + 16 : D * 4 + 16;   // padded LDS row bytes
   constexpr int kSteps = kBf ? D / 32 : D / 4;           // MFMA k-steps over the lane's share of a row
   const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
-  const int t0 = blk * AssignShape<T>::kTokens;
+  const int t0 = blk * Shape::kTokens;
   if (hm.r_eff == 0 || t0 >= hm.nE) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 15, grp = lane >> 4;
@@ -1300,12 +1294,15 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
   if (pl.max_reff > 0) {
     hipLaunchKernelGGL((center_prep<D>), grid(pl.max_reff), dim3(kThreads), 0, st, a); RESKV_CHECK();
     const size_t hist_lds = (size_t)pl.max_reff * sizeof(int);
-    const int ablk = (pl.max_E + AssignShape<T>::kTokens - 1) / AssignShape<T>::kTokens;
+    using S1 = AssignShape<T, D, false>;
+    using S2 = AssignShape<T, D, true>;
     for (int it = 0; it < pl.T; ++it) {
       if (sizeof(T) == 2 && it == 0)  // centres are the seeds' bf16 keys: lo = 0
-        hipLaunchKernelGGL((lloyd_assign<T, D, false>), grid(ablk), dim3(AssignShape<T>::kThreads), hist_lds, st, a, it);
+        hipLaunchKernelGGL((lloyd_assign<T, D, false>), grid((pl.max_E + S1::kTokens - 1) / S1::kTokens),
+                           dim3(S1::kThreads), hist_lds, st, a, it);
       else
-        hipLaunchKernelGGL((lloyd_assign<T, D>), grid(ablk), dim3(AssignShape<T>::kThreads), hist_lds, st, a, it);
+        hipLaunchKernelGGL((lloyd_assign<T, D>), grid((pl.max_E + S2::kTokens - 1) / S2::kTokens), dim3(S2::kThreads),
+                           hist_lds, st, a, it);
       RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), 0, st, a); RESKV_CHECK();
