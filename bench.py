@@ -120,7 +120,7 @@ def construction_mfma_from_profile(src_hash):
     ks = rec["kernels"]
     return {k: {"mfma_busy_pct": round(ks[k]["mfma_util_pct"], 1), "executed_tflops": round(ks[k]["mfma_tflops"]),
                 "algorithmic_tflops": round(ks[k]["alg_tflops"]), "algorithmic_util_pct": round(ks[k]["alg_util_pct"], 1)}
-            for k in ("lse_partial", "score_accum", "lloyd_assign") if k in ks}
+            for k in ("lse_partial", "score_accum", "lloyd_assign_r1", "lloyd_assign") if k in ks}
 
 
 # Validation proxy settings of App. B.3: grid of budget fractions, 8 of the 32

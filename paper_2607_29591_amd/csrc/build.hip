@@ -1094,29 +1094,39 @@ __global__ __launch_bounds__(kThreads) void lloyd_offsets(BuildArgs a) {
   }
 }
 
-// Stable placement: members of a group keep ascending evicted order.
+// Stable placement: members of a group keep ascending evicted order. A
+// token's rank inside its 256-token block is the number of earlier tokens
+// there in the same group: within a wave, the lanes sharing its group come
+// from one ballot per bit of the group index; across the block's waves, from
+// a per-wave count table in LDS (dynamic, kTokBlock / 64 rows of r' ints).
 __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
   const int blk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
   const int t0 = blk * kTokBlock;
   if (hm.r_eff == 0 || t0 >= hm.nE) return;
-  __shared__ int4 s_a4[kTokBlock / 4];
-  int* s_a = reinterpret_cast<int*>(s_a4);
-  const int i = t0 + threadIdx.x;
-  const int g = i < hm.nE ? a.assign[(size_t)bh * a.S + i] : -1;
-  const int src = i < hm.nE ? a.elist[(size_t)bh * a.S + i] : 0;
-  s_a[threadIdx.x] = g;
-  __syncthreads();
-  if (g < 0) return;
-  // stable rank: earlier tokens of the block in the same group, four per read
-  int rank = 0;
-  const int tid = threadIdx.x;
-  for (int q4 = 0; q4 < tid / 4; ++q4) {
-    const int4 v = s_a4[q4];
-    rank += (v.x == g) + (v.y == g) + (v.z == g) + (v.w == g);
+  constexpr int kNW = kTokBlock / 64;
+  extern __shared__ int s_cnt[];  // [kNW][r_eff]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i = t0 + tid;
+  const bool live = i < hm.nE;
+  const int g = live ? a.assign[(size_t)bh * a.S + i] : 0;
+  const int src = live ? a.elist[(size_t)bh * a.S + i] : 0;
+  for (int j = tid; j < kNW * hm.r_eff; j += kTokBlock) s_cnt[j] = 0;
+  uint64_t peers = __ballot(live);
+  const int nbits = hm.r_eff > 1 ? 32 - __clz(hm.r_eff - 1) : 0;
+  for (int bit = 0; bit < nbits; ++bit) {
+    const bool on = (g >> bit) & 1;
+    const uint64_t set = __ballot(live && on);
+    peers &= on ? set : ~set;
   }
-  for (int q = tid & ~3; q < tid; ++q) rank += (s_a[q] == g);
+  const int in_wave = __popcll(peers & ((1ull << lane) - 1));
+  __syncthreads();  // the table is cleared
+  if (live && in_wave == 0) s_cnt[wave * hm.r_eff + g] = __popcll(peers);
+  __syncthreads();
+  if (!live) return;
+  int rank = in_wave;
+  for (int w = 0; w < wave; ++w) rank += s_cnt[w * hm.r_eff + g];
   const int dst = a.hist[((size_t)bh * a.NBLK + blk) * a.Rcap + g] + rank;
   a.order[(size_t)bh * a.S + dst] = src;
 }
@@ -1305,7 +1315,8 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
                            hist_lds, st, a, it);
       RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
-      hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), 0, st, a); RESKV_CHECK();
+      hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), (kTokBlock / 64) * hist_lds, st, a);
+      RESKV_CHECK();
       // the update walks the heads in reverse of the assignment before and
       // after it, so each starts on the keys the other read last
       hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, it == pl.T - 1 ? 1 : 0, 1);
