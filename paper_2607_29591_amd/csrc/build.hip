@@ -1048,49 +1048,76 @@ __global__ __launch_bounds__((AssignShape<T, D, kLo>::kThreads), (AssignShape<T,
 }
 
 // Group sizes and counting-sort offsets: hist[blk][j] becomes the first
-// output position of block blk's members of group j.
-__global__ __launch_bounds__(kThreads) void lloyd_offsets(BuildArgs a) {
+// output position of block blk's members of group j. One 1024-thread block
+// per head; the groups take `cols` threads (r' rounded up to a power of two,
+// at most 1024) and the histogram rows are split among the 1024 / cols row
+// groups, so a head with few groups still has every thread walking rows.
+constexpr int kOffThreads = 1024;
+__global__ __launch_bounds__(kOffThreads) void lloyd_offsets(BuildArgs a) {
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
   if (hm.r_eff == 0) return;
-  __shared__ int s_tmp[kThreads / 64];
+  __shared__ int s_part[kOffThreads];   // per (row group, group) row sums
+  __shared__ int s_start[kOffThreads];  // first output position of each group
+  __shared__ int s_tmp[kOffThreads / 64];
   const int nblk = (hm.nE + kTokBlock - 1) / kTokBlock;
   int32_t* hist = a.hist + (size_t)bh * a.NBLK * a.Rcap;
+  int cols = 1;
+  while (cols < hm.r_eff && cols < kOffThreads) cols <<= 1;
+  const int ngrp = kOffThreads / cols;
+  const int c = threadIdx.x % cols, rg = threadIdx.x / cols;
+  const int per = (nblk + ngrp - 1) / ngrp;
+  const int q_lo = min(nblk, rg * per), q_hi = min(nblk, q_lo + per);
+  // the rows of this thread's range are read in batches of kBatch independent
+  // loads so the walk is not a chain of memory round trips
+  constexpr int kBatch = 16;
   int carry = 0;
-  for (int j0 = 0; j0 < hm.r_eff; j0 += kThreads) {
-    const int j = j0 + threadIdx.x;
-    // the column of block counts is read in batches of kBatch independent
-    // loads so the per-block walk is not a chain of memory round trips
-    constexpr int kBatch = 16;
+  for (int j0 = 0; j0 < hm.r_eff; j0 += cols) {
+    const int j = j0 + c;
+    const bool act = j < hm.r_eff;
     int tot = 0;
-    if (j < hm.r_eff) {
-      for (int q0 = 0; q0 < nblk; q0 += kBatch) {
-        int c[kBatch];
+    if (act) {
+      for (int q0 = q_lo; q0 < q_hi; q0 += kBatch) {
+        int v[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) c[u] = q0 + u < nblk ? hist[(size_t)(q0 + u) * a.Rcap + j] : 0;
+        for (int u = 0; u < kBatch; ++u) v[u] = q0 + u < q_hi ? hist[(size_t)(q0 + u) * a.Rcap + j] : 0;
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) tot += c[u];
+        for (int u = 0; u < kBatch; ++u) tot += v[u];
       }
     }
+    s_part[threadIdx.x] = tot;
+    __syncthreads();
+    int before = 0, col_tot = 0;  // rows of lower row groups come first
+    for (int g2 = 0; g2 < ngrp; ++g2) {
+      const int v = s_part[g2 * cols + c];
+      before += g2 < rg ? v : 0;
+      col_tot += v;
+    }
     int all;
-    const int start = carry + block_excl_scan<kThreads>(tot, s_tmp, all);
-    if (j < hm.r_eff) {
-      a.cstart[(size_t)bh * a.Rcap + j] = start;
-      a.ccount[(size_t)bh * a.Rcap + j] = tot;
-      int run = start;
-      for (int q0 = 0; q0 < nblk; q0 += kBatch) {
-        int c[kBatch];
+    const int start = carry + block_excl_scan<kOffThreads>(rg == 0 && act ? col_tot : 0, s_tmp, all);
+    if (rg == 0) s_start[c] = start;  // the row-group-0 threads come first in the scan
+    __syncthreads();
+    if (act) {
+      const int first = s_start[c];
+      if (rg == 0) {
+        a.cstart[(size_t)bh * a.Rcap + j] = first;
+        a.ccount[(size_t)bh * a.Rcap + j] = col_tot;
+      }
+      int run = first + before;
+      for (int q0 = q_lo; q0 < q_hi; q0 += kBatch) {
+        int v[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) c[u] = q0 + u < nblk ? hist[(size_t)(q0 + u) * a.Rcap + j] : 0;
+        for (int u = 0; u < kBatch; ++u) v[u] = q0 + u < q_hi ? hist[(size_t)(q0 + u) * a.Rcap + j] : 0;
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-          if (q0 + u < nblk) hist[(size_t)(q0 + u) * a.Rcap + j] = run;
-          run += c[u];
+          if (q0 + u < q_hi) hist[(size_t)(q0 + u) * a.Rcap + j] = run;
+          run += v[u];
         }
       }
     }
     carry += all;
+    __syncthreads();  // s_part and s_start are rewritten by the next pass
   }
 }
 
@@ -1314,7 +1341,7 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
         hipLaunchKernelGGL((lloyd_assign<T, D>), grid((pl.max_E + S2::kTokens - 1) / S2::kTokens), dim3(S2::kThreads),
                            hist_lds, st, a, it);
       RESKV_CHECK();
-      hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kThreads), 0, st, a); RESKV_CHECK();
+      hipLaunchKernelGGL(lloyd_offsets, bhg, dim3(kOffThreads), 0, st, a); RESKV_CHECK();
       hipLaunchKernelGGL(lloyd_scatter, grid(pl.NBLK), dim3(kTokBlock), (kTokBlock / 64) * hist_lds, st, a);
       RESKV_CHECK();
       // the update walks the heads in reverse of the assignment before and
