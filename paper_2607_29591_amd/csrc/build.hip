@@ -1161,8 +1161,14 @@ __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
 // New centre of group j = fp64 mean of its members' keys, summed in a fixed
 // order; an empty group keeps its centre. The last round also writes the
 // entry: mean key and mean value in the cache dtype, and log c_j.
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void lloyd_update(BuildArgs a, int last, int rev) {
+// kPacked (bf16): rows stay packed until they are added, which keeps the
+// kernel at 64 registers and eight blocks per CU, the better shape when the
+// groups are of similar size (rounds after the first). The first round's
+// groups, grown around single seed keys, are very uneven; there the wider
+// variant (rows converted as they land, about 100 registers, four blocks per
+// CU) keeps more of a long group's rows in flight and finishes sooner.
+template <typename T, int D, bool kPacked>
+__global__ __launch_bounds__(kThreads, (kPacked && sizeof(T) == 2 ? 8 : 4)) void lloyd_update(BuildArgs a, int last, int rev) {
   const int j = blockIdx.x;
   int b, kvh, bh;
   block_head(a, rev, b, kvh, bh);
@@ -1187,13 +1193,28 @@ __global__ __launch_bounds__(kThreads) void lloyd_update(BuildArgs a, int last, 
     // members g, g + NG, g + 2NG, ... in order; four 16-byte row loads in flight
     int q = g;
     for (; q + 3 * NG < cnt; q += 4 * NG) {
-      float x[4][8];
+      if constexpr (kPacked && sizeof(T) == 2) {  // rows stay packed until added: 4 registers each
+        uint4 w[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) load8_f32(X + (size_t)mem[q + u * NG] * D + 8 * c, x[u]);
+        for (int u = 0; u < 4; ++u) w[u] = *reinterpret_cast<const uint4*>(X + (size_t)mem[q + u * NG] * D + 8 * c);
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t pw[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] += (double)x[u][e];
+          for (int e = 0; e < 4; ++e) {
+            acc[2 * e] += (double)bf16_lo(pw[e]);
+            acc[2 * e + 1] += (double)bf16_hi(pw[e]);
+          }
+        }
+      } else {
+        float x[4][8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) load8_f32(X + (size_t)mem[q + u * NG] * D + 8 * c, x[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] += (double)x[u][e];
+      }
     }
     for (; q < cnt; q += NG) {
       float x[8];
@@ -1346,7 +1367,11 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
       RESKV_CHECK();
       // the update walks the heads in reverse of the assignment before and
       // after it, so each starts on the keys the other read last
-      hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, it == pl.T - 1 ? 1 : 0, 1);
+      const int last = it == pl.T - 1 ? 1 : 0;
+      if (it == 0)
+        hipLaunchKernelGGL((lloyd_update<T, D, false>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
+      else
+        hipLaunchKernelGGL((lloyd_update<T, D, true>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
       RESKV_CHECK();
     }
   }
