@@ -89,6 +89,19 @@ def test_build_workload0_and_decode():
         assert rel_err_rows(out, ref).max() <= TOL["f32"]
 
 
+@pytest.mark.parametrize("s,budget,res,iters", [(4000, 1600, (1500, 1030), 2), (8192, 4200, (4096, 0), 1)])
+def test_build_many_groups(s, budget, res, iters):
+    """More than 1024 residual groups per head, up to the 4096 entries a
+    construction accepts: the group offsets take several column passes and
+    a group index spans 11 to 12 bits in the stable placement; both update
+    variants run in the two-round case."""
+    wl, x = small(31, dtype="bf16", d=128, s=s, hq=8, hkv=2, budget=budget, res=res, window=16, n_heavy=8)
+    assert wl.res_cap == max(res)
+    got = run_build(wl, x, iters=iters)
+    for h in range(wl.hkv):
+        check_head(wl, x, got, 0, h, iters=iters)
+
+
 def test_build_is_deterministic():
     wl, x = small(4, dtype="bf16", d=128, s=2000, budget=256, res=(64, 32), window=16)
     a = run_build(wl, x)
