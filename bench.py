@@ -53,6 +53,8 @@ def parse():
                          "the byte counters; proxy: only construction with the validation proxy, every layer")
     ap.add_argument("--proxy-layers", type=int, default=2,
                     help="layers built with the validation proxy after the timed job (0: skip)")
+    ap.add_argument("--slot-cap", type=int, default=None,
+                    help="slots allocated per (sequence, KV head) cache (default: budget + decode steps)")
     ap.add_argument("--adakv-layers", type=int, default=2,
                     help="layers built with AdaKV's cross-head allocation after the timed job (0: skip)")
     return ap.parse_args()
@@ -316,7 +318,7 @@ def main():
     L, B, Hq, Hkv, d = wl.layers, wl.batch, wl.hq, wl.hkv, wl.d
     elem = 2 if wl.dtype == "bf16" else 4
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    C, Rcap, S = wl.slot_cap, wl.res_cap, wl.max_ctx
+    C, Rcap, S = max(wl.slot_cap, args.slot_cap or 0), wl.res_cap, wl.max_ctx
     shape = rk.make_shape(B, Hq, Hkv, d, wl.dtype, C, Rcap)
     params = rk.BuildParams(S, wl.window, wl.window, wl.lloyd_iters)
 
