@@ -48,8 +48,8 @@ namespace reskv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kKeyGroups = 4;     // 256-key groups per scoring block, one after the other
-constexpr int kKeyChunk = 256 * kKeyGroups;  // keys per scoring block
+constexpr int kKeyGroups = 4;     // 256-key groups per score-pass block, one after the other
+constexpr int kKeyChunk = 256 * kKeyGroups;  // keys per score-pass block
 constexpr int kRowChunk = 128;     // window rows staged in LDS per scoring step
 // s_waitcnt immediate: vector-memory count 0, export and LDS/scalar counts
 // left at their maximum (no wait on them)
@@ -71,7 +71,7 @@ struct BuildArgs {
   float* dbg_scores;
   int32_t* dbg_assign;
   const HeadMeta* meta;
-  float2* lse_part;    // [BH][NCH][R] (max, sum) in base 2
+  float2* lse_part;    // [BH][NCH][R] (max, sum) in base 2, one per lse block
   float* lse2;         // [BH][R]
   float* raw;          // [BH][S]
   float* score;        // [BH][S]
@@ -86,7 +86,7 @@ struct BuildArgs {
   int32_t* cstart;     // [BH][Rcap]
   int32_t* ccount;     // [BH][Rcap]
   int32_t* order;      // [BH][S]   evicted positions grouped by centre
-  int B, Hq, Hkv, G, C, Rcap, S, w, R, NCH, NBLK, T;
+  int B, Hq, Hkv, G, C, Rcap, S, w, R, LG, NCH, NBLK, T;
   int wr;              // leading window rows per query head that score (R = G * wr)
   int pool_half;       // pooling taps on each side of a position
   float scale2;        // log2(e) / sqrt(d)
@@ -132,10 +132,10 @@ __device__ __forceinline__ void stage_window_rows(unsigned char* s_q, const Buil
 
 // ---------------------------------------------------------------- scoring
 
-// Scoring blocks stream kKeyGroups groups of 256 keys; in each group a wave
-// owns 64 keys and runs over every window row, with the next group's key
-// fragments already requested. The window rows are staged in LDS once per
-// block (128 at a time).
+// Scoring blocks stream groups of 256 keys one after the other (the lse pass
+// 4, 8 or 16 groups per block as the plan chooses, the score pass 4); in each
+// group a wave owns 64 keys and runs over every window row. The window rows
+// are staged in LDS once per block (128 at a time).
 
 // Key fragments of the 64 keys from kw (clamped to the sequence).
 template <typename T, int D>
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 3 : 2)) void lse_partia
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
-  const int k0 = ch * kKeyChunk;
+  const int k0 = ch * 256 * a.LG;
   if (hm.all_main || k0 >= hm.s) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 3 : 2)) void lse_partia
     for (int rt = 0; rt < nrt; ++rt) s_ml[wave][16 * rt + col] = make_float2(kNegInf, 0.f);
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // the first group's keys have landed
 #pragma unroll 1
-    for (int gi = 0; gi < kKeyGroups; ++gi) {
+    for (int gi = 0; gi < a.LG; ++gi) {
       const int kw = k0 + 256 * gi + 64 * wave;  // this wave's keys in group gi
       if (gi > 0) load_score_keys<T, D>(kf, K, kw, hm.s, col, grp);
       __builtin_amdgcn_sched_barrier(0);  // the group's key loads go out before its work
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
   const HeadMeta hm = a.meta[bh];
   const int t = blockIdx.x * kThreads + threadIdx.x;
   if (hm.all_main || t >= a.R) return;
-  const int nch = (hm.s + kKeyChunk - 1) / kKeyChunk;
+  const int nch = (hm.s + 256 * a.LG - 1) / (256 * a.LG);
   const float2* pp = a.lse_part + (size_t)bh * a.NCH * a.R + t;
   float M = kNegInf;
   for (int c = 0; c < nch; ++c) M = fmaxf(M, pp[(size_t)c * a.R].x);
@@ -1308,7 +1308,7 @@ BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const voi
   a.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
   a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
   a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
-  a.wr = pl.wr; a.pool_half = pl.pool_half; a.R = pl.R; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
+  a.wr = pl.wr; a.pool_half = pl.pool_half; a.R = pl.R; a.LG = pl.LG; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
   a.scale2 = kLog2e / sqrtf((float)pl.D);
   return a;
 }
@@ -1323,7 +1323,7 @@ hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStrea
   hipLaunchKernelGGL((lse_partial<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
   hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
   // the second pass over the keys walks the heads in reverse (cache reuse)
-  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a, 1); RESKV_CHECK();
+  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1); RESKV_CHECK();
   return hipSuccess;
 }
 
@@ -1415,10 +1415,20 @@ bool fold_build_plan(const std::vector<HeadMeta>& hm, BuildPlan* plan) {
 bool layout_build_plan(BuildPlan* plan) {
   BuildPlan& pl = *plan;
   if (pl.R > 1024 || pl.Rcap > 4096) return false;
-  pl.NCH = (pl.max_s + kKeyChunk - 1) / kKeyChunk;
+  const size_t BH = (size_t)pl.B * pl.Hkv;
+  // the lse pass takes 16, 8 or 4 key groups per block: the longest chunks
+  // that still give at least 1024 blocks (fewer blocks write fewer partial
+  // records and stage the window rows fewer times)
+  pl.LG = kKeyGroups;
+  for (int lg = 16; lg > kKeyGroups; lg /= 2)
+    if (BH * (size_t)((pl.max_s + 256 * lg - 1) / (256 * lg)) >= 1024) {
+      pl.LG = lg;
+      break;
+    }
+  pl.NCH = (pl.max_s + 256 * pl.LG - 1) / (256 * pl.LG);
+  pl.NSC = (pl.max_s + kKeyChunk - 1) / kKeyChunk;
   pl.NBLK = (pl.max_E + kTokBlock - 1) / kTokBlock;
   if (pl.NBLK < 1) pl.NBLK = 1;
-  const size_t BH = (size_t)pl.B * pl.Hkv;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align_up(off + bytes, 256); return o; };
   pl.off_meta = take(BH * sizeof(HeadMeta));

@@ -63,7 +63,9 @@ struct BuildPlan {
   int wr;     // leading window rows per query head that score
   int pool_half;  // score pooling taps on each side
   int R;      // scoring rows per kv head, G * wr
-  int NCH;    // scoring key chunks of the longest sequence
+  int LG;     // 256-key groups per lse block
+  int NCH;    // lse key chunks (256 * LG keys) of the longest sequence
+  int NSC;    // score-pass key chunks of the longest sequence
   int NBLK;   // 256-token blocks of the largest evicted set
   int max_s, max_main, max_reff, max_E;
   size_t off_meta, off_lsep, off_lse, off_raw, off_score, off_elist, off_seeds, off_cent, off_chi,
