@@ -21,8 +21,8 @@
 //                  main_idx (top-k, then the protected window), the evicted
 //                  list E and the Lloyd seeds, all ascending
 //   gather_init    copies the main rows into slots [r, r + m), clears the
-//                  residual slots, seeds the Lloyd centres with K[seed]
-//   center_prep    splits each centre into bf16 hi + lo and its squared norm
+//                  residual slots, seeds the Lloyd centres with K[seed] (fp32,
+//                  bf16 hi + lo and the squared norm)
 //   T x { lloyd_assign   MFMA distances ||mu||^2 - 2 k.mu with mu = hi + lo,
 //                        argmin with ties to the lower centre, and per-block
 //                        group histograms
@@ -769,13 +769,33 @@ __global__ __launch_bounds__(kThreads) void gather_init(BuildArgs a) {
     reinterpret_cast<uint4*>(kc + (size_t)dst * D)[ck] = kv;
     reinterpret_cast<uint4*>(vc + (size_t)dst * D)[ck] = vv;
   }
-  // every log-count starts empty; seeds become the first centres
+  // every log-count starts empty
   for (int j = blockIdx.x * kThreads + threadIdx.x; j < a.Rcap; j += gridDim.x * kThreads)
     a.logc[(size_t)bh * a.Rcap + j] = kNegInf;
+  // seeds become the first centres, one wave per centre: the fp32 copy, the
+  // bf16 hi + lo split and the squared norm, summed as the update sums it (an
+  // fp64 butterfly over each 64 elements, then those partials in order)
+  static_assert(D % 64 == 0, "whole waves per centre row");
   const int32_t* seeds = a.seeds + (size_t)bh * a.Rcap;
-  for (int x = blockIdx.x * kThreads + threadIdx.x; x < hm.r_eff * D; x += gridDim.x * kThreads) {
-    const int j = x / D, d = x % D;
-    a.cent[((size_t)bh * a.Rcap + j) * D + d] = to_f32(K[(size_t)seeds[j] * D + d]);
+  const int lane = threadIdx.x & 63;
+  const int nw = gridDim.x * (kThreads / 64);
+  for (int j = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6); j < hm.r_eff; j += nw) {
+    const T* kr = K + (size_t)seeds[j] * D;
+    const size_t ci = (size_t)bh * a.Rcap + j;
+    double t = 0.0;
+#pragma unroll
+    for (int e0 = 0; e0 < D; e0 += 64) {
+      const float x = to_f32(kr[e0 + lane]);
+      const uint16_t h = f32_to_bf16_rne(x);
+      a.cent[ci * D + e0 + lane] = x;
+      a.cent_hi[ci * D + e0 + lane] = h;
+      a.cent_lo[ci * D + e0 + lane] = f32_to_bf16_rne(x - to_f32(h));
+      double sq = (double)x * x;
+#pragma unroll
+      for (int msk = 1; msk < 64; msk <<= 1) sq += __shfl_xor(sq, msk, 64);
+      t += sq;
+    }
+    if (lane == 0) a.cnorm[ci] = (float)t;
   }
 }
 
@@ -805,16 +825,6 @@ __device__ void prep_center(const BuildArgs& a, size_t ci, const float* mu, doub
   __syncthreads();
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void center_prep(BuildArgs a) {
-  const int j = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int bh = b * a.Hkv + kvh;
-  const HeadMeta hm = a.meta[bh];
-  if (j >= hm.r_eff) return;
-  __shared__ double s_red[D];
-  const size_t ci = (size_t)bh * a.Rcap + j;
-  prep_center<D>(a, ci, a.cent + ci * D, s_red);
-}
 
 // ------------------------------------------------------------------ Lloyd
 
@@ -1350,7 +1360,6 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
   hipLaunchKernelGGL((gather_init<T, D>), grid(gblocks < 64 ? gblocks : 64), dim3(kThreads), 0, st, a);
   RESKV_CHECK();
   if (pl.max_reff > 0) {
-    hipLaunchKernelGGL((center_prep<D>), grid(pl.max_reff), dim3(kThreads), 0, st, a); RESKV_CHECK();
     const size_t hist_lds = (size_t)pl.max_reff * sizeof(int);
     using S1 = AssignShape<T, D, false>;
     using S2 = AssignShape<T, D, true>;
