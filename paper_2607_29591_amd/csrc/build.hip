@@ -1177,8 +1177,10 @@ __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
 // groups, grown around single seed keys, are very uneven; there the wider
 // variant (rows converted as they land, about 100 registers, four blocks per
 // CU) keeps more of a long group's rows in flight and finishes sooner.
-template <typename T, int D, bool kPacked>
-__global__ __launch_bounds__(kThreads, (kPacked && sizeof(T) == 2 ? 8 : 4)) void lloyd_update(BuildArgs a, int last, int rev) {
+// kKV (last round, bf16): each member's key and value rows are read in the
+// same loop, twice the rows in flight of two passes one after the other.
+template <typename T, int D, bool kPacked, bool kKV = false>
+__global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && sizeof(T) == 2 ? 8 : 4)) void lloyd_update(BuildArgs a, int last, int rev) {
   const int j = blockIdx.x;
   int b, kvh, bh;
   block_head(a, rev, b, kvh, bh);
@@ -1195,6 +1197,62 @@ __global__ __launch_bounds__(kThreads, (kPacked && sizeof(T) == 2 ? 8 : 4)) void
   const int32_t* mem = a.order + (size_t)bh * a.S + a.cstart[ci];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
   const T* V = static_cast<const T*>(a.v) + (size_t)bh * a.S * D;
+  if constexpr (kKV && sizeof(T) == 2) {
+    // last round: the key and value rows of each member are read together
+    // (twice the rows in flight), each summed in member order as below
+    double ak[8], av[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ak[e] = av[e] = 0.0;
+    auto add8 = [](double (&acc)[8], const uint4& w) {
+      const uint32_t pw[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] += (double)bf16_lo(pw[e]);
+        acc[2 * e + 1] += (double)bf16_hi(pw[e]);
+      }
+    };
+    int q = g;
+    for (; q + 3 * NG < cnt; q += 4 * NG) {
+      uint4 wk[4], wv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const size_t off = (size_t)mem[q + u * NG] * D + 8 * c;
+        wk[u] = *reinterpret_cast<const uint4*>(K + off);
+        wv[u] = *reinterpret_cast<const uint4*>(V + off);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add8(ak, wk[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add8(av, wv[u]);
+    }
+    for (; q < cnt; q += NG) {
+      const size_t off = (size_t)mem[q] * D + 8 * c;
+      const uint4 wk = *reinterpret_cast<const uint4*>(K + off);
+      const uint4 wv = *reinterpret_cast<const uint4*>(V + off);
+      add8(ak, wk);
+      add8(av, wv);
+    }
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s_sum[g][8 * c + e] = pass == 0 ? ak[e] : av[e];
+      __syncthreads();
+      if (tid < D) {
+        double t = 0.0;
+        for (int gg = 0; gg < NG; ++gg) t += s_sum[gg][tid];
+        const float mean = cnt > 0 ? (float)(t / cnt) : 0.f;
+        if (pass == 0) {
+          const float mu = cnt > 0 ? mean : a.cent[ci * D + tid];  // empty group keeps its centre
+          a.cent[ci * D + tid] = mu;
+          store_elem(static_cast<T*>(a.kc) + ((size_t)bh * a.C + j) * D + tid, mu);
+        } else {
+          store_elem(static_cast<T*>(a.vc) + ((size_t)bh * a.C + j) * D + tid, mean);
+        }
+      }
+      __syncthreads();
+    }
+    if (tid == 0) a.logc[ci] = cnt > 0 ? logf((float)cnt) : kNegInf;
+    return;
+  }
   for (int pass = 0; pass < (last ? 2 : 1); ++pass) {
     const T* X = pass == 0 ? K : V;
     double acc[8];
@@ -1379,6 +1437,8 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
       const int last = it == pl.T - 1 ? 1 : 0;
       if (it == 0)
         hipLaunchKernelGGL((lloyd_update<T, D, false>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
+      else if (last)
+        hipLaunchKernelGGL((lloyd_update<T, D, true, true>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
       else
         hipLaunchKernelGGL((lloyd_update<T, D, true>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
       RESKV_CHECK();
