@@ -1000,19 +1000,30 @@ __global__ __launch_bounds__((AssignShape<T, D, kLo>::kThreads), (AssignShape<T,
 #pragma unroll
       for (int i = 0; i < 4; ++i) nrm[i] = s_norm[16 * ct + 4 * grp + i];
       const int jb = j0 + 16 * ct + 4 * grp;
+      // the lane's 4 centres in ascending order, then against earlier
+      // tiles; each step runs for all token tiles before the next, so the
+      // tiles' independent compare-select chains interleave
+      float bv[kTT];
+      int bi[kTT];
 #pragma unroll
       for (int tt = 0; tt < kTT; ++tt) {
-        // the lane's 4 centres in ascending order, then against earlier tiles
-        float bv = fmaf(-2.f, acc[tt][0], nrm[0]);
-        int bi = jb;
+        bv[tt] = fmaf(-2.f, acc[tt][0], nrm[0]);
+        bi[tt] = jb;
+      }
 #pragma unroll
-        for (int i = 1; i < 4; ++i) {
+      for (int i = 1; i < 4; ++i)
+#pragma unroll
+        for (int tt = 0; tt < kTT; ++tt) {
           const float dist = fmaf(-2.f, acc[tt][i], nrm[i]);
-          bi = dist < bv ? jb + i : bi;
-          bv = dist < bv ? dist : bv;
+          const bool lt = dist < bv[tt];
+          bi[tt] = lt ? jb + i : bi[tt];
+          bv[tt] = lt ? dist : bv[tt];
         }
-        bidx[tt] = bv < best[tt] ? bi : bidx[tt];
-        best[tt] = bv < best[tt] ? bv : best[tt];
+#pragma unroll
+      for (int tt = 0; tt < kTT; ++tt) {
+        const bool lt = bv[tt] < best[tt];
+        bidx[tt] = lt ? bi[tt] : bidx[tt];
+        best[tt] = lt ? bv[tt] : best[tt];
       }
     }
     if (j0 + kCC < hm.r_eff) {  // block-uniform
