@@ -514,8 +514,8 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": ("reskv_decode_attn (one launch per layer-step: decode_head, one block per "
                                 "(sequence, KV head), append fused)" if B * Hkv >= 256 and (elem == 2 or d == 64) else
-                                "reskv_decode_attn (per layer-step: append, decode_split over 256-slot blocks, "
-                                "decode_combine with the gate)"),
+                                "reskv_decode_attn (per layer-step: decode_split over 256-slot blocks with the "
+                                "append fused, decode_combine with the gate)"),
                      "bytes_per_call": avg_bytes, "us_per_call": avg_ms * 1e3,
                      "calls_timed": calls * args.steps},
         "setup_s": t_setup,

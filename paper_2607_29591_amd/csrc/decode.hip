@@ -53,7 +53,7 @@ struct DecodeArgs {
   const float* logc;
   const int32_t* res_len;
   int32_t* main_len;
-  const void* k_new;  // fused append (decode_head only), or NULL
+  const void* k_new;  // fused append of this step's token, or NULL
   const void* v_new;
   float* part_acc;  // [B*Hkv][P][GP][D]
   float* part_ml;   // [B*Hkv][P][GP][2]  (m in base 2, l)
@@ -315,6 +315,14 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
   const int bh = b * a.Hkv + kvh;
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  // fused append: this step's token is main slot r + n, read from k_new /
+  // v_new and stored into the cache by the wave whose unit holds it;
+  // decode_combine advances main_len once every block has read it
+  const bool app = a.k_new != nullptr && r + n < a.C;
+  const int app_row = app ? r + n : -1;
+  const T* kn = app ? static_cast<const T*>(a.k_new) + (size_t)bh * D : nullptr;
+  const T* vn = app ? static_cast<const T*>(a.v_new) + (size_t)bh * D : nullptr;
+  if (app) n += 1;
   // block p < PR covers residual slots [256p, 256p + 256) of [0, r); block
   // p >= PR covers main slots [r + 256(p-PR), ...) of [r, r + n)
   const bool is_res = p < a.PR;
@@ -343,12 +351,21 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
     else q.zero();
     UnitRegs<T, D> u;
     const int nvalid = min(kUnit, end - s0);
-    load_unit_k<T, D>(u, kc, s0, end - 1, hd, g, -1, nullptr);
+    load_unit_k<T, D>(u, kc, s0, end - 1, hd, g, app_row, kn);
     if (is_res) load_unit_lc<T, D>(u, logc, s0, nvalid, g);
     float sc[kTiles][4];
     unit_logits<T, D>(u, q, a.qk_scale, sc);
-    load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, -1, nullptr);
+    load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, app_row, vn);
     softmax_pv<T, D>(st, u, sc, 0, nvalid, is_res, a.beta_log2, g);
+    if (app_row >= s0 && app_row < s0 + nvalid) {  // wave-uniform: the new rows into the cache
+      constexpr int kPieces = D * (int)sizeof(T) / 16;
+      if (lane < 2 * kPieces) {
+        const bool isv = lane >= kPieces;
+        const int c = isv ? lane - kPieces : lane;
+        T* dst = static_cast<T*>(const_cast<void*>(isv ? a.vc : a.kc)) + ((size_t)bh * a.C + app_row) * D;
+        reinterpret_cast<uint4*>(dst)[c] = reinterpret_cast<const uint4*>(isv ? vn : kn)[c];
+      }
+    }
   }
   store_wave_state<D, GP>(st, s_acc[wave], s_m[wave], s_l[wave], hd, g);
   __syncthreads();
@@ -386,6 +403,8 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
   const int bh = b * a.Hkv + kvh;
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  const bool app = a.k_new != nullptr && r + n < a.C;  // as in decode_split
+  if (app) n += 1;
   const int nRC = (r + kChunk - 1) / kChunk, nMC = (n + kChunk - 1) / kChunk;
   const float* ml = a.part_ml + (size_t)bh * a.P * GP * 2;
   const float* pacc = a.part_acc + (size_t)bh * a.P * GP * D;
@@ -452,6 +471,9 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
     if (q < nMC) o0 = fmaf(w[a.PR + q], pacc[((a.PR + q) * GP + hh) * D + d], o0);
     a.out[((size_t)b * a.Hq + kvh * a.G + hh) * D + d] = o0 + o1;
   }
+  // the appended token is in the cache: advance main_len (one block per
+  // head, and every thread of it read the length above)
+  if (app && tid == 0) a.main_len[bh] = n;
 }
 
 
@@ -806,12 +828,8 @@ hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const De
                          float* out, float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate,
                          void* workspace, hipStream_t stream) {
   char* ws = static_cast<char*>(workspace);
-  if (k_new && !pl.whole_head) {  // split-K path: append as its own launch first
-    const hipError_t e = launch_append(s, k_new, v_new, kc, vc, res_len, main_len, stream);
-    if (e != hipSuccess) return e;
-  }
   DecodeArgs da{};
-  if (pl.whole_head) { da.k_new = k_new; da.v_new = v_new; }
+  da.k_new = k_new; da.v_new = v_new;  // appended inside the decode kernels
   da.q = q; da.kc = kc; da.vc = vc; da.logc = logc;
   da.res_len = res_len; da.main_len = main_len;
   da.part_acc = reinterpret_cast<float*>(ws + pl.acc_off);

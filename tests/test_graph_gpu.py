@@ -36,7 +36,8 @@ def clone(state):
 @pytest.mark.parametrize("B,Hkv,G", [(64, 4, 4), (2, 2, 7)])
 def test_decode_step_graph_replays_match_eager(B, Hkv, G):
     """(64, 4, 4): one block per (sequence, KV head) with the append fused;
-    (2, 2, 7): the split-K path (append launch, partial blocks, combine)."""
+    (2, 2, 7): the split-K path (partial blocks with the append fused, then
+    the combine, which advances the main lengths)."""
     d, C, Rcap = 128, 320, 64
     shape = rk.make_shape(B, G * Hkv, Hkv, d, "bf16", C, Rcap)
     rng, base = decode_state(B, Hkv, G, d, C, Rcap, 5 + G)
