@@ -11,13 +11,22 @@ One timed step = the whole job on one batch: reskv_build_cache for all 32
 layers (from prefill K/V resident in HBM), then 256 decode steps, each of
 which runs reskv_decode_attn for all 32 layers with that step's token
 appended inside the call.
-value = decode tokens (batch x layers x decode steps) / step time.
+value = decode tokens (batch x layers x decode steps) / step time, i.e. the
+decode rate of the whole job with its construction included (the metric
+label says so); decode_tokens_per_s beside it is the decode phase alone.
 
 Also reported: decode-only throughput and HBM GB/s, construction GB/s,
 construction with the validation proxy choosing r and with AdaKV's
-cross-head allocation (ms per layer, untimed in the job), the roofline of the decode kernels (algorithmic bytes per call / average call
-time from HIP events on the launch stream), and the fp64 oracle's throughput
-on the host cores over a bounded sample of the same job.
+cross-head allocation (ms per layer, untimed in the job), the roofline of
+the decode kernels (algorithmic bytes per call / average call time from HIP
+events on the launch stream), and the fp64 oracle's throughput on the host
+cores over a bounded sample of the same job. After the main job its
+buffers are freed and two more workloads are measured (per_config): the
+long-context construction workload (B 4, 128K context, 8 layers, budget
+1024 = 768 + 256, window 64: construction GB/s and TFLOP/s against the
+MFMA roofline, decode GB/s) and the ragged GQA-7 workload (B 64, 28 q / 4
+KV heads, contexts 4K-64K, budgets 256-1024, 28 layers: decode GB/s
+against the HBM roofline, construction time).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -57,6 +66,10 @@ def parse():
                     help="slots allocated per (sequence, KV head) cache (default: budget + decode steps)")
     ap.add_argument("--adakv-layers", type=int, default=2,
                     help="layers built with AdaKV's cross-head allocation after the timed job (0: skip)")
+    ap.add_argument("--per-config", default="3,4",
+                    help="other workloads measured after the main job, comma-separated indices "
+                         "(3 = long-context construction, 4 = ragged GQA-7; empty: none)")
+    ap.add_argument("--per-config-reps", type=int, default=2, help="timed constructions per layer of those workloads")
     return ap.parse_args()
 
 
@@ -180,7 +193,7 @@ def adakv_runs(rk, torch, wl, shape, layers, caches, res_layers, n_layers, dev):
     import numpy as np
     S = wl.max_ctx
     params = rk.BuildParams(S, wl.window, wl.window, wl.lloyd_iters, 0)
-    nws = max(rk.reskv_build_adakv_workspace_size(shape, params, ADAKV_SAFEGUARD, layers[l]["seq_len"],
+    nws = max(rk.reskv_build_adakv_workspace_size(shape, params, ADAKV_SAFEGUARD, wl.steps, layers[l]["seq_len"],
                                                   layers[l]["budget"], res_layers[l].reshape(-1))
               for l in range(n_layers))
     ws = torch.empty(nws, dtype=torch.uint8, device=dev)
@@ -188,7 +201,7 @@ def adakv_runs(rk, torch, wl, shape, layers, caches, res_layers, n_layers, dev):
 
     def call(l):
         x, c = layers[l], caches[l]
-        rk.reskv_build_cache_adakv(shape, params, ADAKV_SAFEGUARD, x["K"], x["V"], x["seq_len"], x["q_obs"],
+        rk.reskv_build_cache_adakv(shape, params, ADAKV_SAFEGUARD, wl.steps, x["K"], x["V"], x["seq_len"], x["q_obs"],
                                    x["budget"], res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"],
                                    c["main_idx"], c["res_len"], c["main_len"], ws)
 
@@ -208,11 +221,14 @@ def adakv_runs(rk, torch, wl, shape, layers, caches, res_layers, n_layers, dev):
 
 def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
     """Time the fp64 oracle on a bounded sample of the job on the host and
-    extrapolate to the whole job: one (sequence, KV head) of construction
-    (scores + selection, then Lloyd, whose cost grows with r) and one decode
-    layer-step for every query head of every sequence."""
+    extrapolate to the whole job: construction of one (sequence, KV head)
+    for each residual count that layer 0 of sequence 0 uses (scores +
+    selection, then Lloyd, whose cost grows with r), and a few decode
+    layer-steps for every query head of every sequence. Heads of other
+    layers are priced at the measured head with their r (linear in r between
+    measured counts); the sample stops taking heads once `budget_s` of
+    construction has been spent."""
     import numpy as np
-    import torch
     from oracle import reskv_oracle as orc
     try:
         from threadpoolctl import threadpool_info
@@ -221,63 +237,235 @@ def cpu_baseline(wl, x0, q0, tau0, res_layers, budget_s):
         blas_threads = None
     cores = len(os.sched_getaffinity(0))
     B, Hkv, G, d = wl.batch, wl.hkv, wl.group, wl.d
-    # sample head: first (b=0, kv head) whose r is positive, smallest such r
-    r_row = res_layers[0][0]
-    cand = [h for h in range(Hkv) if r_row[h] > 0] or [0]
-    h = min(cand, key=lambda j: r_row[j])
-    r = int(r_row[h])
     s = wl.ctx[0]
-    m = wl.budget[0] - r
-    K = x0["K"][0, h, :s].float().cpu().numpy().astype(np.float64)
-    V = x0["V"][0, h, :s].float().cpu().numpy().astype(np.float64)
-    Qw = x0["q_obs"][0, h * G:(h + 1) * G].float().cpu().numpy().astype(np.float64)
-    t0 = time.perf_counter()
-    n = orc.scored_length(s, m, wl.window)
-    raw = orc.window_raw_scores(K, Qw)
-    sc = orc.pool5(raw[:n])
-    main, ev, seeds = orc.select_main(sc, s, m, wl.window, r)
-    t_score = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    if r > 0:
-        a, mu, _ = orc.lloyd(K[ev], K[seeds], wl.lloyd_iters)
-        orc.residual_entries(K[ev], V[ev], a, mu, r, d)
-    t_lloyd = time.perf_counter() - t0
-    per_center = t_lloyd / max(r, 1)
-    # decode: one layer-step, every (sequence, query head), on a cache of the
-    # decode shape (main rows drawn from the prefill, residual rows from means)
+    r_row = res_layers[0][0]
+    picks = {}
+    for h in sorted(range(Hkv), key=lambda j: r_row[j]):
+        picks.setdefault(int(r_row[h]), h)
+    t_build = {}
+    spent = 0.0
+    for r, h in sorted(picks.items()):
+        if spent > budget_s:
+            break
+        m = wl.budget[0] - r
+        K = x0["K"][0, h, :s].float().cpu().numpy().astype(np.float64)
+        V = x0["V"][0, h, :s].float().cpu().numpy().astype(np.float64)
+        Qw = x0["q_obs"][0, h * G:(h + 1) * G].float().cpu().numpy().astype(np.float64)
+        t0 = time.perf_counter()
+        n = orc.scored_length(s, m, wl.window)
+        raw = orc.window_raw_scores(K, Qw)
+        sc = orc.pool5(raw[:n])
+        main, ev, seeds = orc.select_main(sc, s, m, wl.window, r)
+        if r > 0:
+            a, mu, _ = orc.lloyd(K[ev], K[seeds], wl.lloyd_iters)
+            orc.residual_entries(K[ev], V[ev], a, mu, r, d)
+        t_build[r] = time.perf_counter() - t0
+        spent += t_build[r]
+    rs = np.array(sorted(t_build))
+    ts = np.array([t_build[r] for r in rs])
+
+    def head_cost(r):
+        if len(rs) == 1:
+            return ts[0] * max(r, 1) / max(rs[0], 1)
+        return float(np.interp(r, rs, ts, left=None, right=None)) if r <= rs[-1] else \
+            ts[-1] + (r - rs[-1]) * (ts[-1] - ts[-2]) / (rs[-1] - rs[-2])
+
+    # decode: a few layer-steps, every (sequence, query head), on caches of
+    # the decode shape (main rows from the prefill, residual rows from means)
     rng = np.random.default_rng(0)
+    r = int(np.median(r_row))
+    m = wl.budget[0] - r
     n_main = m + wl.steps // 2
-    kc = np.zeros((B, Hkv, r + n_main, d))
-    vc = np.zeros_like(kc)
-    Kall = x0["K"][:, :, :n_main + r].float().cpu().numpy().astype(np.float64)
-    Vall = x0["V"][:, :, :n_main + r].float().cpu().numpy().astype(np.float64)
-    kc[:] = Kall
-    vc[:] = Vall
+    kc = x0["K"][:, :, :n_main + r].float().cpu().numpy().astype(np.float64)
+    vc = x0["V"][:, :, :n_main + r].float().cpu().numpy().astype(np.float64)
     logc = np.log(rng.integers(1, 100, size=(B, Hkv, max(r, 1))).astype(np.float64))
     res_len = np.full((B, Hkv), r)
     main_len = np.full((B, Hkv), n_main)
     q = q0.float().cpu().numpy().astype(np.float64)
     tau = tau0.cpu().numpy().astype(np.float64)
+    n_dec = 4
     t0 = time.perf_counter()
-    orc.decode(q, kc, vc, logc, res_len, main_len, tau, wl.alpha, wl.g_min, wl.beta)
-    t_dec = time.perf_counter() - t0
+    for _ in range(n_dec):
+        orc.decode(q, kc, vc, logc, res_len, main_len, tau, wl.alpha, wl.g_min, wl.beta)
+    t_dec = (time.perf_counter() - t0) / n_dec
     # extrapolate to one job
-    job = 0.0
-    for l in range(wl.layers):
-        for b in range(B):
-            for hh in range(Hkv):
-                job += t_score + per_center * int(res_layers[l][b][hh])
+    job = sum(head_cost(int(res_layers[l][b][hh])) for l in range(wl.layers) for b in range(B) for hh in range(Hkv))
     job += t_dec * wl.layers * wl.steps
     tokens = B * wl.layers * wl.steps
+    built = ", ".join(f"r={r}: {t_build[r]:.2f}s" for r in rs)
     return dict(value=tokens / job, unit="tokens/s", cores=cores, blas_threads=blas_threads, kind="oracle",
-                sample=(f"fp64 numpy oracle on the host: construction of 1 (sequence, KV head) of layer 0 "
-                        f"(s={s}, r={r}: scoring+selection {t_score:.2f}s, Lloyd+summaries {t_lloyd:.2f}s) "
-                        f"and one decode layer-step for all {B}x{wl.hq} query heads ({t_dec:.2f}s); "
-                        f"extrapolated to the whole job ({job:.0f}s) with Lloyd cost scaled by r"),
-                seconds_measured=t_score + t_lloyd + t_dec)
+                sample=(f"fp64 numpy oracle on the host: construction (scores, selection, Lloyd, summaries) of "
+                        f"{len(rs)} (sequence, KV head) pairs of layer 0, one per residual count ({built}; "
+                        f"context {s}), and {n_dec} decode layer-steps for all {B}x{wl.hq} query heads "
+                        f"({t_dec:.2f}s each); extrapolated to the whole job ({job:.0f}s) with each head priced "
+                        f"at the measured head of its r"),
+                seconds_measured=spent + t_dec * n_dec)
 
 
-def workload_text(wl, L):
+def build_call_flops(wl, res):
+    """Algorithmic flops of one construction call: the window logits once
+    (2 d per visible (window row, key) pair, causal inside the window, every
+    query head of the group) and T Lloyd assignments of 2 |E| r' d each
+    (the method's products; the split-bf16 centres' second MFMA pass is not
+    counted)."""
+    B, Hkv, G, d, w, T = wl.batch, wl.hkv, wl.group, wl.d, wl.window, wl.lloyd_iters
+    score = lloyd = 0.0
+    for b in range(B):
+        s = wl.ctx[b]
+        pairs = w * (s - w) + w * (w + 1) // 2
+        for h in range(Hkv):
+            r = int(res[b][h])
+            m = wl.budget[b] - r
+            score += G * pairs * 2 * d
+            if s > m:
+                nE = s - m
+                lloyd += T * 2 * nE * min(r, nE) * d
+    return score, lloyd
+
+
+def counters_from_profile(name, src_hash):
+    """A committed rocprofv3 counter summary (profiles/<name>.json), if it was
+    taken on the current construction source."""
+    path = os.path.join(ROOT, "profiles", name + ".json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("build_source_sha256_16") != src_hash:
+        return None
+    return rec
+
+
+def progress(msg):
+    """One line on stderr per finished phase (the JSON result goes to stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+
+def per_config_run(rk, torch, np, synth, idx, dev, reps):
+    """Construction and decode of another workload, after the main job's
+    buffers are freed. Every layer is generated into one reused prefill
+    buffer, built once untimed and then `reps` times between events on the
+    launch stream (inputs resident in HBM); then every decode call of the
+    workload runs once as a warm-up, the cache lengths are reset to the built
+    ones, and the whole decode phase is captured as one HIP graph and
+    replayed between events. Returns the measurements."""
+    wl = synth.workload(idx)
+    L, B, Hq, Hkv, d = wl.layers, wl.batch, wl.hq, wl.hkv, wl.d
+    elem = 2 if wl.dtype == "bf16" else 4
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    C, Rcap, S = wl.slot_cap, wl.res_cap, wl.max_ctx
+    shape = rk.make_shape(B, Hq, Hkv, d, wl.dtype, C, Rcap)
+    params = rk.BuildParams(S, wl.window, wl.window, wl.lloyd_iters)
+    seq = np.asarray(wl.ctx, np.int32)
+    bud = np.asarray(wl.budget, np.int32)
+    res_layers = [np.asarray(wl.res[l], np.int32) for l in range(L)]
+    nws = max(rk.reskv_build_workspace_size(shape, params, seq, bud, res_layers[l].reshape(-1)) for l in range(L))
+    build_ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    buf = dict(K=torch.empty((B, Hkv, S, d), dtype=tdt, device=dev),
+               V=torch.empty((B, Hkv, S, d), dtype=tdt, device=dev))
+    stream = torch.cuda.current_stream()
+    caches, dec_in, built_len = [], [], []
+    build_ms = 0.0
+    for l in range(L):
+        x = synth.gen_layer_device(wl, l, dev, out=buf)
+        c = dict(kc=torch.empty((B, Hkv, C, d), dtype=tdt, device=dev),
+                 vc=torch.empty((B, Hkv, C, d), dtype=tdt, device=dev),
+                 logc=torch.empty((B, Hkv, Rcap), device=dev),
+                 main_idx=torch.empty((B, Hkv, C), dtype=torch.int32, device=dev),
+                 res_len=torch.empty((B * Hkv,), dtype=torch.int32, device=dev),
+                 main_len=torch.empty((B * Hkv,), dtype=torch.int32, device=dev))
+
+        def build():
+            rk.reskv_build_cache(shape, params, buf["K"], buf["V"], seq, x["q_obs"], bud, res_layers[l].reshape(-1),
+                                 c["kc"], c["vc"], c["logc"], c["main_idx"], c["res_len"], c["main_len"], build_ws)
+
+        build()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            build()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        build_ms += e0.elapsed_time(e1) / reps
+        if l == 0 or l == L - 1:
+            progress(f"{wl.name}: layer {l} built")
+        caches.append(c)
+        built_len.append(c["main_len"].clone())
+        dec_in.append(dict(q=x["q_dec"], kn=x["k_new"], vn=x["v_new"], tau=x["tau"]))
+        del x
+    del buf
+    dec_ws = torch.empty(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device=dev)
+    out = torch.empty((B, Hq, d), device=dev)
+    gates = [[rk.make_gate(tau=dec_in[l]["tau"][t], alpha=wl.alpha, g_min=wl.g_min, beta=wl.beta)
+              for t in range(wl.steps)] for l in range(L)]
+
+    def calls_on(st):
+        return [[rk.prepare_decode_attn(shape, gates[l][t], dec_in[l]["q"][t], caches[l]["kc"], caches[l]["vc"],
+                                        caches[l]["logc"], caches[l]["res_len"], caches[l]["main_len"], out, dec_ws,
+                                        k_new=dec_in[l]["kn"][t], v_new=dec_in[l]["vn"][t], stream=st)
+                 for l in range(L)] for t in range(wl.steps)]
+
+    for step in calls_on(stream):
+        for call in step:
+            call()
+    torch.cuda.synchronize()
+    for l in range(L):
+        caches[l]["main_len"].copy_(built_len[l])
+    torch.cuda.synchronize()
+    cap = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        for step in calls_on(cap):
+            for call in step:
+                call()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dec_ms = e0.elapsed_time(e1)
+    progress(f"{wl.name}: decode phase timed")
+    ended = np.concatenate([c["main_len"].cpu().numpy() for c in caches])
+    started = np.concatenate([x.cpu().numpy() for x in built_len])
+    assert (ended == started + wl.steps).all(), "decode appends missing"
+    dec_bytes = 0
+    for l in range(L):
+        r = res_layers[l].astype(np.int64)
+        m0 = np.minimum(np.asarray(wl.budget)[:, None] - r, np.asarray(wl.ctx)[:, None])
+        for t in range(wl.steps):
+            dec_bytes += decode_call_bytes(B, Hq, Hkv, d, elem, r, np.minimum(m0 + t + 1, C - r))
+    calls = L * wl.steps
+    b_bytes = sum(build_call_bytes(wl, elem, res_layers[l]) for l in range(L))
+    f_score = f_lloyd = 0.0
+    for l in range(L):
+        fs, fl = build_call_flops(wl, res_layers[l])
+        f_score += fs
+        f_lloyd += fl
+    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
+    b_tflops = (f_score + f_lloyd) / (build_ms * 1e-3) / 1e12
+    del g, caches, dec_in, built_len, build_ws, dec_ws
+    torch.cuda.empty_cache()
+    return wl, dict(
+        workload=workload_text(wl, L, what="construction of all layers + all decode steps, timed apart"),
+        layers=L, decode_steps=wl.steps,
+        build_ms_per_layer=build_ms / L, build_gbs=b_bytes / (build_ms * 1e-3) / 1e9,
+        build_bytes_per_layer=b_bytes / L, build_tflop_per_layer=(f_score + f_lloyd) / L / 1e12,
+        build_roofline={"bound": "mfma" if (f_score + f_lloyd) / 2.5e15 > b_bytes / 8e12 else "hbm",
+                        "achieved": b_tflops, "peak": 2500.0, "unit": "TFLOP/s", "frac": b_tflops / 2500.0,
+                        "hbm_gbs": b_bytes / (build_ms * 1e-3) / 1e9,
+                        "floor_ms_per_layer": max((f_score + f_lloyd) / 2.5e15, b_bytes / 8e12) * 1e3 / L},
+        decode_us_per_call=dec_ms * 1e3 / calls, decode_bytes_per_call=dec_bytes / calls, decode_gbs=dec_gbs,
+        decode_tokens_per_s=B * L * wl.steps / (dec_ms * 1e-3),
+        decode_roofline={"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": dec_gbs / HBM_PEAK_GBS, "calls_timed": calls},
+        decode_launch="hip_graph")
+
+
+def workload_text(wl, L, what="step = construction of all layers + all decode steps"):
     """What one timed step covers, with the workload's sizes."""
     import numpy as np
     ctx = (f"context {wl.ctx[0]}" if min(wl.ctx) == max(wl.ctx)
@@ -288,8 +476,7 @@ def workload_text(wl, L):
     rtxt = f"residual r per (layer, head) in {{{','.join(map(str, rs))}}}" if len(rs) <= 6 else \
         f"residual r per (layer, head) from {rs[0]} to {rs[-1]}"
     return (f"{wl.name}: {L} layers x (Hq {wl.hq} / Hkv {wl.hkv}, head_dim {wl.d}), batch {wl.batch}, {ctx} -> "
-            f"{bud} per KV head, {rtxt}, {wl.steps} decode steps with appends; "
-            f"step = construction of all layers + all decode steps")
+            f"{bud} per KV head, {rtxt}, {wl.steps} decode steps with appends; {what}")
 
 
 def main():
@@ -432,8 +619,10 @@ def main():
                           "copy_bytes_each_way": 256 << 20}), flush=True)
         return
 
+    progress(f"setup done ({t_setup:.1f} s)")
     for _ in range(args.warmup):
         job(False)
+    progress("warm-up jobs done")
     decode_launch = "eager"
     if not args.eager_decode:
         if args.warmup == 0:
@@ -454,6 +643,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1000 / args.steps
+    progress(f"{args.steps} timed jobs done ({ms_per_step:.1f} ms each)")
     graph_check = None
     if dec_graph is not None:
         # the replayed job's last output against the same job issued call by call
@@ -490,7 +680,8 @@ def main():
         source_hash("paper_2607_29591_amd/csrc/build.hip", "paper_2607_29591_amd/csrc/common.h"))
 
     result = {
-        "metric": "decode attn tokens/s (batch x layers)",
+        "metric": ("decode attn tokens/s (batch x layers), whole job: construction of every layer from the "
+                   "prefill plus every decode step"),
         "value": tokens / (ms_per_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -528,9 +719,26 @@ def main():
     if args.adakv_layers > 0:
         result["adakv_build"] = adakv_runs(rk, torch, wl, shape, layers, caches, res_layers,
                                            min(args.adakv_layers, L), dev)
+    progress("proxy and AdaKV constructions done")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, layers[0], q_stage[0, 0], tau_stage[0, 0], res_layers,
                                               args.cpu_budget_s)
+        progress("oracle baseline done")
+    others = [int(v) for v in args.per_config.split(",") if v.strip() != ""]
+    if others:
+        # the main job's buffers go before the other workloads are generated
+        del layers, caches, q_stage, kn_stage, vn_stage, tau_stage, dec_calls, build_ws, dec_ws, gates
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        bsrc = source_hash("paper_2607_29591_amd/csrc/build.hip", "paper_2607_29591_amd/csrc/common.h")
+        per = {}
+        for idx in others:
+            wl_i, rec = per_config_run(rk, torch, np, synth, idx, dev, args.per_config_reps)
+            prof = counters_from_profile(f"{wl_i.name}_construction_counters", bsrc)
+            if prof is not None:
+                rec["construction_mfma"] = prof["summary"]
+            per[wl_i.name] = rec
+        result["per_config"] = per
     print(json.dumps(result), flush=True)
 
 

@@ -116,6 +116,12 @@ typedef struct {
  *   dbg_assign      [T, B, Hkv, S]   optional (NULL): per Lloyd round, the
  *                                    group of each evicted position (-1 for
  *                                    main positions and rows >= s)
+ *   dbg_centers     [T, B, Hkv, Rcap, d] optional (NULL), fp32: per Lloyd
+ *                                    round, the centres that round assigns
+ *                                    against (round 0: the seed keys; round
+ *                                    t: the means of round t-1's groups, an
+ *                                    empty group keeping its centre); rows
+ *                                    j >= r' = min(r, |E|) are 0
  *   workspace       device scratch of reskv_build_workspace_size() bytes
  *
  * When s <= m every token is main and the r residual entries are empty.
@@ -132,11 +138,14 @@ reskv_status_t reskv_build_cache(const reskv_shape_t* shape,
                                  int32_t* main_idx,
                                  int32_t* res_len, int32_t* main_len,
                                  float* dbg_scores, int32_t* dbg_assign,
+                                 float* dbg_centers,
                                  void* workspace, size_t workspace_bytes,
                                  void* stream);
 
 /* Bytes of device workspace reskv_build_cache needs for these arguments
- * (0 if the arguments are invalid). */
+ * (0 if the arguments are invalid). The per-head sizes (s, b, r) fix the
+ * grids and scratch of the construction, so the host arrays of the call
+ * are arguments here too. */
 size_t reskv_build_workspace_size(const reskv_shape_t* shape,
                                   const reskv_build_params_t* params,
                                   const int32_t* seq_len_host,
@@ -159,9 +168,9 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
  *   - the remaining sum(k_top_h) - sum(floor) slots go down one ranking of
  *     every head's other scored tokens, by score descending, then KV head
  *     ascending, then position ascending; a head takes its next token only
- *     while it holds fewer than cap_h = min(s - |P|, C - r_h - |P|) top-k
+ *     while it holds fewer than cap_h = min(s - |P|, C' - r_h - |P|) top-k
  *     tokens (a head can hold more than k_top_h, so slot_cap above the
- *     budget leaves room to grow).
+ *     budget leaves room to grow), with C' = slot_cap - decode_reserve.
  * Head h then keeps its |P| recent tokens and its k'_h best-scored tokens
  * (ties to the lower position), and its r residual entries summarise the
  * rest as in reskv_build_cache (seeds: the evicted tokens of rank
@@ -169,6 +178,12 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
  * reskv_build_cache; safeguard = 0 is one top-k over all heads of a sequence.
  *
  *   safeguard       in [0, 1] (App. B.2.2: 0.2); Hkv <= 32
+ *   decode_reserve  slots per (b, kv head) kept free for the tokens that
+ *                   decode appends (Sec. 3.1): no head grows past
+ *                   slot_cap - decode_reserve, so after construction every
+ *                   head has room for decode_reserve appended tokens;
+ *                   0 <= decode_reserve and budget[b] + decode_reserve <=
+ *                   slot_cap
  *   other arguments as for reskv_build_cache, except:
  *   main_len        out int32 [B*Hkv]: |P| + k'_h (min(m, s) for heads with
  *                   s <= m); main_idx holds that many positions
@@ -179,6 +194,7 @@ size_t reskv_build_workspace_size(const reskv_shape_t* shape,
 reskv_status_t reskv_build_cache_adakv(const reskv_shape_t* shape,
                                        const reskv_build_params_t* params,
                                        double safeguard,
+                                       int32_t decode_reserve,
                                        const void* k, const void* v,
                                        const int32_t* seq_len_host,
                                        const void* q_obs,
@@ -188,6 +204,7 @@ reskv_status_t reskv_build_cache_adakv(const reskv_shape_t* shape,
                                        int32_t* main_idx,
                                        int32_t* res_len, int32_t* main_len,
                                        float* dbg_scores, int32_t* dbg_assign,
+                                       float* dbg_centers,
                                        void* workspace, size_t workspace_bytes,
                                        void* stream);
 
@@ -195,6 +212,7 @@ reskv_status_t reskv_build_cache_adakv(const reskv_shape_t* shape,
 size_t reskv_build_adakv_workspace_size(const reskv_shape_t* shape,
                                         const reskv_build_params_t* params,
                                         double safeguard,
+                                        int32_t decode_reserve,
                                         const int32_t* seq_len_host,
                                         const int32_t* budget_host,
                                         const int32_t* res_count_host);

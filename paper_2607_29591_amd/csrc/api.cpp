@@ -210,7 +210,7 @@ reskv_status_t reskv_build_cache(const reskv_shape_t* shape, const reskv_build_p
                                  const void* v, const int32_t* seq_len_host, const void* q_obs,
                                  const int32_t* budget_host, const int32_t* res_count_host, void* kc, void* vc,
                                  float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
-                                 float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                                 float* dbg_scores, int32_t* dbg_assign, float* dbg_centers, void* workspace,
                                  size_t workspace_bytes, void* stream) {
   reskv_status_t st = check_build(shape, params, seq_len_host, budget_host, res_count_host);
   if (st != RESKV_OK) return st;
@@ -223,15 +223,21 @@ reskv_status_t reskv_build_cache(const reskv_shape_t* shape, const reskv_build_p
     return fail(RESKV_ERR_WORKSPACE, "build needs %zu workspace bytes, got %zu", plan.bytes,
                 workspace ? workspace_bytes : (size_t)0);
   hipError_t e = launch_build(*shape, *params, plan, k, v, seq_len_host, q_obs, budget_host, res_count_host, kc,
-                              vc, logc, main_idx, res_len, main_len, dbg_scores, dbg_assign, workspace,
-                              (hipStream_t)stream);
+                              vc, logc, main_idx, res_len, main_len, dbg_scores, dbg_assign, dbg_centers,
+                              workspace, (hipStream_t)stream);
   if (e != hipSuccess) return fail(RESKV_ERR_HIP, "build launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 
-static reskv_status_t check_adakv(const reskv_shape_t* shape, double safeguard) {
+static reskv_status_t check_adakv(const reskv_shape_t* shape, double safeguard, int32_t decode_reserve,
+                                  const int32_t* budget) {
   if (!(safeguard >= 0.0 && safeguard <= 1.0))
     return fail(RESKV_ERR_INVALID_ARG, "safeguard %g outside [0, 1]", safeguard);
+  if (decode_reserve < 0) return fail(RESKV_ERR_INVALID_ARG, "decode_reserve %d must be >= 0", decode_reserve);
+  for (int b = 0; b < shape->batch; ++b)
+    if ((long long)budget[b] + decode_reserve > shape->slot_cap)
+      return fail(RESKV_ERR_INVALID_ARG, "budget[%d] + decode_reserve = %lld exceeds slot_cap (%d)", b,
+                  (long long)budget[b] + decode_reserve, shape->slot_cap);
   if (shape->num_kv_heads > kAdaMaxHeads)
     return fail(RESKV_ERR_UNSUPPORTED, "cross-head allocation over %d KV heads (at most %d)", shape->num_kv_heads,
                 kAdaMaxHeads);
@@ -239,36 +245,39 @@ static reskv_status_t check_adakv(const reskv_shape_t* shape, double safeguard) 
 }
 
 size_t reskv_build_adakv_workspace_size(const reskv_shape_t* shape, const reskv_build_params_t* params,
-                                        double safeguard, const int32_t* seq_len_host, const int32_t* budget_host,
-                                        const int32_t* res_count_host) {
+                                        double safeguard, int32_t decode_reserve, const int32_t* seq_len_host,
+                                        const int32_t* budget_host, const int32_t* res_count_host) {
   if (check_build(shape, params, seq_len_host, budget_host, res_count_host) != RESKV_OK) return 0;
-  if (check_adakv(shape, safeguard) != RESKV_OK) return 0;
+  if (check_adakv(shape, safeguard, decode_reserve, budget_host) != RESKV_OK) return 0;
   BuildPlan plan;
-  if (!make_build_plan_adakv(*shape, *params, safeguard, seq_len_host, budget_host, res_count_host, &plan))
+  if (!make_build_plan_adakv(*shape, *params, safeguard, decode_reserve, seq_len_host, budget_host, res_count_host,
+                             &plan))
     return 0;
   return plan.bytes;
 }
 
 reskv_status_t reskv_build_cache_adakv(const reskv_shape_t* shape, const reskv_build_params_t* params,
-                                       double safeguard, const void* k, const void* v, const int32_t* seq_len_host,
-                                       const void* q_obs, const int32_t* budget_host, const int32_t* res_count_host,
-                                       void* kc, void* vc, float* logc, int32_t* main_idx, int32_t* res_len,
-                                       int32_t* main_len, float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                                       double safeguard, int32_t decode_reserve, const void* k, const void* v,
+                                       const int32_t* seq_len_host, const void* q_obs, const int32_t* budget_host,
+                                       const int32_t* res_count_host, void* kc, void* vc, float* logc,
+                                       int32_t* main_idx, int32_t* res_len, int32_t* main_len, float* dbg_scores,
+                                       int32_t* dbg_assign, float* dbg_centers, void* workspace,
                                        size_t workspace_bytes, void* stream) {
   reskv_status_t st = check_build(shape, params, seq_len_host, budget_host, res_count_host);
   if (st != RESKV_OK) return st;
-  if ((st = check_adakv(shape, safeguard)) != RESKV_OK) return st;
+  if ((st = check_adakv(shape, safeguard, decode_reserve, budget_host)) != RESKV_OK) return st;
   if (!k || !v || !q_obs || !kc || !vc || !logc || !main_idx || !res_len || !main_len)
     return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
   BuildPlan plan;
-  if (!make_build_plan_adakv(*shape, *params, safeguard, seq_len_host, budget_host, res_count_host, &plan))
+  if (!make_build_plan_adakv(*shape, *params, safeguard, decode_reserve, seq_len_host, budget_host, res_count_host,
+                             &plan))
     return fail(RESKV_ERR_UNSUPPORTED, "construction plan could not be formed for these sizes");
   if (!workspace || workspace_bytes < plan.bytes)
     return fail(RESKV_ERR_WORKSPACE, "build needs %zu workspace bytes, got %zu", plan.bytes,
                 workspace ? workspace_bytes : (size_t)0);
-  hipError_t e = launch_build_adakv(*shape, *params, safeguard, plan, k, v, seq_len_host, q_obs, budget_host,
-                                    res_count_host, kc, vc, logc, main_idx, res_len, main_len, dbg_scores, dbg_assign,
-                                    workspace, (hipStream_t)stream);
+  hipError_t e = launch_build_adakv(*shape, *params, safeguard, decode_reserve, plan, k, v, seq_len_host, q_obs,
+                                    budget_host, res_count_host, kc, vc, logc, main_idx, res_len, main_len,
+                                    dbg_scores, dbg_assign, dbg_centers, workspace, (hipStream_t)stream);
   if (e != hipSuccess) return fail(RESKV_ERR_HIP, "build launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -70,6 +70,7 @@ struct BuildArgs {
   int32_t* main_len;
   float* dbg_scores;
   int32_t* dbg_assign;
+  float* dbg_centers;  // [T][BH][Rcap][D] or NULL
   const HeadMeta* meta;
   float2* lse_part;    // [BH][NCH][R] (max, sum) in base 2, one per lse block
   float* lse2;         // [BH][R]
@@ -89,6 +90,7 @@ struct BuildArgs {
   int B, Hq, Hkv, G, C, Rcap, S, w, R, LG, NCH, NBLK, T;
   int wr;              // leading window rows per query head that score (R = G * wr)
   int pool_half;       // pooling taps on each side of a position
+  int cap_slots;       // slots a head may fill at construction (C minus the decode reserve)
   float scale2;        // log2(e) / sqrt(d)
 };
 
@@ -626,7 +628,7 @@ __global__ __launch_bounds__(kAdaThreads) void adakv_alloc(BuildArgs a, HeadMeta
     const HeadMeta hm = meta[b * H + tid];
     const bool live = !hm.all_main;
     const int fl = live ? (int)floor(safeguard * (double)hm.k_top) : 0;
-    const int cap = live ? min(hm.n_sc, a.C - hm.r - hm.P) : 0;
+    const int cap = live ? min(hm.n_sc, a.cap_slots - hm.r - hm.P) : 0;
     s_floor[tid] = fl;
     s_room[tid] = live ? cap - fl : 0;
     s_n[tid] = live ? hm.n_sc : 0;
@@ -1330,6 +1332,19 @@ __global__ void fill_i32(int32_t* p, size_t n, int32_t v) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
+// Debug export of the centres round `iter` assigns against: rows j < r' of
+// the fp32 centres, zero rows after them.
+__global__ __launch_bounds__(kThreads) void export_centres(BuildArgs a, int iter, int D) {
+  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int bh = b * a.Hkv + kvh;
+  const int r_eff = a.meta[bh].r_eff;
+  const size_t n = (size_t)a.Rcap * D;
+  const float* src = a.cent + (size_t)bh * n;
+  float* dst = a.dbg_centers + ((size_t)iter * a.B * a.Hkv + bh) * n;
+  for (size_t i = blockIdx.x * (size_t)kThreads + threadIdx.x; i < n; i += (size_t)gridDim.x * kThreads)
+    dst[i] = (int)(i / D) < r_eff ? src[i] : 0.f;
+}
+
 // Sizes of one (b, kv head) from its context length s, residual count r and
 // budget b (main-selection equation, Sec. 5.2; reading R4 for |P|).
 __host__ __device__ inline HeadMeta make_meta(int s, int r, int budget, int recent) {
@@ -1363,13 +1378,14 @@ __global__ void meta_kernel(HeadMeta* meta, MetaChunk c) {
 // Arguments of every construction kernel; `meta` and the outputs belong to
 // the candidate being built, the scratch to the plan's workspace.
 BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const void* q_obs, const HeadMeta* meta,
-                    const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, void* workspace) {
+                    const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, float* dbg_centers,
+                    void* workspace) {
   char* ws = static_cast<char*>(workspace);
   BuildArgs a{};
   a.k = k; a.v = v; a.q_obs = q_obs;
   a.kc = out.kc; a.vc = out.vc; a.logc = out.logc; a.main_idx = out.main_idx;
   a.res_len = out.res_len; a.main_len = out.main_len;
-  a.dbg_scores = dbg_scores; a.dbg_assign = dbg_assign;
+  a.dbg_scores = dbg_scores; a.dbg_assign = dbg_assign; a.dbg_centers = dbg_centers;
   a.meta = meta;
   a.lse_part = reinterpret_cast<float2*>(ws + pl.off_lsep);
   a.lse2 = reinterpret_cast<float*>(ws + pl.off_lse);
@@ -1388,6 +1404,7 @@ BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const voi
   a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
   a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
   a.wr = pl.wr; a.pool_half = pl.pool_half; a.R = pl.R; a.LG = pl.LG; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
+  a.cap_slots = pl.C;
   a.scale2 = kLog2e / sqrtf((float)pl.D);
   return a;
 }
@@ -1433,6 +1450,11 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
     using S1 = AssignShape<T, D, false>;
     using S2 = AssignShape<T, D, true>;
     for (int it = 0; it < pl.T; ++it) {
+      if (a.dbg_centers) {
+        hipLaunchKernelGGL(export_centres, grid((pl.Rcap * D + kThreads * 8 - 1) / (kThreads * 8)), dim3(kThreads),
+                           0, st, a, it, D);
+        RESKV_CHECK();
+      }
       if (sizeof(T) == 2 && it == 0)  // centres are the seeds' bf16 keys: lo = 0
         hipLaunchKernelGGL((lloyd_assign<T, D, false>), grid((pl.max_E + S1::kTokens - 1) / S1::kTokens),
                            dim3(S1::kThreads), hist_lds, st, a, it);
@@ -1532,15 +1554,16 @@ bool layout_build_plan(BuildPlan* plan) {
 }
 
 bool make_build_plan_adakv(const reskv_shape_t& s, const reskv_build_params_t& p, double safeguard,
-                           const int32_t* seq_len, const int32_t* budget, const int32_t* res_count,
-                           BuildPlan* plan) {
+                           int decode_reserve, const int32_t* seq_len, const int32_t* budget,
+                           const int32_t* res_count, BuildPlan* plan) {
   init_build_plan(s, p, plan);
   std::vector<HeadMeta> hm;
   head_meta(*plan, seq_len, budget, res_count, p.recent_window, hm);
+  const int cslots = s.slot_cap - decode_reserve;
   for (HeadMeta& m : hm) {  // widest sizes the allocation can give each head
     if (m.all_main) continue;
     const int fl = (int)floor(safeguard * (double)m.k_top);
-    const int cap = m.n_sc < s.slot_cap - m.r - m.P ? m.n_sc : s.slot_cap - m.r - m.P;
+    const int cap = m.n_sc < cslots - m.r - m.P ? m.n_sc : cslots - m.r - m.P;
     m.main_len = m.P + cap;
     m.nE = m.s - m.P - fl;
     m.r_eff = m.r < m.nE ? m.r : m.nE;
@@ -1579,7 +1602,7 @@ hipError_t upload_meta(const BuildPlan& pl, const int32_t* seq_len, const int32_
 
 hipError_t launch_build_scores(const BuildPlan& pl, const void* k, const void* q_obs, const HeadMeta* meta,
                                void* workspace, hipStream_t stream) {
-  const BuildArgs a = make_args(pl, k, nullptr, q_obs, meta, BuildOut{}, nullptr, nullptr, workspace);
+  const BuildArgs a = make_args(pl, k, nullptr, q_obs, meta, BuildOut{}, nullptr, nullptr, nullptr, workspace);
   const bool bf = pl.dtype == RESKV_BF16;
   if (pl.D == 128) return bf ? launch_scores_typed<uint16_t, 128>(pl, a, stream) : launch_scores_typed<float, 128>(pl, a, stream);
   if (pl.D == 64) return bf ? launch_scores_typed<uint16_t, 64>(pl, a, stream) : launch_scores_typed<float, 64>(pl, a, stream);
@@ -1587,10 +1610,11 @@ hipError_t launch_build_scores(const BuildPlan& pl, const void* k, const void* q
 }
 
 hipError_t launch_build_adakv(const reskv_shape_t& s, const reskv_build_params_t& p, double safeguard,
-                              const BuildPlan& pl, const void* k, const void* v, const int32_t* seq_len,
-                              const void* q_obs, const int32_t* budget, const int32_t* res_count, void* kc,
-                              void* vc, float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
-                              float* dbg_scores, int32_t* dbg_assign, void* workspace, hipStream_t stream) {
+                              int decode_reserve, const BuildPlan& pl, const void* k, const void* v,
+                              const int32_t* seq_len, const void* q_obs, const int32_t* budget,
+                              const int32_t* res_count, void* kc, void* vc, float* logc, int32_t* main_idx,
+                              int32_t* res_len, int32_t* main_len, float* dbg_scores, int32_t* dbg_assign,
+                              float* dbg_centers, void* workspace, hipStream_t stream) {
   (void)s;
   HeadMeta* meta = reinterpret_cast<HeadMeta*>(static_cast<char*>(workspace) + pl.off_meta);
   hipError_t e = upload_meta(pl, seq_len, budget, res_count, p.recent_window, meta, stream);
@@ -1598,7 +1622,8 @@ hipError_t launch_build_adakv(const reskv_shape_t& s, const reskv_build_params_t
   e = launch_build_scores(pl, k, q_obs, meta, workspace, stream);
   if (e != hipSuccess) return e;
   const BuildOut out{kc, vc, logc, main_idx, res_len, main_len};
-  const BuildArgs a = make_args(pl, k, v, nullptr, meta, out, dbg_scores, dbg_assign, workspace);
+  BuildArgs a = make_args(pl, k, v, nullptr, meta, out, dbg_scores, dbg_assign, dbg_centers, workspace);
+  a.cap_slots = pl.C - decode_reserve;
   const bool bf = pl.dtype == RESKV_BF16;
   if (pl.D == 128)
     return bf ? launch_candidate_typed<uint16_t, 128>(pl, a, stream, meta, safeguard)
@@ -1610,9 +1635,9 @@ hipError_t launch_build_adakv(const reskv_shape_t& s, const reskv_build_params_t
 }
 
 hipError_t launch_build_candidate(const BuildPlan& pl, const void* k, const void* v, const HeadMeta* meta,
-                                  const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, void* workspace,
-                                  hipStream_t stream) {
-  const BuildArgs a = make_args(pl, k, v, nullptr, meta, out, dbg_scores, dbg_assign, workspace);
+                                  const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, float* dbg_centers,
+                                  void* workspace, hipStream_t stream) {
+  const BuildArgs a = make_args(pl, k, v, nullptr, meta, out, dbg_scores, dbg_assign, dbg_centers, workspace);
   const bool bf = pl.dtype == RESKV_BF16;
   if (pl.D == 128) return bf ? launch_candidate_typed<uint16_t, 128>(pl, a, stream) : launch_candidate_typed<float, 128>(pl, a, stream);
   if (pl.D == 64) return bf ? launch_candidate_typed<uint16_t, 64>(pl, a, stream) : launch_candidate_typed<float, 64>(pl, a, stream);
@@ -1623,7 +1648,7 @@ hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, c
                         const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
                         const int32_t* budget, const int32_t* res_count, void* kc, void* vc,
                         float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
-                        float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                        float* dbg_scores, int32_t* dbg_assign, float* dbg_centers, void* workspace,
                         hipStream_t stream) {
   (void)s;
   HeadMeta* meta = reinterpret_cast<HeadMeta*>(static_cast<char*>(workspace) + pl.off_meta);
@@ -1632,7 +1657,7 @@ hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, c
   e = launch_build_scores(pl, k, q_obs, meta, workspace, stream);
   if (e != hipSuccess) return e;
   const BuildOut out{kc, vc, logc, main_idx, res_len, main_len};
-  return launch_build_candidate(pl, k, v, meta, out, dbg_scores, dbg_assign, workspace, stream);
+  return launch_build_candidate(pl, k, v, meta, out, dbg_scores, dbg_assign, dbg_centers, workspace, stream);
 }
 
 }  // namespace reskv

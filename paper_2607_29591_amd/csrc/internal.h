@@ -102,31 +102,32 @@ hipError_t launch_build_scores(const BuildPlan& pl, const void* k, const void* q
 // Pooling, selection, gather and Lloyd rounds from the workspace's raw
 // scores, for the counts of `meta`, writing `out`.
 hipError_t launch_build_candidate(const BuildPlan& pl, const void* k, const void* v, const HeadMeta* meta,
-                                  const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, void* workspace,
-                                  hipStream_t stream);
+                                  const BuildOut& out, float* dbg_scores, int32_t* dbg_assign, float* dbg_centers,
+                                  void* workspace, hipStream_t stream);
 
 // AdaKV cross-head allocation (App. B.2.2 compared methods): at most this
 // many KV heads per sequence share their budgets.
 constexpr int kAdaMaxHeads = 32;
 
 // Plan whose grids cover every allocation the cross-head step can make: a
-// head may hold up to min(s, C - r) main slots and as few as
-// floor(safeguard * k_top) + |P|.
+// head may hold up to min(s, C' - r) main slots (C' = C - decode_reserve) and
+// as few as floor(safeguard * k_top) + |P|.
 bool make_build_plan_adakv(const reskv_shape_t& s, const reskv_build_params_t& p, double safeguard,
-                           const int32_t* seq_len, const int32_t* budget, const int32_t* res_count,
-                           BuildPlan* plan);
+                           int decode_reserve, const int32_t* seq_len, const int32_t* budget,
+                           const int32_t* res_count, BuildPlan* plan);
 
 hipError_t launch_build_adakv(const reskv_shape_t& s, const reskv_build_params_t& p, double safeguard,
-                              const BuildPlan& plan, const void* k, const void* v, const int32_t* seq_len,
-                              const void* q_obs, const int32_t* budget, const int32_t* res_count, void* kc,
-                              void* vc, float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
-                              float* dbg_scores, int32_t* dbg_assign, void* workspace, hipStream_t stream);
+                              int decode_reserve, const BuildPlan& plan, const void* k, const void* v,
+                              const int32_t* seq_len, const void* q_obs, const int32_t* budget,
+                              const int32_t* res_count, void* kc, void* vc, float* logc, int32_t* main_idx,
+                              int32_t* res_len, int32_t* main_len, float* dbg_scores, int32_t* dbg_assign,
+                              float* dbg_centers, void* workspace, hipStream_t stream);
 
 hipError_t launch_build(const reskv_shape_t& s, const reskv_build_params_t& p, const BuildPlan& plan,
                         const void* k, const void* v, const int32_t* seq_len, const void* q_obs,
                         const int32_t* budget, const int32_t* res_count, void* kc, void* vc,
                         float* logc, int32_t* main_idx, int32_t* res_len, int32_t* main_len,
-                        float* dbg_scores, int32_t* dbg_assign, void* workspace,
+                        float* dbg_scores, int32_t* dbg_assign, float* dbg_centers, void* workspace,
                         hipStream_t stream);
 
 // Validation proxy (Sec. 5.5.1; App. D, Algorithm 1).

@@ -301,7 +301,7 @@ hipError_t launch_build_proxy(const reskv_shape_t& s, const reskv_build_params_t
     const BuildOut out{kc_c + c * cache_elems * esz, vc_c + c * cache_elems * esz,
                        logc_c + (size_t)c * BH * bp.Rcap, midx_c + (size_t)c * BH * bp.C,
                        rlen_c + (size_t)c * BH, mlen_c + (size_t)c * BH};
-    RESKV_TRY(launch_build_candidate(bp, k, v, cmeta + (size_t)c * BH, out, nullptr, nullptr, workspace, stream));
+    RESKV_TRY(launch_build_candidate(bp, k, v, cmeta + (size_t)c * BH, out, nullptr, nullptr, nullptr, workspace, stream));
   }
   // validation queries and the uncompressed reference lengths
   GatherArgs ga{q_obs, ws + pl.off_q, bp.B, bp.Hq, bp.Hkv, bp.G, bp.w, bp.wr, pl.val, pl.GV, pl.GC, pl.NQC, pl.NG};

@@ -55,14 +55,14 @@ _lib = None
 _P = ctypes.c_void_p
 _SIG = {
     "reskv_build_cache": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams), _P, _P, _P, _P,
-                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_build_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
                                                      _P, _P, _P]),
     "reskv_build_cache_adakv": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams), ctypes.c_double,
-                                               _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                               ctypes.c_size_t, _P]),
+                                               ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                               _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_build_adakv_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
-                                                           ctypes.c_double, _P, _P, _P]),
+                                                           ctypes.c_double, ctypes.c_int32, _P, _P, _P]),
     "reskv_build_cache_proxy": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(BuildParams),
                                                ctypes.POINTER(ProxyParams), ctypes.POINTER(Gate), _P, _P, _P, _P,
                                                _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -138,34 +138,36 @@ def reskv_build_workspace_size(shape, params, seq_len, budget, res_count):
 
 
 def reskv_build_cache(shape, params, k, v, seq_len, q_obs, budget, res_count, kc, vc, logc, main_idx,
-                      res_len, main_len, workspace, dbg_scores=None, dbg_assign=None, stream=None):
+                      res_len, main_len, workspace, dbg_scores=None, dbg_assign=None, dbg_centers=None,
+                      stream=None):
     sl, slp = _host_i32(seq_len)
     bu, bup = _host_i32(budget)
     rc, rcp = _host_i32(res_count)
     _check(lib().reskv_build_cache(ctypes.byref(shape), ctypes.byref(params), _ptr(k), _ptr(v), slp,
                                    _ptr(q_obs), bup, rcp, _ptr(kc), _ptr(vc), _ptr(logc), _ptr(main_idx),
                                    _ptr(res_len), _ptr(main_len), _ptr(dbg_scores), _ptr(dbg_assign),
-                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                   _ptr(dbg_centers), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                    _stream(stream)))
 
 
-def reskv_build_adakv_workspace_size(shape, params, safeguard, seq_len, budget, res_count):
+def reskv_build_adakv_workspace_size(shape, params, safeguard, decode_reserve, seq_len, budget, res_count):
     sl, slp = _host_i32(seq_len)
     bu, bup = _host_i32(budget)
     rc, rcp = _host_i32(res_count)
     return lib().reskv_build_adakv_workspace_size(ctypes.byref(shape), ctypes.byref(params), float(safeguard),
-                                                  slp, bup, rcp)
+                                                  int(decode_reserve), slp, bup, rcp)
 
 
-def reskv_build_cache_adakv(shape, params, safeguard, k, v, seq_len, q_obs, budget, res_count, kc, vc, logc,
-                            main_idx, res_len, main_len, workspace, dbg_scores=None, dbg_assign=None, stream=None):
+def reskv_build_cache_adakv(shape, params, safeguard, decode_reserve, k, v, seq_len, q_obs, budget, res_count, kc,
+                            vc, logc, main_idx, res_len, main_len, workspace, dbg_scores=None, dbg_assign=None,
+                            dbg_centers=None, stream=None):
     sl, slp = _host_i32(seq_len)
     bu, bup = _host_i32(budget)
     rc, rcp = _host_i32(res_count)
-    _check(lib().reskv_build_cache_adakv(ctypes.byref(shape), ctypes.byref(params), float(safeguard), _ptr(k),
-                                         _ptr(v), slp, _ptr(q_obs), bup, rcp, _ptr(kc), _ptr(vc), _ptr(logc),
-                                         _ptr(main_idx), _ptr(res_len), _ptr(main_len), _ptr(dbg_scores),
-                                         _ptr(dbg_assign), _ptr(workspace),
+    _check(lib().reskv_build_cache_adakv(ctypes.byref(shape), ctypes.byref(params), float(safeguard),
+                                         int(decode_reserve), _ptr(k), _ptr(v), slp, _ptr(q_obs), bup, rcp, _ptr(kc),
+                                         _ptr(vc), _ptr(logc), _ptr(main_idx), _ptr(res_len), _ptr(main_len),
+                                         _ptr(dbg_scores), _ptr(dbg_assign), _ptr(dbg_centers), _ptr(workspace),
                                          workspace.numel() * workspace.element_size(), _stream(stream)))
 
 

@@ -30,7 +30,8 @@ int main(void) {
   /* valid sizes */
   EXPECT(reskv_decode_workspace_size(&sh) > 0);
   EXPECT(reskv_build_workspace_size(&sh, &bp, seq, bud, res) > 0);
-  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, 0.2, seq, bud, res) > 0);
+  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, 0.2, 0, seq, bud, res) > 0);
+  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, 0.2, 64, seq, bud, res) > 0);
   EXPECT(reskv_build_proxy_workspace_size(&sh, &bp, &px, seq, bud) > 0);
 
   /* invalid shapes and parameters: sizes are 0, calls return errors */
@@ -41,7 +42,7 @@ int main(void) {
          RESKV_ERR_UNSUPPORTED);
   bad = sh;
   bad.num_q_heads = 7;
-  EXPECT(reskv_build_cache(&bad, &bp, p, p, seq, p, bud, res, p, p, p, p, p, p, NULL, NULL, p, 64, NULL) ==
+  EXPECT(reskv_build_cache(&bad, &bp, p, p, seq, p, bud, res, p, p, p, p, p, p, NULL, NULL, NULL, p, 64, NULL) ==
          RESKV_ERR_INVALID_ARG);
   EXPECT(strlen(reskv_last_error()) > 0);
   reskv_gate_t bg = gate;
@@ -52,11 +53,16 @@ int main(void) {
          RESKV_ERR_WORKSPACE);
   int32_t bres[4] = {64, 0, 0, 0}; /* r >= budget */
   EXPECT(reskv_build_workspace_size(&sh, &bp, seq, bud, bres) == 0);
-  EXPECT(reskv_build_cache(&sh, &bp, p, p, seq, p, bud, bres, p, p, p, p, p, p, NULL, NULL, p, 1 << 30, NULL) ==
+  EXPECT(reskv_build_cache(&sh, &bp, p, p, seq, p, bud, bres, p, p, p, p, p, p, NULL, NULL, NULL, p, 1 << 30, NULL) ==
          RESKV_ERR_INVALID_ARG);
-  EXPECT(reskv_build_cache_adakv(&sh, &bp, 1.5, p, p, seq, p, bud, res, p, p, p, p, p, p, NULL, NULL, p, 1 << 30,
-                                 NULL) == RESKV_ERR_INVALID_ARG);
-  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, NAN, seq, bud, res) == 0);
+  EXPECT(reskv_build_cache_adakv(&sh, &bp, 1.5, 0, p, p, seq, p, bud, res, p, p, p, p, p, p, NULL, NULL, NULL, p,
+                                 1 << 30, NULL) == RESKV_ERR_INVALID_ARG);
+  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, NAN, 0, seq, bud, res) == 0);
+  /* the decode reserve must leave every budget inside the slot capacity */
+  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, 0.2, 577, seq, bud, res) == 0);
+  EXPECT(reskv_build_adakv_workspace_size(&sh, &bp, 0.2, -1, seq, bud, res) == 0);
+  EXPECT(reskv_build_cache_adakv(&sh, &bp, 0.2, 577, p, p, seq, p, bud, res, p, p, p, p, p, p, NULL, NULL, NULL, p,
+                                 1 << 30, NULL) == RESKV_ERR_INVALID_ARG);
   double nogrid[2] = {0.05, 0.1}; /* no zero fraction */
   reskv_proxy_params_t bpx = {nogrid, 2, 4, 0.01f};
   EXPECT(reskv_build_proxy_workspace_size(&sh, &bp, &bpx, seq, bud) == 0);

@@ -10,7 +10,8 @@ Parity contract for construction (scores, selection, Lloyd, entries):
   * Lloyd replay: in every round each evicted token's GPU group is an
     eps-argmin of the fp64 distances to the centres the oracle recomputes from
     the GPU's previous round (the first round uses the seeds the oracle selects
-    from the GPU scores);
+    from the GPU scores), with eps the error bound of the kernel's distance
+    arithmetic derived in replay_bound();
   * counts equal the oracle's recount of the GPU's last assignment; stored
     mean keys/values are within one storage ulp of the fp64 means of the GPU's
     groups (fp32 caches: 1e-6 relative); empty groups have log-count -inf.
@@ -43,12 +44,14 @@ class HostView:
 
 
 def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=False, host_cache=True, fit=0,
-              res=None, pool=0, adakv=None, slot_cap=None):
+              res=None, pool=0, adakv=None, slot_cap=None, reserve=0, centers=True):
     """Build one layer on the GPU; returns host numpy copies of the outputs
     (and the device tensors under "dev" when keep_device is set). `fit` > 0
     scores with the leading `fit` window rows only; `res` overrides x["res"];
     `pool` is the pooling kernel (0: the default 5); `adakv` = a safeguard
-    builds through reskv_build_cache_adakv; `slot_cap` overrides C."""
+    builds through reskv_build_cache_adakv with `reserve` slots per head kept
+    for decode appends; `slot_cap` overrides C; `centers` (with `dbg`)
+    exports every round's Lloyd centres."""
     B, Hkv, d = wl.batch, wl.hkv, wl.d
     S = x["K"].shape[2]
     C, Rcap = wl.slot_cap if slot_cap is None else slot_cap, wl.res_cap
@@ -68,18 +71,20 @@ def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=Fal
     main_len = torch.full((B * Hkv,), -7, dtype=torch.int32, device="cuda")
     dbg_s = torch.empty((B, Hkv, S), device="cuda") if dbg else None
     dbg_a = torch.empty((T, B, Hkv, S), dtype=torch.int32, device="cuda") if dbg else None
+    dbg_c = torch.full((T, B, Hkv, Rcap, d), float("nan"), device="cuda") if dbg and centers else None
     if adakv is None:
         nws = rk.reskv_build_workspace_size(shape, params, x["seq_len"], x["budget"], res)
     else:
-        nws = rk.reskv_build_adakv_workspace_size(shape, params, adakv, x["seq_len"], x["budget"], res)
+        nws = rk.reskv_build_adakv_workspace_size(shape, params, adakv, reserve, x["seq_len"], x["budget"], res)
     assert nws > 0
     ws = torch.empty(nws, dtype=torch.uint8, device="cuda")
     if adakv is None:
         rk.reskv_build_cache(shape, params, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc, main_idx,
-                             res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
+                             res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a, dbg_centers=dbg_c)
     else:
-        rk.reskv_build_cache_adakv(shape, params, adakv, K, V, x["seq_len"], Q, x["budget"], res, kc, vc, logc,
-                                   main_idx, res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a)
+        rk.reskv_build_cache_adakv(shape, params, adakv, reserve, K, V, x["seq_len"], Q, x["budget"], res, kc, vc,
+                                   logc, main_idx, res_len, main_len, ws, dbg_scores=dbg_s, dbg_assign=dbg_a,
+                                   dbg_centers=dbg_c)
     torch.cuda.synchronize()
     out = dict(logc=logc.cpu().numpy().astype(np.float64), main_idx=main_idx.cpu().numpy(),
                res_len=res_len.cpu().numpy().reshape(B, Hkv), main_len=main_len.cpu().numpy().reshape(B, Hkv))
@@ -93,6 +98,8 @@ def run_build(wl, x, layer=0, dbg=True, recent=None, iters=None, keep_device=Fal
     if dbg:
         out["scores"] = dbg_s.cpu().numpy().astype(np.float64)
         out["assign"] = dbg_a.cpu().numpy()
+    if dbg_c is not None:
+        out["centers"] = HostView(dbg_c)
     return out
 
 
@@ -105,12 +112,64 @@ def ulp(x, dtype):
     return np.maximum(x, 1e-30) * 2.0 ** -23
 
 
+# Lloyd replay tolerance. The kernel ranks centres by
+#   delta_pj = ||mu_j||^2 - 2 k_p . mu_j   (= ||k_p - mu_j||^2 - ||k_p||^2)
+# with mu_j the fp32 rounding of the group mean; bf16 caches split mu_j into
+# hi = bf16(mu_j) and lo = bf16(mu_j - hi), both rounded to nearest even, and
+# run the products k . hi and k . lo on MFMA (bf16 x bf16 products are exact in
+# fp32) with fp32 accumulation; ||mu_j||^2 is an fp64 sum rounded to fp32 and
+# delta is formed by one fp32 fma. With A_pj = sum_i |k_pi| |mu_ji| and
+# u = 2^-24, the kernel's delta differs from the exact one by at most
+#   e_pj = 2 (u_split + u + gamma) A_pj + u (3 ||mu_j||^2 + |delta_pj|)
+# where u_split = 2^-16 bounds |mu - hi - lo| / |mu| per element (lo's own
+# rounding, 2^-8 of |mu - hi| <= 2^-8 |mu|), u covers the fp32 rounding of the
+# mean, and gamma = n u bounds the fp32 accumulation of the n = 2D hi and lo
+# products (worst case, any summation order). fp32 caches have no split
+# (u_split = 0) and round each of the D products: gamma = (D + 1) u.
+# A token assigned to a while the exact argmin is j* must satisfy
+#   delta_pa - delta_pj* <= e_pa + e_pj*.
+# A kernel that dropped the lo part would err by up to 2^-8 A (bf16 rounding
+# of mu itself), 128 times the split term, and fails this bound.
+U32 = 2.0 ** -24
+U_SPLIT = 2.0 ** -16
+
+
+def replay_bound(d, dtype):
+    """(u_split, gamma) of the kernel's distance arithmetic at head_dim d."""
+    if dtype == "bf16":
+        return U_SPLIT, 2 * d * U32
+    return 0.0, (d + 1) * U32
+
+
+def replay_round(KE, mu, a, dtype):
+    """Check one Lloyd round: the tokens KE [n, d] were assigned a [n] against
+    centres mu [r', d] (fp64: the exact means of the previous round's
+    groups). Returns (mask of tokens outside the bound, largest excess of the
+    chosen centre over the exact best in units of the bound)."""
+    KE = np.asarray(KE, np.float64)
+    mu = np.asarray(mu, np.float64)
+    n = KE.shape[0]
+    nrm = (mu * mu).sum(axis=1)
+    delta = nrm[None, :] - 2.0 * (KE @ mu.T)
+    A = np.abs(KE) @ np.abs(mu).T
+    u_split, gamma = replay_bound(KE.shape[1], dtype)
+    e = 2.0 * (u_split + U32 + gamma) * A + U32 * (3.0 * nrm[None, :] + np.abs(delta))
+    rows = np.arange(n)
+    jstar = np.argmin(delta, axis=1)
+    excess = delta[rows, a] - delta[rows, jstar]
+    tol = e[rows, a] + e[rows, jstar]
+    bad = excess > tol
+    return bad, float((excess / tol).max()) if n else 0.0
+
+
 def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, replay=True, fit=None, r=None, pool=5,
-               k_top=None):
+               k_top=None, lloyd_info=True):
     """All construction checks for one (b, kv head). Returns a report dict.
     `fit` = leading window rows that scored (None: all); `r` overrides
     x["res"]; `pool` = pooling kernel; `k_top` = the head's top-k count when
-    a cross-head allocation set it (None: the uniform m - |P|)."""
+    a cross-head allocation set it (None: the uniform m - |P|);
+    `lloyd_info` also runs the oracle's own Lloyd from the same seeds and
+    reports its agreement (information only, slow at full size)."""
     recent = wl.window if recent is None else recent
     T = wl.lloyd_iters if iters is None else iters
     G = wl.group
@@ -164,16 +223,24 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
     r_eff = min(r, nE)
     mu = K[seeds_g].copy()
     assign = None
+    rep["replay_worst"] = 0.0
     for it in range(T):
         a = got["assign"][it, b, h][ev_g]
         assert (a >= 0).all() and (a < r_eff).all()
-        _, dist = orc.assign_nearest(KE, mu)
-        chosen = dist[np.arange(nE), a]
-        M = np.sqrt((mu ** 2).sum(1).max())
-        kn = np.sqrt((KE ** 2).sum(1))
-        eps = 1e-4 * (kn * M + M * M) + 1e-6
-        bad = chosen > dist.min(axis=1) + eps
-        assert not bad.any(), f"round {it}: {bad.sum()} tokens not at an eps-argmin"
+        if "centers" in got:
+            # the exported centres of this round are the fp32 roundings of the
+            # means the oracle recomputes (round 0: the seed keys, exactly);
+            # rows past r' are zero
+            cg = got["centers"][it, b, h]
+            ref32 = mu[:r_eff].astype(np.float32).astype(np.float64)
+            ulp32 = np.spacing(np.abs(ref32).astype(np.float32)).astype(np.float64)
+            assert (np.abs(cg[:r_eff] - ref32) <= ulp32).all(), f"round {it}: centres differ from the group means"
+            if it == 0:
+                np.testing.assert_array_equal(cg[:r_eff], K[seeds_g])
+            assert (cg[r_eff:] == 0).all()
+        bad, worst = replay_round(KE, mu[:r_eff], a, wl.dtype)
+        rep["replay_worst"] = max(rep["replay_worst"], worst)
+        assert not bad.any(), f"round {it}: {bad.sum()} tokens not at an eps-argmin (worst {worst:.2f} of the bound)"
         for j in range(r_eff):
             mem = a == j
             if mem.any():
@@ -192,7 +259,7 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
             assert (np.abs(got["kc"][b, h, j] - km) <= ulp(km, wl.dtype) * 1.0001).all(), f"kbar {j}"
             assert (np.abs(got["vc"][b, h, j] - vm) <= ulp(vm, wl.dtype) * 1.0001).all(), f"vbar {j}"
     assert cnt.sum() == nE
-    if full_oracle:
+    if full_oracle and lloyd_info:
         a_o, _, _ = orc.lloyd(KE, K[seeds_g], T)
         rep["lloyd_agree"] = float((a_o == assign).mean())
     return rep

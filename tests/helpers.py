@@ -13,6 +13,27 @@ from paper_2607_29591_amd import reskv as rk
 TOL = {"f32": 1e-5, "bf16": 2e-3}
 
 
+def gate_atol(q, Kmain, gate, lse_main, alpha):
+    """Bound on |g_gpu - g_ref| for one query from the kernel's logit
+    arithmetic. A logit a_p = <q, k_p> / sqrt(d) is an fp32 sum of d exact
+    products (bf16 x bf16, or fp32 products each rounded), scaled once and
+    fed to a base-2 exponential of a few ulp; with
+    delta = (d + 4) u max_p sum_i |q_i k_pi| / sqrt(d) + 2^-20 (u = 2^-24)
+    every logit is within delta, so p_max = e^{a_max - lse_main} is within
+    p_max (e^{2 delta} - 1) and the gate g = sigmoid((tau - p_max) alpha),
+    whose slope in p_max is alpha g (1 - g), within alpha g (1 - g) of that.
+    At large logits (heavy keys) this exceeds 1e-5 relative: the gate
+    amplifies p_max's relative error by alpha (1 - g) p_max."""
+    q = np.asarray(q, np.float64)
+    K = np.asarray(Kmain, np.float64)
+    d = q.shape[-1]
+    mag = (np.abs(K) @ np.abs(q)) / np.sqrt(d)
+    delta = (d + 4) * 2.0 ** -24 * float(mag.max()) + 2.0 ** -20
+    a_max = float((K @ q).max()) / np.sqrt(d)
+    p_max = float(np.exp(a_max - lse_main))
+    return alpha * gate * (1.0 - gate) * p_max * (np.exp(2.0 * delta) - 1.0) + 1e-6
+
+
 def tdtype(dtype):
     return torch.bfloat16 if dtype == "bf16" else torch.float32
 

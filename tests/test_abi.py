@@ -195,7 +195,21 @@ def test_adakv_workspace_covers_the_widest_allocation(L):
     p = rk.BuildParams(300, 16, 16, 4, 0, 0)
     uni = rk.reskv_build_workspace_size(sh, p, (300,), (64,), [13, 0])
     for g in (0.0, 0.2, 1.0):
-        assert rk.reskv_build_adakv_workspace_size(sh, p, g, (300,), (64,), [13, 0]) >= uni > 0
+        assert rk.reskv_build_adakv_workspace_size(sh, p, g, 0, (300,), (64,), [13, 0]) >= uni > 0
+        assert rk.reskv_build_adakv_workspace_size(sh, p, g, 64, (300,), (64,), [13, 0]) >= uni
+
+
+@pytest.mark.parametrize("reserve", [-1, 65])
+def test_adakv_rejects_bad_decode_reserve(L, reserve):
+    """budget + decode_reserve must fit the slot capacity (128 = 64 + 64)."""
+    sh = rk.make_shape(1, 4, 2, 64, "f32", 128, 13)
+    p = rk.BuildParams(300, 16, 16, 4, 0, 0)
+    assert rk.reskv_build_adakv_workspace_size(sh, p, 0.2, reserve, (300,), (64,), [13, 0]) == 0
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_build_cache_adakv(sh, p, 0.2, reserve, t, t, (300,), t, (64,), [13, 0], t, t, t, t, t, t, t,
+                                   stream=FakeStream())
+    assert ei.value.status == 1 and "decode_reserve" in rk.last_error()
 
 
 @pytest.mark.parametrize("safeguard,hkv,code", [(-0.1, 2, 1), (1.5, 2, 1), (float("nan"), 2, 1), (0.2, 33, 2)])
@@ -203,10 +217,10 @@ def test_adakv_rejects_bad_arguments(L, safeguard, hkv, code):
     sh = rk.make_shape(1, hkv, hkv, 64, "f32", 64, 13)
     p = rk.BuildParams(300, 16, 16, 4, 0, 0)
     res = [0] * hkv
-    assert rk.reskv_build_adakv_workspace_size(sh, p, safeguard, (300,), (64,), res) == 0
+    assert rk.reskv_build_adakv_workspace_size(sh, p, safeguard, 0, (300,), (64,), res) == 0
     t = FakeTensor()
     with pytest.raises(rk.ReskvError) as ei:
-        rk.reskv_build_cache_adakv(sh, p, safeguard, t, t, (300,), t, (64,), res, t, t, t, t, t, t, t,
+        rk.reskv_build_cache_adakv(sh, p, safeguard, 0, t, t, (300,), t, (64,), res, t, t, t, t, t, t, t,
                                    stream=FakeStream())
     assert ei.value.status == code
     assert rk.last_error()
@@ -217,7 +231,7 @@ def test_adakv_rejects_small_workspace(L):
     p = rk.BuildParams(300, 16, 16, 4, 0, 0)
     t = FakeTensor()
     with pytest.raises(rk.ReskvError) as ei:
-        rk.reskv_build_cache_adakv(sh, p, 0.2, t, t, (300,), t, (64,), [13, 0], t, t, t, t, t, t, FakeTensor(8),
+        rk.reskv_build_cache_adakv(sh, p, 0.2, 0, t, t, (300,), t, (64,), [13, 0], t, t, t, t, t, t, FakeTensor(8),
                                    stream=FakeStream())
     assert ei.value.status == 3
 

@@ -203,3 +203,52 @@ def test_adakv_llama_layer():
     got = run_build(wl, x, adakv=0.2, slot_cap=C, host_cache=False)
     replay = {0, int(np.argmax(wl.res[0, 0]))}
     assert check_sequence(wl, x, got, 0, 0.2, C, wl.window, replay_heads=replay) <= 2
+
+
+def test_adakv_decode_reserve_keeps_room_for_appends():
+    """With a decode reserve of R slots no head grows past C - R at
+    construction, so the next R decode steps append on every head (Sec. 3.1):
+    main_len grows by one per step everywhere, the appended rows are the
+    step's K/V bit for bit, and each step's output matches the oracle's
+    decode of the cache it attended. Safeguard 0 (one top-k over the heads of
+    a sequence) drives the best-scored heads to their caps."""
+    import torch
+    from paper_2607_29591_amd import reskv as rk
+    wl, x = workload(21, "bf16", 128, [900, 600], [96, 64], [[24, 0, 8, 40], [5, 16, 0, 31]], 16, 4)
+    C, R = 128, 8
+    wl.steps = R + 1
+    x = host_copies(synth.gen_layer(wl, 0, seed=21, n_decode=R + 1))
+    got = run_build(wl, x, adakv=0.0, slot_cap=C, reserve=R, keep_device=True)
+    for b in range(wl.batch):
+        check_sequence(wl, x, got, b, 0.0, C - R, wl.window)
+    ml0 = got["main_len"].reshape(-1).astype(np.int64)
+    rl = got["res_len"].reshape(-1).astype(np.int64)
+    assert (rl + ml0 <= C - R).all() and (rl + ml0 == C - R).any(), "no head reached its cap"
+    dev = got["dev"]
+    shape = rk.make_shape(wl.batch, wl.hq, wl.hkv, wl.d, wl.dtype, C, wl.res_cap)
+    ws = torch.empty(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    out = torch.empty((wl.batch, wl.hq, wl.d), device="cuda")
+    gate = rk.make_gate()
+    for t in range(R + 1):
+        q = torch.as_tensor(x["q_dec"][t]).to(torch.bfloat16).cuda().contiguous()
+        kn = torch.as_tensor(x["k_new"][t]).to(torch.bfloat16).cuda().contiguous()
+        vn = torch.as_tensor(x["v_new"][t]).to(torch.bfloat16).cuda().contiguous()
+        before = dev["main_len"].cpu().numpy().astype(np.int64)
+        rk.reskv_decode_attn(shape, gate, q, dev["kc"], dev["vc"], dev["logc"], dev["res_len"], dev["main_len"],
+                             out, ws, k_new=kn, v_new=vn)
+        torch.cuda.synchronize()
+        after = dev["main_len"].cpu().numpy().astype(np.int64)
+        room = rl + before < C
+        if t < R:
+            assert room.all()
+        np.testing.assert_array_equal(after, before + room)
+        kc = dev["kc"].float().cpu().numpy().astype(np.float64)
+        vc = dev["vc"].float().cpu().numpy().astype(np.float64)
+        for bh in np.nonzero(room)[0]:
+            b, h = divmod(int(bh), wl.hkv)
+            slot = int(rl[bh] + before[bh])
+            np.testing.assert_array_equal(kc[b, h, slot], x["k_new"][t, b, h])
+            np.testing.assert_array_equal(vc[b, h, slot], x["v_new"][t, b, h])
+        ref, *_ = orc.decode(x["q_dec"][t].astype(np.float64), kc, vc, got["logc"], rl.reshape(wl.batch, wl.hkv),
+                             after.reshape(wl.batch, wl.hkv), 0.25, 12.0, 0.0, 1.0)
+        assert rel_err_rows(out.double().cpu().numpy(), ref).max() <= TOL["bf16"], f"step {t}"

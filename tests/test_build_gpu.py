@@ -110,22 +110,6 @@ def test_build_is_deterministic():
         np.testing.assert_array_equal(a[k], b[k])
 
 
-def test_build_llama_layer_sampled():
-    """Llama-3.1-8B-shaped layer (32 q / 8 KV heads, d 128, 32K context,
-    budget 512, r per head from {0,16,32,64,128}): every head built on the
-    GPU; two heads checked in full against the oracle, every head checked for
-    exact selection on its own scores."""
-    wl = synth.workload(1)
-    x = host_copies(synth.gen_layer(wl, 0, n_decode=1))
-    got = run_build(wl, x)
-    ties = 0
-    for h in range(wl.hkv):
-        full = h in (0, int(np.argmax(wl.res[0, 0])))
-        rep = check_head(wl, x, got, 0, h, full_oracle=full, replay=full)
-        ties += rep["near_ties"]
-    assert ties <= 1
-
-
 @pytest.mark.parametrize("scorer", ["h2o", "tova", "pool3"])
 def test_build_alternative_scorers(scorer):
     """The compared scorers of App. B.2.2 through the same selection and

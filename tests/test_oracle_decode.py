@@ -59,6 +59,16 @@ def test_no_residual_is_eviction_attention():
         out, _ = orc.decode_head(q, K[kept], V[kept], np.zeros((0, K.shape[1])),
                                  np.zeros((0, K.shape[1])), np.zeros(0), 0.25, 12.0, 0.0, 1.0)
         np.testing.assert_allclose(out, sdpa(q, K[kept], V[kept]), rtol=1e-12, atol=1e-14)
+        # the oracle's eviction attention over the kept rows (Sec. 3.2) is
+        # the same library result, and equals the r = 0 decode
+        ev = orc.evict_attention(q, K, V, kept)
+        np.testing.assert_allclose(ev, sdpa(q, K[kept], V[kept]), rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(out, ev, rtol=1e-12, atol=1e-14)
+    # unsorted kept indices select the same rows
+    q, K, V = rand_qkv(11)
+    kept = np.array([30, 2, 17, 5])
+    np.testing.assert_allclose(orc.evict_attention(q, K, V, kept), sdpa(q, K[np.sort(kept)], V[np.sort(kept)]),
+                               rtol=1e-12, atol=1e-14)
 
 
 def test_empty_entries_contribute_nothing():
