@@ -331,6 +331,36 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
 size_t reskv_decode_workspace_size(const reskv_shape_t* shape);
 
 /*
+ * reskv_decode_attn_static - reskv_decode_attn without a workspace, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation). Same arguments,
+ * results and kernels as reskv_decode_attn; the split-K records live in a
+ * scratch array of 16 MiB that the library holds in device memory on every
+ * GPU it runs on until the process ends. The call allocates nothing.
+ *
+ *   stream          must belong to the calling thread's current device (the
+ *                   scratch of that device is used)
+ * Errors: RESKV_ERR_WORKSPACE when the shape takes the split-K path (fewer
+ * than 256 (sequence, KV head) pairs, or fp32 rows of 128) and its records
+ * need more than 16 MiB (reskv_decode_workspace_size(shape) > 16 MiB);
+ * otherwise as for reskv_decode_attn. All calls on one GPU share its scratch: calls that
+ * overlap in time on one GPU (on different streams) race and must not be
+ * issued; calls ordered on one stream are safe.
+ */
+reskv_status_t reskv_decode_attn_static(const reskv_shape_t* shape,
+                                        const reskv_gate_t* gate,
+                                        const void* q,
+                                        void* kc, void* vc,
+                                        const float* logc,
+                                        const int32_t* res_len,
+                                        int32_t* main_len,
+                                        const void* k_new, const void* v_new,
+                                        float* out,
+                                        float* dbg_lse_main, float* dbg_lse_res,
+                                        float* dbg_gate,
+                                        void* stream);
+
+/*
  * reskv_decode_branches - the two branches of one decode step, each under
  * its own softmax: the form in which a fused main-branch attention kernel
  * and a separately evaluated residual branch are combined through

@@ -106,6 +106,36 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape, const reskv_gate_t*
   return ok();
 }
 
+reskv_status_t reskv_decode_attn_static(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
+                                        void* kc, void* vc, const float* logc, const int32_t* res_len,
+                                        int32_t* main_len, const void* k_new, const void* v_new, float* out,
+                                        float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate, void* stream) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if ((st = check_gate(gate)) != RESKV_OK) return st;
+  if (!q || !kc || !vc || !logc || !res_len || !main_len || !out)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return fail(RESKV_ERR_INVALID_ARG, "k_new and v_new must both be given or both be NULL");
+  const DecodePlan plan = make_decode_plan(*shape);
+  if ((size_t)plan.GP * plan.P * sizeof(float) > decode_max_lds_weights())
+    return fail(RESKV_ERR_UNSUPPORTED, "%d split-K records per head do not fit the combine", plan.P);
+  // one block per (b, kv head) writes no split-K records
+  const size_t need = plan.whole_head ? 0 : plan.bytes;
+  if (need > kStaticScratchBytes)
+    return fail(RESKV_ERR_WORKSPACE,
+                "this shape needs %zu bytes of split-K scratch, above the %zu bytes of the library's static "
+                "scratch; use reskv_decode_attn with a workspace",
+                need, kStaticScratchBytes);
+  void* ws = nullptr;
+  hipError_t e = static_scratch(&ws);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "static scratch lookup failed: %s", hipGetErrorString(e));
+  e = launch_decode(*shape, *gate, plan, q, kc, vc, logc, res_len, main_len, k_new, v_new, out, dbg_lse_main,
+                    dbg_lse_res, dbg_gate, ws, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 reskv_status_t reskv_decode_branches(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
                                      const void* kc, const void* vc, const float* logc, const int32_t* res_len,
                                      const int32_t* main_len, float* out_main, float* lse_main, float* out_res,

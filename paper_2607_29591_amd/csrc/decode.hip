@@ -32,10 +32,19 @@
 //     (two MFMAs), fp32 caches use the fp32 MFMA. Lane (hd, g) ends with
 //     O[head hd][columns g*D/4 .. (g+1)*D/4), so rescaling by the per-head
 //     alpha and the final write need no cross-lane traffic.
+#include <mutex>
+
 #include "common.h"
 #include "internal.h"
 
 namespace reskv {
+
+// Scratch of the allocation-free decode entry point: split-K records live in
+// this file-scope device array instead of a caller workspace. Each GPU the
+// library runs on holds its own copy until the process ends; host code uses
+// the device address hipGetSymbolAddress returns for the current device,
+// never the array's name.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -844,6 +853,29 @@ hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const De
   if (pl.D == 128) return bf ? launch_gp<uint16_t, 128>(pl, da, stream) : launch_gp<float, 128>(pl, da, stream);
   if (pl.D == 64) return bf ? launch_gp<uint16_t, 64>(pl, da, stream) : launch_gp<float, 64>(pl, da, stream);
   return hipErrorInvalidValue;
+}
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::once_flag g_scratch_once[kMaxScratchDevices];
+void* g_scratch_ptr[kMaxScratchDevices];
+hipError_t g_scratch_err[kMaxScratchDevices];
+}  // namespace
+
+hipError_t static_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  // once per device, with that device current: the address of this GPU's copy
+  std::call_once(g_scratch_once[dev], [dev]() {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? p : nullptr;
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_decode_branches(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& pl,

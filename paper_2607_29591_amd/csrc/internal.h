@@ -21,6 +21,11 @@ struct DecodePlan {
 // Largest dynamic LDS the combine kernel may use for its weights.
 size_t decode_max_lds_weights();
 
+// Size of the file-scope device scratch of the allocation-free decode entry
+// point, and the current device's address of it (looked up once per device).
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+hipError_t static_scratch(void** ptr);
+
 DecodePlan make_decode_plan(const reskv_shape_t& s);
 
 hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& plan,

@@ -71,6 +71,8 @@ _SIG = {
     "reskv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
                                          _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_decode_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape)]),
+    "reskv_decode_attn_static": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P,
+                                                _P, _P, _P, _P, _P, _P, _P, _P]),
     "reskv_decode_branches": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
                                              _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_merge_branches": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P]),
@@ -207,6 +209,14 @@ def reskv_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, work
                                    _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(k_new), _ptr(v_new), _ptr(out),
                                    _ptr(dbg_lse_main), _ptr(dbg_lse_res), _ptr(dbg_gate), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def reskv_decode_attn_static(shape, gate, q, kc, vc, logc, res_len, main_len, out, dbg_lse_main=None,
+                             dbg_lse_res=None, dbg_gate=None, k_new=None, v_new=None, stream=None):
+    _check(lib().reskv_decode_attn_static(ctypes.byref(shape), ctypes.byref(gate), _ptr(q), _ptr(kc), _ptr(vc),
+                                          _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(k_new), _ptr(v_new),
+                                          _ptr(out), _ptr(dbg_lse_main), _ptr(dbg_lse_res), _ptr(dbg_gate),
+                                          _stream(stream)))
 
 
 def prepare_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, workspace,

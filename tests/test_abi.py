@@ -244,3 +244,14 @@ def test_prepared_decode_call_reports_errors(L):
     with pytest.raises(rk.ReskvError) as ei:
         call()
     assert ei.value.status == 2
+
+
+def test_static_decode_rejects_shapes_above_its_scratch(L):
+    """A shape whose split-K records exceed the 16 MiB static scratch is
+    refused before anything is launched (no GPU needed)."""
+    sh = rk.make_shape(1, 800, 200, 128, "bf16", 65536, 4096)
+    assert rk.reskv_decode_workspace_size(sh) > 16 << 20
+    t = FakeTensor()
+    with pytest.raises(rk.ReskvError) as ei:
+        rk.reskv_decode_attn_static(sh, rk.make_gate(), t, t, t, t, t, t, t, stream=FakeStream())
+    assert ei.value.status == 3 and "static scratch" in rk.last_error()
