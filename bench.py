@@ -341,7 +341,7 @@ def progress(msg):
     print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
-def per_config_run(rk, torch, np, synth, idx, dev, reps):
+def per_config_run(rk, torch, np, synth, idx, dev, reps, ragged):
     """Construction and decode of another workload, after the main job's
     buffers are freed. Every layer is generated into one reused prefill
     buffer, built once untimed and then `reps` times between events on the
@@ -401,37 +401,54 @@ def per_config_run(rk, torch, np, synth, idx, dev, reps):
     gates = [[rk.make_gate(tau=dec_in[l]["tau"][t], alpha=wl.alpha, g_min=wl.g_min, beta=wl.beta)
               for t in range(wl.steps)] for l in range(L)]
 
-    def calls_on(st):
-        return [[rk.prepare_decode_attn(shape, gates[l][t], dec_in[l]["q"][t], caches[l]["kc"], caches[l]["vc"],
-                                        caches[l]["logc"], caches[l]["res_len"], caches[l]["main_len"], out, dec_ws,
-                                        k_new=dec_in[l]["kn"][t], v_new=dec_in[l]["vn"][t], stream=st)
+    rag_ws = None
+    if ragged:
+        rag_ws = torch.empty(rk.reskv_decode_ragged_workspace_size(shape), dtype=torch.uint8, device=dev)
+
+    def calls_on(st, rag):
+        prep = rk.prepare_decode_attn_ragged if rag else rk.prepare_decode_attn
+        ws = rag_ws if rag else dec_ws
+        return [[prep(shape, gates[l][t], dec_in[l]["q"][t], caches[l]["kc"], caches[l]["vc"], caches[l]["logc"],
+                      caches[l]["res_len"], caches[l]["main_len"], out, ws, k_new=dec_in[l]["kn"][t],
+                      v_new=dec_in[l]["vn"][t], stream=st)
                  for l in range(L)] for t in range(wl.steps)]
 
-    for step in calls_on(stream):
-        for call in step:
-            call()
-    torch.cuda.synchronize()
-    for l in range(L):
-        caches[l]["main_len"].copy_(built_len[l])
-    torch.cuda.synchronize()
-    cap = torch.cuda.Stream()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=cap):
-        for step in calls_on(cap):
+    def timed_decode(rag):
+        """Warm-up pass, lengths reset, then the whole decode phase captured
+        as one HIP graph and replayed between events; the appends must have
+        grown every head by the number of steps."""
+        for step in calls_on(stream, rag):
             for call in step:
                 call()
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    g.replay()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    dec_ms = e0.elapsed_time(e1)
+        torch.cuda.synchronize()
+        for l in range(L):
+            caches[l]["main_len"].copy_(built_len[l])
+        torch.cuda.synchronize()
+        cap = torch.cuda.Stream()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            for step in calls_on(cap, rag):
+                for call in step:
+                    call()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ended = np.concatenate([c["main_len"].cpu().numpy() for c in caches])
+        started = np.concatenate([x.cpu().numpy() for x in built_len])
+        assert (ended == started + wl.steps).all(), "decode appends missing"
+        del g
+        return e0.elapsed_time(e1)
+
+    # the per-head schedule (reskv_decode_attn), then for ragged batches the
+    # balanced-range one (reskv_decode_attn_ragged) beside it, each from the
+    # built lengths
+    dec_ms = timed_decode(False)
+    rag_ms = timed_decode(True) if ragged else None
     progress(f"{wl.name}: decode phase timed")
-    ended = np.concatenate([c["main_len"].cpu().numpy() for c in caches])
-    started = np.concatenate([x.cpu().numpy() for x in built_len])
-    assert (ended == started + wl.steps).all(), "decode appends missing"
     dec_bytes = 0
     for l in range(L):
         r = res_layers[l].astype(np.int64)
@@ -447,7 +464,7 @@ def per_config_run(rk, torch, np, synth, idx, dev, reps):
         f_lloyd += fl
     dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
     b_tflops = (f_score + f_lloyd) / (build_ms * 1e-3) / 1e12
-    del g, caches, dec_in, built_len, build_ws, dec_ws
+    del caches, dec_in, built_len, build_ws, dec_ws, rag_ws
     torch.cuda.empty_cache()
     return wl, dict(
         workload=workload_text(wl, L, what="construction of all layers + all decode steps, timed apart"),
@@ -461,7 +478,11 @@ def per_config_run(rk, torch, np, synth, idx, dev, reps):
         decode_us_per_call=dec_ms * 1e3 / calls, decode_bytes_per_call=dec_bytes / calls, decode_gbs=dec_gbs,
         decode_tokens_per_s=B * L * wl.steps / (dec_ms * 1e-3),
         decode_roofline={"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": dec_gbs / HBM_PEAK_GBS, "calls_timed": calls},
+                         "frac": dec_gbs / HBM_PEAK_GBS, "calls_timed": calls,
+                         "kernel": ("reskv_decode_attn (decode_head: one block per (sequence, KV head), append "
+                                    "fused)" if B * Hkv >= 256 else "reskv_decode_attn (decode_split + "
+                                    "decode_combine, append fused)")},
+        decode_us_per_call_ragged_schedule=(rag_ms * 1e3 / calls if rag_ms is not None else None),
         decode_launch="hip_graph")
 
 
@@ -733,7 +754,9 @@ def main():
         bsrc = source_hash("paper_2607_29591_amd/csrc/build.hip", "paper_2607_29591_amd/csrc/common.h")
         per = {}
         for idx in others:
-            wl_i, rec = per_config_run(rk, torch, np, synth, idx, dev, args.per_config_reps)
+            # the ragged GQA-7 batch (budgets and contexts differ per sequence)
+            # decodes with the balanced-range schedule
+            wl_i, rec = per_config_run(rk, torch, np, synth, idx, dev, args.per_config_reps, ragged=idx == 4)
             prof = counters_from_profile(f"{wl_i.name}_construction_counters", bsrc)
             if prof is not None:
                 rec["construction_mfma"] = prof["summary"]

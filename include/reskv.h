@@ -331,6 +331,43 @@ reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
 size_t reskv_decode_workspace_size(const reskv_shape_t* shape);
 
 /*
+ * reskv_decode_attn_ragged - reskv_decode_attn scheduled for batches whose
+ * (b, kv head) caches differ widely in length (ragged contexts, budgets or
+ * residual counts): the same computation (Sec. 5.4, Sec. 5.5.2, App. D,
+ * Algorithm 2, with the optional fused append) and the same arguments, but
+ * the work is split into 64-slot units over the whole batch (per head its
+ * residual units, then its main units) and every block of the grid streams
+ * an equal range of that list, so no compute unit waits on the longest
+ * head. Heads that span several blocks are merged by a second kernel, which
+ * also advances main_len. Outputs equal reskv_decode_attn's within rounding
+ * (a different order of the same fp32 sums).
+ *
+ *   workspace       device scratch of reskv_decode_ragged_workspace_size()
+ *                   bytes (the per-call plan and the partial records of
+ *                   shared heads); calls sharing one must not overlap.
+ * Supported: G <= 8, B*Hkv <= 2048, C <= 64960 slots, bf16 rows (fp32
+ * rows of d = 64); otherwise RESKV_ERR_UNSUPPORTED. Errors as for
+ * reskv_decode_attn.
+ */
+reskv_status_t reskv_decode_attn_ragged(const reskv_shape_t* shape,
+                                        const reskv_gate_t* gate,
+                                        const void* q,
+                                        void* kc, void* vc,
+                                        const float* logc,
+                                        const int32_t* res_len,
+                                        int32_t* main_len,
+                                        const void* k_new, const void* v_new,
+                                        float* out,
+                                        float* dbg_lse_main, float* dbg_lse_res,
+                                        float* dbg_gate,
+                                        void* workspace, size_t workspace_bytes,
+                                        void* stream);
+
+/* Bytes of device workspace reskv_decode_attn_ragged needs (0 if invalid or
+ * unsupported). */
+size_t reskv_decode_ragged_workspace_size(const reskv_shape_t* shape);
+
+/*
  * reskv_decode_attn_static - reskv_decode_attn without a workspace, for
  * callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation). Same arguments,

@@ -136,6 +136,39 @@ reskv_status_t reskv_decode_attn_static(const reskv_shape_t* shape, const reskv_
   return ok();
 }
 
+size_t reskv_decode_ragged_workspace_size(const reskv_shape_t* shape) {
+  if (check_shape(shape) != RESKV_OK) return 0;
+  RaggedPlan plan;
+  if (!make_ragged_plan(*shape, &plan)) return 0;
+  return plan.bytes;
+}
+
+reskv_status_t reskv_decode_attn_ragged(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
+                                        void* kc, void* vc, const float* logc, const int32_t* res_len,
+                                        int32_t* main_len, const void* k_new, const void* v_new, float* out,
+                                        float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  reskv_status_t st = check_shape(shape);
+  if (st != RESKV_OK) return st;
+  if ((st = check_gate(gate)) != RESKV_OK) return st;
+  if (!q || !kc || !vc || !logc || !res_len || !main_len || !out)
+    return fail(RESKV_ERR_INVALID_ARG, "a required pointer is NULL");
+  if ((k_new == nullptr) != (v_new == nullptr))
+    return fail(RESKV_ERR_INVALID_ARG, "k_new and v_new must both be given or both be NULL");
+  RaggedPlan plan;
+  if (!make_ragged_plan(*shape, &plan))
+    return fail(RESKV_ERR_UNSUPPORTED,
+                "the ragged schedule takes group sizes up to 8, at most 2048 (sequence, KV head) pairs, slot "
+                "capacities up to 64960 and bf16 rows (fp32 rows of 64)");
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(RESKV_ERR_WORKSPACE, "ragged decode needs %zu workspace bytes, got %zu", plan.bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  hipError_t e = launch_decode_ragged(*shape, *gate, plan, q, kc, vc, logc, res_len, main_len, k_new, v_new, out,
+                                      dbg_lse_main, dbg_lse_res, dbg_gate, workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(RESKV_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 reskv_status_t reskv_decode_branches(const reskv_shape_t* shape, const reskv_gate_t* gate, const void* q,
                                      const void* kc, const void* vc, const float* logc, const int32_t* res_len,
                                      const int32_t* main_len, float* out_main, float* lse_main, float* out_res,

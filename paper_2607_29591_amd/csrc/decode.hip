@@ -72,7 +72,12 @@ struct DecodeArgs {
   float* dbg_lse_res;
   float* dbg_gate;
   float* out_res;   // two-branch mode: the residual branch's own output (out = the main branch's)
+  int32_t* plan;    // ragged schedule: [BH] unit prefix, then U and the block count
+  float* rec;       // ragged schedule: [blocks][2 edges][2 kinds][GP][D + 2] partial states
   int Hq, Hkv, G, C, Rcap, PR, P;
+  int BH;           // B * Hkv
+  int rag_blocks;   // ragged schedule: at least this many blocks (one per CU)
+  int rag_min_units;  // ragged schedule: at least this many units per block
   float qk_scale;   // log2(e) / sqrt(d)
   float beta_log2;  // beta * log2(e)
   float tau_scalar, alpha, g_min;
@@ -657,9 +662,11 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
       for (int t = 0; t < kTiles; ++t)
         if (s0 + 16 * t + hd == app_row) ur.k[t].store(kc + (size_t)app_row * D, g);
     }
+    // the value rows are requested before the logits wait on the keys, so
+    // both halves of the unit are in flight together
+    load_unit_v<T, D>(ur, vc, s0, nvalid, hd, g, app_row, vn);
     float sc[kTiles][4];
     unit_logits<T, D>(ur, q, a.qk_scale, sc);
-    load_unit_v<T, D>(ur, vc, s0, nvalid, hd, g, app_row, vn);
     softmax_pv<T, D>(st, ur, sc, 0, nvalid, is_res, a.beta_log2, g);
     if (has_app) {
 #pragma unroll
@@ -760,6 +767,326 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   if (app && tid == 0) a.main_len[bh] = n;
 }
 
+// ------------------------------------------------------ ragged schedule
+//
+// For batches whose (b, kv head) caches differ in length, one block per head
+// leaves the CUs of short heads idle while the longest heads finish. Here the
+// heads' 64-slot units form one list (per head: its residual units, then its
+// main units) and block i streams units [i U / NB, (i + 1) U / NB) of it, so
+// every block streams about the same number of slots; NB = max(CUs,
+// ceil(U / kRagUnits)) keeps a block at <= 2 units per wave. Within a block
+// unit j goes to wave j % 8; a wave keeps one online-softmax state and
+// parks it in LDS slot j (the wave's first unit of that (head, kind)
+// segment) when its next unit belongs to another segment, so a segment's
+// states are the slots of its first (up to) 8 units. A head that lies wholly
+// inside a block is finished there (gate, shared denominator); the blocks
+// that share a head write partial records (per kind: max, sum, accumulator)
+// and decode_ragged_combine merges them after the kernel boundary. Every
+// block reads every head's lengths for the plan, so main_len is advanced by
+// the combine kernel, never while a block may still read it.
+constexpr int kRagUnits = 16;       // units per block at most (2 per wave)
+constexpr int kRagMaxHeads = 2048;  // (b, kv head) pairs the plan holds in LDS
+constexpr int kRagMinBlocks = 256;  // the chip's compute units
+constexpr int kRagMaxRec = 128;     // blocks one head may span (records the combine merges)
+
+// Head of global unit u: the last h with pre[h] <= u (pre ascending).
+__device__ __forceinline__ int rag_head(const int* pre, int BH, int u) {
+  int lo = 0, hi = BH - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= u) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// First unit of block b of NB over U units, and the block of unit u.
+__device__ __forceinline__ int rag_lo(int b, int U, int NB) { return (int)(((long long)b * U) / NB); }
+__device__ __forceinline__ int rag_block(int u, int U, int NB) {
+  return (int)((((long long)u + 1) * NB - 1) / U);
+}
+
+// Units of one head: residual units, then main units (with this step's token).
+__device__ __forceinline__ void rag_units(const DecodeArgs& a, int bh, int& r, int& n, int& ur, int& um, bool& app) {
+  cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  app = a.k_new != nullptr && r + n < a.C;
+  ur = (r + kUnit - 1) / kUnit;
+  um = (n + (app ? 1 : 0) + kUnit - 1) / kUnit;
+}
+
+// Shared-softmax output of query head h from the merged main (M, l, o) and
+// residual (mR, lR, oR) states of one output element (base-2 maxima), with
+// the gate; returns the output and, through the references, p_max's gate.
+__device__ __forceinline__ float rag_output(const DecodeArgs& a, int qh, float M, float l, float oM, float mR,
+                                            float lR, float oR, float& g) {
+  const float pmax = l > 0.f ? 1.f / l : 1.f;
+  const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
+  g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
+  const float lg2g = g > 0.f ? log2f(g) : kNegInf;
+  const float mRg = (mR == kNegInf || lg2g == kNegInf) ? kNegInf : mR + lg2g;
+  const float Mx = fmaxf(M, mRg);
+  const float fM = M != kNegInf ? exp2f(M - Mx) : 0.f;
+  const float fR = mRg != kNegInf ? exp2f(mRg - Mx) : 0.f;
+  const float den = l * fM + lR * fR;
+  const float num = oM * fM + oR * fR;
+  return den > 0.f ? num / den : 0.f;
+}
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kHeadThreads) void decode_ragged(DecodeArgs a) {
+  __shared__ int s_pre[kRagMaxHeads];  // first unit of each head
+  __shared__ int s_r[kRagMaxHeads];    // residual slots
+  __shared__ int s_n[kRagMaxHeads];    // main slots, bit 30: this step's token is appended
+  __shared__ int s_wsum[kHeadWaves];
+  __shared__ int s_tot;
+  __shared__ float s_acc[kRagUnits][GP][D];  // parked wave states, slot = relative unit
+  __shared__ float s_m[kRagUnits][GP];
+  __shared__ float s_l[kRagUnits][GP];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int hd = lane & 15, g = lane >> 4;
+  const int BH = a.BH;
+  constexpr int kApp = 1 << 30;
+
+  // plan: the heads' lengths, then the exclusive prefix of their unit counts
+  // (each thread a run of consecutive heads, then a block scan of the run sums)
+  const int per = (BH + kHeadThreads - 1) / kHeadThreads;
+  const int h0 = min(BH, tid * per), h1 = min(BH, h0 + per);
+  int run = 0;
+  for (int h = h0; h < h1; ++h) {
+    int r, n, ur, um;
+    bool app;
+    rag_units(a, h, r, n, ur, um, app);
+    s_r[h] = r;
+    s_n[h] = n | (app ? kApp : 0);
+    s_pre[h] = ur + um;
+    run += ur + um;
+  }
+  int incl = run;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  if (lane == 63) s_wsum[wave] = incl;
+  __syncthreads();
+  int before = incl - run;
+  for (int w = 0; w < wave; ++w) before += s_wsum[w];
+  if (tid == kHeadThreads - 1) s_tot = before + run;
+  for (int h = h0; h < h1; ++h) {
+    const int c = s_pre[h];
+    s_pre[h] = before;
+    before += c;
+  }
+  __syncthreads();
+  const int U = s_tot;
+  // at least one block per CU and at most kRagUnits units per block, but no
+  // fewer than rag_min_units per block, so a head spans at most kRagMaxRec
+  // blocks
+  const int NB = max(1, min(max(a.rag_blocks, (U + kRagUnits - 1) / kRagUnits), U / a.rag_min_units));
+  const int blk = blockIdx.x;
+  if (blk == 0) {  // the plan the combine kernel reads: prefix, U, NB, block starts
+    for (int h = tid; h < BH; h += kHeadThreads) a.plan[h] = s_pre[h];
+    for (int b = tid; b <= NB; b += kHeadThreads) a.plan[BH + 2 + b] = rag_lo(b, U, NB);
+    if (tid == 0) { a.plan[BH] = U; a.plan[BH + 1] = NB; }
+  }
+  if (blk >= NB) return;  // block-uniform
+  const int lo = rag_lo(blk, U, NB), hi = rag_lo(blk + 1, U, NB);
+  if (lo >= hi) return;  // fewer units than blocks: this block has none
+
+  // this wave's units lo + wave, lo + wave + 8, ...
+  WaveState<D> st;
+  st.reset();
+  int cur_seg = -1, cur_slot = 0, cur_bh = -1;
+  Frag<T, D> q;
+  for (int j = wave; j < hi - lo; j += kHeadWaves) {  // wave-uniform
+    const int u = lo + j;
+    const int bh = rag_head(s_pre, BH, u);
+    const int r = s_r[bh], nw = s_n[bh];
+    const bool app = (nw & kApp) != 0;
+    const int n = nw & (kApp - 1);
+    const int ur = (r + kUnit - 1) / kUnit;
+    const int k = u - s_pre[bh];
+    const bool is_res = k < ur;
+    const int seg = 2 * bh + (is_res ? 0 : 1);
+    const int nn = n + (app ? 1 : 0);
+    const int s0 = is_res ? k * kUnit : r + (k - ur) * kUnit;
+    const int end = is_res ? r : r + nn;
+    const int nvalid = min(kUnit, end - s0);
+    const int app_row = app ? r + n : -1;
+    const T* kc = static_cast<const T*>(a.kc) + (size_t)bh * a.C * D;
+    const T* vc = static_cast<const T*>(a.vc) + (size_t)bh * a.C * D;
+    const T* kn = app ? static_cast<const T*>(a.k_new) + (size_t)bh * D : nullptr;
+    const T* vn = app ? static_cast<const T*>(a.v_new) + (size_t)bh * D : nullptr;
+    UnitRegs<T, D> ur_;
+    load_unit_k<T, D>(ur_, kc, s0, end - 1, hd, g, app_row, kn);
+    if (seg != cur_seg) {
+      if (cur_seg >= 0) store_wave_state<D, GP>(st, s_acc[cur_slot], s_m[cur_slot], s_l[cur_slot], hd, g);
+      st.reset();
+      cur_seg = seg;
+      cur_slot = j;
+    }
+    if (bh != cur_bh) {
+      const int b = bh / a.Hkv, kvh = bh - b * a.Hkv;
+      if (hd < a.G) q.load(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + hd) * D, g);
+      else q.zero();
+      cur_bh = bh;
+    }
+    if (is_res) load_unit_lc<T, D>(ur_, a.logc + (size_t)bh * a.Rcap, s0, nvalid, g);
+    float sc[kTiles][4];
+    unit_logits<T, D>(ur_, q, a.qk_scale, sc);
+    load_unit_v<T, D>(ur_, vc, s0, nvalid, hd, g, app_row, vn);
+    softmax_pv<T, D>(st, ur_, sc, 0, nvalid, is_res, a.beta_log2, g);
+    if (app_row >= s0 && app_row < s0 + nvalid) {  // wave-uniform: the new rows into the cache
+      constexpr int kPieces = D * (int)sizeof(T) / 16;
+      if (lane < 2 * kPieces) {
+        const bool isv = lane >= kPieces;
+        const int c = isv ? lane - kPieces : lane;
+        T* dst = static_cast<T*>(const_cast<void*>(isv ? a.vc : a.kc)) + ((size_t)bh * a.C + app_row) * D;
+        reinterpret_cast<uint4*>(dst)[c] = reinterpret_cast<const uint4*>(isv ? vn : kn)[c];
+      }
+    }
+  }
+  if (cur_seg >= 0) store_wave_state<D, GP>(st, s_acc[cur_slot], s_m[cur_slot], s_l[cur_slot], hd, g);
+  __syncthreads();
+
+  // merge the parked states of each (head, kind) segment of the block; a head
+  // wholly inside the block is finished here, the others leave records
+  constexpr int kPer = (GP * D + kHeadThreads - 1) / kHeadThreads;
+  const int hlo = rag_head(s_pre, BH, lo), hhi = rag_head(s_pre, BH, hi - 1);
+  for (int bh = hlo; bh <= hhi; ++bh) {  // block-uniform
+    const int r = s_r[bh], nw = s_n[bh];
+    const int ur = (r + kUnit - 1) / kUnit;
+    const int um = ((nw & (kApp - 1)) + ((nw & kApp) ? 1 : 0) + kUnit - 1) / kUnit;
+    const int P0 = s_pre[bh];
+    const bool whole = P0 >= lo && P0 + ur + um <= hi;
+    const int edge = bh == hlo ? 0 : 1;
+    const int b = bh / a.Hkv, kvh = bh - b * a.Hkv;
+    // relative unit ranges of the two kinds inside the block
+    const int ra = max(P0, lo) - lo, rb = min(P0 + ur, hi) - lo;
+    const int ma = max(P0 + ur, lo) - lo, mb = min(P0 + ur + um, hi) - lo;
+#pragma unroll
+    for (int kk = 0; kk < kPer; ++kk) {
+      const int idx = tid + kk * kHeadThreads;
+      if (idx >= GP * D) continue;
+      const int h = idx / D, d = idx % D;
+      float Mk[2], Lk[2], Ok[2];
+#pragma unroll
+      for (int kind = 0; kind < 2; ++kind) {
+        const int sa = kind == 0 ? ra : ma, sb = kind == 0 ? rb : mb;
+        const int se = min(sa + kHeadWaves, sb);
+        float M = kNegInf;
+        for (int sl = sa; sl < se; ++sl) M = fmaxf(M, s_m[sl][h]);
+        float l = 0.f, o = 0.f;
+        if (M != kNegInf)
+          for (int sl = sa; sl < se; ++sl) {
+            const float f = exp2f(s_m[sl][h] - M);
+            o = fmaf(f, s_acc[sl][h][d], o);
+            l = fmaf(f, s_l[sl][h], l);
+          }
+        Mk[kind] = M; Lk[kind] = l; Ok[kind] = o;
+      }
+      if (whole) {
+        if (h < a.G) {
+          const int qh = b * a.Hq + kvh * a.G + h;
+          float gg;
+          a.out[(size_t)qh * D + d] = rag_output(a, qh, Mk[1], Lk[1], Ok[1], Mk[0], Lk[0], Ok[0], gg);
+          if (d == 0) {
+            if (a.dbg_lse_main) a.dbg_lse_main[qh] = Lk[1] > 0.f ? (Mk[1] + log2f(Lk[1])) * kLn2 : kNegInf;
+            if (a.dbg_lse_res) a.dbg_lse_res[qh] = Lk[0] > 0.f ? (Mk[0] + log2f(Lk[0])) * kLn2 : kNegInf;
+            if (a.dbg_gate) a.dbg_gate[qh] = gg;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kind = 0; kind < 2; ++kind) {
+          float* rc = a.rec + (((size_t)blk * 2 + edge) * 2 + kind) * GP * (D + 2);
+          rc[h * D + d] = Ok[kind];
+          if (d == 0) {
+            rc[GP * D + h] = Mk[kind];
+            rc[GP * D + GP + h] = Lk[kind];
+          }
+        }
+      }
+    }
+  }
+}
+
+// Heads shared by several blocks: merge their records (ascending block
+// order), apply the gate and write the outputs; then advance every head's
+// main_len by the appended token. One block per (b, kv head).
+template <int D, int GP>
+__global__ __launch_bounds__(kThreads) void decode_ragged_combine(DecodeArgs a) {
+  __shared__ int s_idx[kRagMaxRec];
+  __shared__ float s_w[kRagMaxRec][2][GP];  // record max, then its weight e^{m - M}
+  __shared__ float s_lr[kRagMaxRec][2][GP]; // record sum
+  __shared__ float s_lw[2][GP];             // merged sums
+  __shared__ float s_mx[2][GP];             // merged maxima
+  __shared__ int s_nrec;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  int r, n, ur, um;
+  bool app;
+  rag_units(a, bh, r, n, ur, um, app);
+  const int U = a.plan[a.BH], NB = a.plan[a.BH + 1];
+  const int* blo = a.plan + a.BH + 2;  // block starts
+  const int P0 = a.plan[bh];
+  const int b0 = rag_block(P0, U, NB), b1 = rag_block(P0 + ur + um - 1, U, NB);
+  const bool shared = ur + um > 0 && b0 != b1;
+  constexpr int kRec = GP * (D + 2);  // floats per (block, edge, kind) record
+  if (shared) {
+    // the head's records: blocks with an empty range left none; the head's
+    // first block holds it as its last head unless the block starts with it
+    if (tid == 0) {
+      int c = 0;
+      for (int bb = b0; bb <= b1 && c < kRagMaxRec; ++bb)
+        if (blo[bb] < blo[bb + 1]) s_idx[c++] = bb * 2 + (blo[bb] >= P0 ? 0 : 1);
+      s_nrec = c;
+    }
+    __syncthreads();
+    const int nrec = s_nrec;
+    // every record's (max, sum) per kind and query head, loaded at once
+    for (int x = tid; x < nrec * 2 * GP; x += kThreads) {
+      const int i = x / (2 * GP), kind = (x / GP) % 2, h = x % GP;
+      const float* rc = a.rec + ((size_t)s_idx[i] * 2 + kind) * kRec;
+      s_w[i][kind][h] = rc[GP * D + h];
+      s_lr[i][kind][h] = rc[GP * D + GP + h];
+    }
+    __syncthreads();
+    if (tid < 2 * GP) {
+      const int kind = tid / GP, h = tid % GP;
+      float M = kNegInf;
+      for (int i = 0; i < nrec; ++i) M = fmaxf(M, s_w[i][kind][h]);
+      float L = 0.f;
+      for (int i = 0; i < nrec; ++i) {
+        const float w = M != kNegInf ? exp2f(s_w[i][kind][h] - M) : 0.f;
+        s_w[i][kind][h] = w;
+        L = fmaf(w, s_lr[i][kind][h], L);
+      }
+      s_mx[kind][h] = M;
+      s_lw[kind][h] = L;
+    }
+    __syncthreads();
+    const int b = bh / a.Hkv, kvh = bh - b * a.Hkv;
+    for (int idx = tid; idx < a.G * D; idx += kThreads) {
+      const int h = idx / D, d = idx % D;
+      float Ok[2] = {0.f, 0.f};
+#pragma unroll
+      for (int kind = 0; kind < 2; ++kind)
+        for (int i = 0; i < nrec; ++i)
+          Ok[kind] = fmaf(s_w[i][kind][h], a.rec[((size_t)s_idx[i] * 2 + kind) * kRec + h * D + d], Ok[kind]);
+      const int qh = b * a.Hq + kvh * a.G + h;
+      float gg;
+      const float Mm = s_mx[1][h], Lm = s_lw[1][h], Mr = s_mx[0][h], Lr = s_lw[0][h];
+      a.out[(size_t)qh * D + d] = rag_output(a, qh, Mm, Lm, Ok[1], Mr, Lr, Ok[0], gg);
+      if (d == 0) {
+        if (a.dbg_lse_main) a.dbg_lse_main[qh] = Lm > 0.f ? (Mm + log2f(Lm)) * kLn2 : kNegInf;
+        if (a.dbg_lse_res) a.dbg_lse_res[qh] = Lr > 0.f ? (Mr + log2f(Lr)) * kLn2 : kNegInf;
+        if (a.dbg_gate) a.dbg_gate[qh] = gg;
+      }
+    }
+  }
+  __syncthreads();  // every thread has read the lengths
+  if (app && tid == 0) a.main_len[bh] = n + 1;
+}
+
 template <typename T, int D>
 __global__ void append_kernel(const T* k_new, const T* v_new, T* kc, T* vc, const int32_t* res_len,
                               int32_t* main_len, int C) {
@@ -796,6 +1123,29 @@ hipError_t launch_typed(const DecodePlan& pl, const DecodeArgs& da, hipStream_t 
   return hipGetLastError();
 }
 
+template <typename T, int D, int GP>
+hipError_t launch_ragged_typed(const RaggedPlan& pl, const DecodeArgs& da, hipStream_t stream) {
+  if constexpr (GP <= 8 && (sizeof(T) == 2 || D == 64)) {
+    hipLaunchKernelGGL((decode_ragged<T, D, GP>), dim3(pl.blocks), dim3(kHeadThreads), 0, stream, da);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((decode_ragged_combine<D, GP>), dim3(pl.BH), dim3(kThreads), 0, stream, da);
+    return hipGetLastError();
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int D>
+hipError_t launch_ragged_gp(const RaggedPlan& pl, const DecodeArgs& da, hipStream_t stream) {
+  switch (pl.GP) {
+    case 1: return launch_ragged_typed<T, D, 1>(pl, da, stream);
+    case 2: return launch_ragged_typed<T, D, 2>(pl, da, stream);
+    case 4: return launch_ragged_typed<T, D, 4>(pl, da, stream);
+    case 8: return launch_ragged_typed<T, D, 8>(pl, da, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <typename T, int D>
 hipError_t launch_gp(const DecodePlan& pl, const DecodeArgs& da, hipStream_t stream) {
   switch (pl.GP) {
@@ -830,6 +1180,57 @@ DecodePlan make_decode_plan(const reskv_shape_t& s) {
 }
 
 size_t decode_max_lds_weights() { return 48 * 1024; }
+
+bool make_ragged_plan(const reskv_shape_t& s, RaggedPlan* plan) {
+  RaggedPlan& p = *plan;
+  p = RaggedPlan{};
+  p.BH = s.batch * s.num_kv_heads;
+  const int G = s.num_q_heads / s.num_kv_heads;
+  p.GP = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : G <= 8 ? 8 : 16;
+  if (p.GP > 8 || p.BH > kRagMaxHeads) return false;
+  if (!(s.dtype == RESKV_BF16 || s.head_dim == 64)) return false;
+  // a head holds at most ceil(r / 64) + ceil((C - r) / 64) <= ceil(C / 64) + 1
+  // units; blocks of at least min_units units keep a head within kRagMaxRec
+  // blocks, and min_units <= kRagUnits / 2 keeps every block within
+  // kRagUnits units when the block count is cut to U / min_units
+  const int uhead = (s.slot_cap + kUnit - 1) / kUnit + 1;
+  p.min_units = (uhead + kRagMaxRec - 2) / (kRagMaxRec - 1);
+  if (p.min_units > kRagUnits / 2) return false;
+  const long long umax = (long long)p.BH * uhead;
+  const long long nb = (umax + kRagUnits - 1) / kRagUnits;
+  p.blocks = (int)(nb > kRagMinBlocks ? nb : kRagMinBlocks);
+  p.plan_off = 0;
+  p.rec_off = align_up((size_t)(p.BH + 3 + p.blocks) * sizeof(int32_t), 256);
+  p.bytes = p.rec_off + align_up((size_t)p.blocks * 4 * p.GP * (s.head_dim + 2) * sizeof(float), 256);
+  return true;
+}
+
+hipError_t launch_decode_ragged(const reskv_shape_t& s, const reskv_gate_t& g, const RaggedPlan& pl,
+                                const void* q, void* kc, void* vc, const float* logc, const int32_t* res_len,
+                                int32_t* main_len, const void* k_new, const void* v_new, float* out,
+                                float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate, void* workspace,
+                                hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  DecodeArgs da{};
+  da.k_new = k_new; da.v_new = v_new;
+  da.q = q; da.kc = kc; da.vc = vc; da.logc = logc;
+  da.res_len = res_len; da.main_len = main_len;
+  da.plan = reinterpret_cast<int32_t*>(ws + pl.plan_off);
+  da.rec = reinterpret_cast<float*>(ws + pl.rec_off);
+  da.tau = g.tau; da.out = out;
+  da.dbg_lse_main = dbg_lse_main; da.dbg_lse_res = dbg_lse_res; da.dbg_gate = dbg_gate;
+  da.Hq = s.num_q_heads; da.Hkv = s.num_kv_heads; da.G = s.num_q_heads / s.num_kv_heads;
+  da.C = s.slot_cap; da.Rcap = s.res_cap; da.BH = pl.BH; da.rag_blocks = kRagMinBlocks;
+  da.rag_min_units = pl.min_units;
+  da.qk_scale = kLog2e / sqrtf((float)s.head_dim);
+  da.beta_log2 = g.beta * kLog2e;
+  da.tau_scalar = g.tau_scalar; da.alpha = g.alpha; da.g_min = g.g_min;
+  const bool bf = s.dtype == RESKV_BF16;
+  if (s.head_dim == 128) return bf ? launch_ragged_gp<uint16_t, 128>(pl, da, stream) : hipErrorInvalidValue;
+  if (s.head_dim == 64)
+    return bf ? launch_ragged_gp<uint16_t, 64>(pl, da, stream) : launch_ragged_gp<float, 64>(pl, da, stream);
+  return hipErrorInvalidValue;
+}
 
 hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& pl,
                          const void* q, void* kc, void* vc, const float* logc,

@@ -28,6 +28,19 @@ hipError_t static_scratch(void** ptr);
 
 DecodePlan make_decode_plan(const reskv_shape_t& s);
 
+// Ragged schedule: balanced ranges of 64-slot units over the whole batch.
+struct RaggedPlan {
+  int BH, GP, blocks;  // blocks launched (enough for any lengths the capacity allows)
+  int min_units;       // units per block at least (a head spans at most 64 blocks)
+  size_t plan_off, rec_off, bytes;
+};
+bool make_ragged_plan(const reskv_shape_t& s, RaggedPlan* plan);
+hipError_t launch_decode_ragged(const reskv_shape_t& s, const reskv_gate_t& g, const RaggedPlan& pl,
+                                const void* q, void* kc, void* vc, const float* logc, const int32_t* res_len,
+                                int32_t* main_len, const void* k_new, const void* v_new, float* out,
+                                float* dbg_lse_main, float* dbg_lse_res, float* dbg_gate, void* workspace,
+                                hipStream_t stream);
+
 hipError_t launch_decode(const reskv_shape_t& s, const reskv_gate_t& g, const DecodePlan& plan,
                          const void* q, void* kc, void* vc, const float* logc,
                          const int32_t* res_len, int32_t* main_len, const void* k_new, const void* v_new,

@@ -71,6 +71,9 @@ _SIG = {
     "reskv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
                                          _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "reskv_decode_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape)]),
+    "reskv_decode_attn_ragged": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P,
+                                                _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "reskv_decode_ragged_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(Shape)]),
     "reskv_decode_attn_static": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P,
                                                 _P, _P, _P, _P, _P, _P, _P, _P]),
     "reskv_decode_branches": (ctypes.c_int, [ctypes.POINTER(Shape), ctypes.POINTER(Gate), _P, _P, _P, _P, _P, _P,
@@ -209,6 +212,38 @@ def reskv_decode_attn(shape, gate, q, kc, vc, logc, res_len, main_len, out, work
                                    _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(k_new), _ptr(v_new), _ptr(out),
                                    _ptr(dbg_lse_main), _ptr(dbg_lse_res), _ptr(dbg_gate), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def reskv_decode_ragged_workspace_size(shape):
+    return lib().reskv_decode_ragged_workspace_size(ctypes.byref(shape))
+
+
+def reskv_decode_attn_ragged(shape, gate, q, kc, vc, logc, res_len, main_len, out, workspace, dbg_lse_main=None,
+                             dbg_lse_res=None, dbg_gate=None, k_new=None, v_new=None, stream=None):
+    _check(lib().reskv_decode_attn_ragged(ctypes.byref(shape), ctypes.byref(gate), _ptr(q), _ptr(kc), _ptr(vc),
+                                          _ptr(logc), _ptr(res_len), _ptr(main_len), _ptr(k_new), _ptr(v_new),
+                                          _ptr(out), _ptr(dbg_lse_main), _ptr(dbg_lse_res), _ptr(dbg_gate),
+                                          _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                          _stream(stream)))
+
+
+def prepare_decode_attn_ragged(shape, gate, q, kc, vc, logc, res_len, main_len, out, workspace,
+                               dbg_lse_main=None, dbg_lse_res=None, dbg_gate=None, k_new=None, v_new=None,
+                               stream=None):
+    """As prepare_decode_attn, for reskv_decode_attn_ragged."""
+    fn = lib().reskv_decode_attn_ragged
+    args = (ctypes.byref(shape), ctypes.byref(gate), _ptr(q), _ptr(kc), _ptr(vc), _ptr(logc), _ptr(res_len),
+            _ptr(main_len), _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(dbg_lse_main), _ptr(dbg_lse_res),
+            _ptr(dbg_gate), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    keep = (shape, gate)
+
+    def call():
+        status = fn(*args)
+        if status != 0:
+            _check(status)
+
+    call.keep = keep
+    return call
 
 
 def reskv_decode_attn_static(shape, gate, q, kc, vc, logc, res_len, main_len, out, dbg_lse_main=None,
