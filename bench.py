@@ -106,11 +106,17 @@ def source_hash(*paths):
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(src_hash):
+# Committed rocprofv3 summaries per workload (profiles/<name>.json).
+PROFILES = {2: {"decode": "decode_head_batched_decode_traffic", "construction": "construction_batched_decode_counters"},
+            3: {"construction": "construction_long_context_counters"},
+            4: {"decode": "decode_head_ragged_gqa7_traffic"}}
+
+
+def traffic_from_profile(src_hash, name=PROFILES[2]["decode"]):
     """Measured / algorithmic HBM bytes of the decode calls profiled with
     rocprofv3 counters, if that measurement was taken on the current decode
     source."""
-    path = os.path.join(ROOT, "profiles", "decode_traffic.json")
+    path = os.path.join(ROOT, "profiles", name + ".json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -120,22 +126,13 @@ def traffic_from_profile(src_hash):
     return rec.get("bytes_per_call") / rec.get("algorithmic_bytes_per_call")
 
 
-def construction_mfma_from_profile(src_hash):
+def construction_mfma_from_profile(src_hash, name=PROFILES[2]["construction"]):
     """MFMA use of the construction's MFMA kernels from the committed
-    rocprofv3 counters (busy percent, executed and algorithmic TFLOP/s, and
-    algorithmic flops over the 2.5 PF/s peak), if the measurement was taken on
-    the current construction source."""
-    path = os.path.join(ROOT, "profiles", "construction_counters.json")
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        rec = json.load(f)
-    if rec.get("build_source_sha256_16") != src_hash:
-        return None
-    ks = rec["kernels"]
-    return {k: {"mfma_busy_pct": round(ks[k]["mfma_util_pct"], 1), "executed_tflops": round(ks[k]["mfma_tflops"]),
-                "algorithmic_tflops": round(ks[k]["alg_tflops"]), "algorithmic_util_pct": round(ks[k]["alg_util_pct"], 1)}
-            for k in ("lse_partial", "score_accum", "lloyd_assign_r1", "lloyd_assign") if k in ks}
+    rocprofv3 counters (kernel time, busy percent, executed and algorithmic
+    TFLOP/s, and algorithmic flops over the 2.5 PF/s peak), if the
+    measurement was taken on the current construction source."""
+    rec = counters_from_profile(name, src_hash)
+    return rec["summary"] if rec is not None else None
 
 
 # Validation proxy settings of App. B.3: grid of budget fractions, 8 of the 32
@@ -753,13 +750,18 @@ def main():
         torch.cuda.empty_cache()
         bsrc = source_hash("paper_2607_29591_amd/csrc/build.hip", "paper_2607_29591_amd/csrc/common.h")
         per = {}
+        dsrc = source_hash("paper_2607_29591_amd/csrc/decode.hip", "paper_2607_29591_amd/csrc/common.h")
         for idx in others:
             # the ragged GQA-7 batch (budgets and contexts differ per sequence)
-            # decodes with the balanced-range schedule
+            # also decodes with the balanced-range schedule, reported beside
             wl_i, rec = per_config_run(rk, torch, np, synth, idx, dev, args.per_config_reps, ragged=idx == 4)
-            prof = counters_from_profile(f"{wl_i.name}_construction_counters", bsrc)
-            if prof is not None:
-                rec["construction_mfma"] = prof["summary"]
+            names = PROFILES.get(idx, {})
+            if "construction" in names:
+                rec["construction_mfma"] = construction_mfma_from_profile(bsrc, names["construction"])
+            if "decode" in names:
+                ratio = traffic_from_profile(dsrc, names["decode"])
+                rec["decode_roofline"]["traffic"] = (ratio * rec["decode_bytes_per_call"]
+                                                     if ratio is not None else None)
             per[wl_i.name] = rec
         result["per_config"] = per
     print(json.dumps(result), flush=True)
