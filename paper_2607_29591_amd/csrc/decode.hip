@@ -612,6 +612,15 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   load_unit_k<T, D>(ur0, kc, kUnit * wave, a.C - 1, hd, g, -1, nullptr);
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
+  // the per-query tau of the outputs this thread finishes, requested now so
+  // that the epilogue does not wait on a global load
+  constexpr int kPer = (GP * D + kHeadThreads - 1) / kHeadThreads;
+  float tau_q[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int h = min((tid + k * kHeadThreads) / D, a.G - 1);
+    tau_q[k] = a.tau ? a.tau[(size_t)b * a.Hq + (size_t)kvh * a.G + h] : a.tau_scalar;
+  }
 
   // fused append of this step's token as main slot r + n (Sec. 3.1): this
   // call reads it from k_new / v_new, and the wave whose unit holds it
@@ -707,7 +716,6 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
 
   // merge the waves' states of one kind for the outputs this thread owns:
   // max, sum and accumulator of (head h, column d) over the 8 waves
-  constexpr int kPer = (GP * D + kHeadThreads - 1) / kHeadThreads;
   auto merge = [&](int kind, int idx, float& M, float& l, float& o) {
     const int h = idx / D, d = idx % D;
     const int buf = kBufs == 2 ? kind : 0;
@@ -748,8 +756,7 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
     // p_max = 1 / l_main (the max term is exactly 1), then the gate
     const float pmax = l > 0.f ? 1.f / l : 1.f;
     const int qh = b * a.Hq + kvh * a.G + h;
-    const float tau = a.tau ? a.tau[qh] : a.tau_scalar;
-    const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau - pmax) * a.alpha)));
+    const float g = fmaxf(a.g_min, 1.f / (1.f + expf(-(tau_q[k] - pmax) * a.alpha)));
     const float lg2g = g > 0.f ? log2f(g) : kNegInf;
     const float mRg = (mR[k] == kNegInf || lg2g == kNegInf) ? kNegInf : mR[k] + lg2g;
     const float Mx = fmaxf(M, mRg);
