@@ -50,7 +50,10 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kKeyGroups = 4;     // 256-key groups per score-pass block, one after the other
 constexpr int kKeyChunk = 256 * kKeyGroups;  // keys per score-pass block
-constexpr int kRowChunk = 128;     // window rows staged in LDS per scoring step
+// window rows staged in LDS per scoring step: 128, or 256 when there are
+// more than 128 (each key group is then loaded once for all of them)
+constexpr int kRowChunk = 128;
+constexpr int kRowChunkWide = 256;
 // s_waitcnt immediate: vector-memory count 0, export and LDS/scalar counts
 // left at their maximum (no wait on them)
 constexpr int kWaitVmcnt0 = 0x0F70;
@@ -137,7 +140,9 @@ __device__ __forceinline__ void stage_window_rows(unsigned char* s_q, const Buil
 // Scoring blocks stream groups of 256 keys one after the other (the lse pass
 // 4, 8 or 16 groups per block as the plan chooses, the score pass 4); in each
 // group a wave owns 64 keys and runs over every window row. The window rows
-// are staged in LDS once per block (128 at a time).
+// are staged in LDS once per block, RC at a time: every row chunk loads the
+// block's keys again, so with more than 128 rows (G w = 224, 256) the wide
+// chunk of 256 rows reads each key once per pass, at two blocks per CU.
 
 // Key fragments of the 64 keys from kw (clamped to the sequence).
 template <typename T, int D>
@@ -151,8 +156,8 @@ __device__ __forceinline__ void load_score_keys(Frag<T, D> (&f)[4], const T* K, 
 // Each wave keeps a running (max, sum) per row over its key groups. A wave
 // holds one 64-key group at a time (no second key buffer): at three waves
 // per SIMD (bf16) the other blocks on the CU cover its load latency.
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 3 : 2)) void lse_partial(BuildArgs a) {
+template <typename T, int D, int RC>
+__global__ __launch_bounds__(kThreads, (RC > kRowChunk ? 2 : sizeof(T) == 2 ? 3 : 2)) void lse_partial(BuildArgs a) {
   const int ch = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
@@ -161,11 +166,11 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 3 : 2)) void lse_partia
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   constexpr int kQRowB = D * (int)sizeof(T) + 16;
-  __shared__ __align__(16) unsigned char s_q[kRowChunk * kQRowB];
-  __shared__ float2 s_ml[4][kRowChunk];
+  __shared__ __align__(16) unsigned char s_q[RC * kQRowB];
+  __shared__ float2 s_ml[4][RC];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
-  for (int r0 = 0; r0 < a.R; r0 += kRowChunk) {
-    const int nrt = (min(kRowChunk, a.R - r0) + 15) / 16;
+  for (int r0 = 0; r0 < a.R; r0 += RC) {
+    const int nrt = (min(RC, a.R - r0) + 15) / 16;
     if (r0 > 0) __syncthreads();  // the previous chunk's rows and records are consumed
     Frag<T, D> kf[4];
     load_score_keys<T, D>(kf, K, k0 + 64 * wave, hm.s, col, grp);
@@ -226,7 +231,7 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 3 : 2)) void lse_partia
 
     }
     __syncthreads();
-    for (int t = threadIdx.x; t < min(kRowChunk, a.R - r0); t += kThreads) {
+    for (int t = threadIdx.x; t < min(RC, a.R - r0); t += kThreads) {
       float M = kNegInf;
 #pragma unroll
       for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][t].x);
@@ -265,8 +270,8 @@ __global__ __launch_bounds__(kThreads) void lse_final(BuildArgs a) {
 // sums stay in registers until two final cross-lane steps, and no cross-wave
 // merge is needed. One key group per wave at a time and a rolled row-tile
 // loop keep it at four waves per SIMD (bf16).
-template <typename T, int D>
-__global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 4 : 2)) void score_accum(BuildArgs a, int rev) {
+template <typename T, int D, int RC>
+__global__ __launch_bounds__(kThreads, (RC > kRowChunk ? 2 : sizeof(T) == 2 ? 4 : 2)) void score_accum(BuildArgs a, int rev) {
   const int ch = blockIdx.x;
   int b, kvh, bh;
   block_head(a, rev, b, kvh, bh);
@@ -276,12 +281,12 @@ __global__ __launch_bounds__(kThreads, (sizeof(T) == 2 ? 4 : 2)) void score_accu
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   constexpr int kQRowB = D * (int)sizeof(T) + 16;
-  constexpr int kRT = kRowChunk / 16;
-  __shared__ __align__(16) unsigned char s_q[kRowChunk * kQRowB];
-  __shared__ float s_lse[kRowChunk];
+  constexpr int kRT = RC / 16;
+  __shared__ __align__(16) unsigned char s_q[RC * kQRowB];
+  __shared__ float s_lse[RC];
   const T* K = static_cast<const T*>(a.k) + (size_t)bh * a.S * D;
-  for (int r0 = 0; r0 < a.R; r0 += kRowChunk) {
-    const int nr = min(kRowChunk, a.R - r0), nrt = (nr + 15) / 16;
+  for (int r0 = 0; r0 < a.R; r0 += RC) {
+    const int nr = min(RC, a.R - r0), nrt = (nr + 15) / 16;
     if (r0 > 0) __syncthreads();  // the previous chunk's rows are consumed
     Frag<T, D> kf[4];
     load_score_keys<T, D>(kf, K, k0 + 64 * wave, hm.s, col, grp);
@@ -1416,10 +1421,16 @@ template <typename T, int D>
 hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
   auto grid = [&](int x) { return dim3(x < 1 ? 1 : x, pl.Hkv, pl.B); };
   hipError_t e;
-  hipLaunchKernelGGL((lse_partial<T, D>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  // the wide chunk at bf16 rows (fp32 rows of 128 would hold one block per CU)
+  const bool wide = pl.R > kRowChunk && (sizeof(T) == 2 || D == 64);
+  if (wide) hipLaunchKernelGGL((lse_partial<T, D, kRowChunkWide>), grid(pl.NCH), dim3(kThreads), 0, st, a);
+  else hipLaunchKernelGGL((lse_partial<T, D, kRowChunk>), grid(pl.NCH), dim3(kThreads), 0, st, a);
+  RESKV_CHECK();
   hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
   // the second pass over the keys walks the heads in reverse (cache reuse)
-  hipLaunchKernelGGL((score_accum<T, D>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1); RESKV_CHECK();
+  if (wide) hipLaunchKernelGGL((score_accum<T, D, kRowChunkWide>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1);
+  else hipLaunchKernelGGL((score_accum<T, D, kRowChunk>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1);
+  RESKV_CHECK();
   return hipSuccess;
 }
 

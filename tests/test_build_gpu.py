@@ -102,6 +102,20 @@ def test_build_many_groups(s, budget, res, iters):
         check_head(wl, x, got, 0, h, iters=iters)
 
 
+@pytest.mark.parametrize("dtype,d,hq,hkv,window", [("bf16", 128, 16, 2, 20), ("bf16", 64, 16, 1, 24),
+                                                  ("f32", 64, 8, 1, 40), ("f32", 128, 8, 2, 40)])
+def test_build_many_window_rows(dtype, d, hq, hkv, window):
+    """More than 128 window rows (G w = 160, 384, 320, 160): the scoring
+    passes stage the rows in one or two 256-row chunks (bf16, fp32 at d 64)
+    or in 128-row chunks (fp32 at d 128), with a partial last chunk."""
+    res = (48, 16)[:hkv]
+    wl, x = small(41, dtype=dtype, d=d, s=1500, hq=hq, hkv=hkv, budget=200, res=res, window=window, n_heavy=6)
+    assert wl.group * window > 128
+    got = run_build(wl, x)
+    for h in range(wl.hkv):
+        check_head(wl, x, got, 0, h)
+
+
 def test_build_is_deterministic():
     wl, x = small(4, dtype="bf16", d=128, s=2000, budget=256, res=(64, 32), window=16)
     a = run_build(wl, x)
