@@ -1197,6 +1197,12 @@ __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
 // CU) keeps more of a long group's rows in flight and finishes sooner.
 // kKV (last round, bf16): each member's key and value rows are read in the
 // same loop, twice the rows in flight of two passes one after the other.
+// Member indices q, q + NG, q + 2NG, q + 3NG of a group's sorted list.
+__device__ __forceinline__ void load_ids(int (&id)[4], const int32_t* mem, int q, int NG) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) id[u] = mem[q + u * NG];
+}
+
 template <typename T, int D, bool kPacked, bool kKV = false>
 __global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && sizeof(T) == 2 ? 8 : 4)) void lloyd_update(BuildArgs a, int last, int rev) {
   const int j = blockIdx.x;
@@ -1230,14 +1236,17 @@ __global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && s
       }
     };
     int q = g;
+    int id[4];
+    if (q + 3 * NG < cnt) load_ids(id, mem, q, NG);
     for (; q + 3 * NG < cnt; q += 4 * NG) {
       uint4 wk[4], wv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const size_t off = (size_t)mem[q + u * NG] * D + 8 * c;
+        const size_t off = (size_t)id[u] * D + 8 * c;
         wk[u] = *reinterpret_cast<const uint4*>(K + off);
         wv[u] = *reinterpret_cast<const uint4*>(V + off);
       }
+      if (q + 7 * NG < cnt) load_ids(id, mem, q + 4 * NG, NG);  // the next rows' indices
 #pragma unroll
       for (int u = 0; u < 4; ++u) add8(ak, wk[u]);
 #pragma unroll
@@ -1276,10 +1285,15 @@ __global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && s
     double acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-    // members g, g + NG, g + 2NG, ... in order; four 16-byte row loads in flight
+    // members g, g + NG, g + 2NG, ... in order; four 16-byte row loads in
+    // flight, and (wider variant) the next four members' indices requested
+    // behind them; the packed variant has no registers to spare for them
+    constexpr bool kPacked16 = kPacked && sizeof(T) == 2;
     int q = g;
+    int id[4];
+    if (!kPacked16 && q + 3 * NG < cnt) load_ids(id, mem, q, NG);
     for (; q + 3 * NG < cnt; q += 4 * NG) {
-      if constexpr (kPacked && sizeof(T) == 2) {  // rows stay packed until added: 4 registers each
+      if constexpr (kPacked16) {  // rows stay packed until added: 4 registers each
         uint4 w[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) w[u] = *reinterpret_cast<const uint4*>(X + (size_t)mem[q + u * NG] * D + 8 * c);
@@ -1295,7 +1309,8 @@ __global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && s
       } else {
         float x[4][8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) load8_f32(X + (size_t)mem[q + u * NG] * D + 8 * c, x[u]);
+        for (int u = 0; u < 4; ++u) load8_f32(X + (size_t)id[u] * D + 8 * c, x[u]);
+        if (q + 7 * NG < cnt) load_ids(id, mem, q + 4 * NG, NG);
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
