@@ -441,6 +441,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
   int krem[2] = {kk[0], kk[1]};
   const int wave = tid >> 6, lane = tid & 63;
   for (int shift = 24; shift >= 0; shift -= 8) {
+    // while both thresholds share their prefix (always in the first pass, and
+    // as long as they take the same digits) one histogram serves both
+    const bool shared = krem[0] > 0 && krem[1] > 0 && prefix[0] == prefix[1];  // block-uniform
     for (int i = tid; i < 512; i += kSelThreads) (&s_hist[0][0])[i] = 0;
     __syncthreads();
     // coalesced, kHistBatch keys in flight per thread
@@ -453,9 +456,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
       for (int v = 0; v < kHistBatch; ++v) {
         const int dig = (u[v] >> shift) & 0xff;
         const bool in = i0 + v * kSelThreads < n;
-#pragma unroll
-        for (int q = 0; q < 2; ++q)
-          wave_hist_add(s_hist[q], dig, in && krem[q] > 0 && (u[v] & mask) == prefix[q], lane);
+        wave_hist_add(s_hist[0], dig, in && krem[0] > 0 && (u[v] & mask) == prefix[0], lane);
+        if (!shared) wave_hist_add(s_hist[1], dig, in && krem[1] > 0 && (u[v] & mask) == prefix[1], lane);
       }
     }
     __syncthreads();
@@ -463,11 +465,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
     // descending digit order; an inclusive scan over lanes gives the count of
     // keys at or above each digit
     if (wave < 2) {
-      const int q = wave;
+      const int q = wave, hq = shared ? 0 : q;
       if (krem[q] > 0) {
         int c[4], own = 0;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) { c[v] = s_hist[q][255 - 4 * lane - v]; own += c[v]; }
+        for (int v = 0; v < 4; ++v) { c[v] = s_hist[hq][255 - 4 * lane - v]; own += c[v]; }
         int incl = own;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
@@ -485,7 +487,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
         const unsigned long long hit = __ballot(hit_d >= 0);
         const int src = hit ? __ffsll((long long)hit) - 1 : 63;
         int d = __shfl(hit_d, src, 64), acc = __shfl(hit_acc, src, 64);
-        if (!hit) { d = 0; acc = __shfl(incl, 63, 64) - s_hist[q][0]; }
+        if (!hit) { d = 0; acc = __shfl(incl, 63, 64) - s_hist[hq][0]; }
         if (lane == 0) {
           s_pref[q] = prefix[q] | ((uint32_t)d << shift);
           s_krem[q] = krem[q] - acc;
