@@ -15,11 +15,12 @@
 //                  between the KV heads of a sequence (one ranking of all
 //                  heads' scores, per-head safeguard floor and slot cap) and
 //                  rewrites each head's sizes before the selection
-//   select         radix select (4 x 8-bit digits of the fp32 bit pattern) of
-//                  the k_top-th and (k_top + r')-th largest score; ties at a
-//                  threshold go to the lower position. Stable compaction writes
-//                  main_idx (top-k, then the protected window), the evicted
-//                  list E and the Lloyd seeds, all ascending
+//   select_hist x4 radix select (4 x 8-bit digits of the fp32 bit pattern) of
+//   select_count   the k_top-th and (k_top + r')-th largest score over blocks
+//   select_write   of 8192 scores; ties at a threshold go to the lower
+//                  position. Stable compaction writes main_idx (top-k, then
+//                  the protected window), the evicted list E and the Lloyd
+//                  seeds, all ascending
 //   gather_init    copies the main rows into slots [r, r + m), clears the
 //                  residual slots, seeds the Lloyd centres with K[seed] (fp32,
 //                  bf16 hi + lo and the squared norm)
@@ -59,6 +60,9 @@ constexpr int kRowChunkWide = 256;
 constexpr int kWaitVmcnt0 = 0x0F70;
 constexpr int kTokBlock = 256;     // evicted tokens per counting-sort block (histograms, scatter)
 constexpr int kSelThreads = 1024;
+constexpr int kSelPer = 8;                          // scores per selection thread
+constexpr int kSelChunk = kSelPer * kSelThreads;   // scores per selection block
+constexpr int kSelHist = 4 * 2 * 256;              // selection pass histograms per head: [pass][threshold][digit]
 constexpr int kAdaThreads = 1024;
 
 struct BuildArgs {
@@ -90,7 +94,9 @@ struct BuildArgs {
   int32_t* cstart;     // [BH][Rcap]
   int32_t* ccount;     // [BH][Rcap]
   int32_t* order;      // [BH][S]   evicted positions grouped by centre
-  int B, Hq, Hkv, G, C, Rcap, S, w, R, LG, NCH, NBLK, T;
+  int32_t* sel_hist;   // [BH][4][2][256] selection pass histograms (zeroed by pool_scores)
+  int32_t* sel_cnt;    // [BH][NSEL][4] per selection block: above / equal to each threshold
+  int B, Hq, Hkv, G, C, Rcap, S, w, R, LG, NCH, NBLK, NSEL, T;
   int wr;              // leading window rows per query head that score (R = G * wr)
   int pool_half;       // pooling taps on each side of a position
   int cap_slots;       // slots a head may fill at construction (C minus the decode reserve)
@@ -356,6 +362,8 @@ __global__ __launch_bounds__(kThreads) void pool_scores(BuildArgs a) {
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
+  if (blockIdx.x == 0)  // the selection's pass histograms start from zero
+    for (int i = threadIdx.x; i < kSelHist; i += kThreads) a.sel_hist[(size_t)bh * kSelHist + i] = 0;
   const int p = blockIdx.x * kThreads + threadIdx.x;
   if (p >= a.S) return;
   const int n = hm.all_main ? 0 : hm.n_sc;
@@ -415,194 +423,300 @@ __device__ __forceinline__ void wave_hist_add(int* hist, int dig, bool act, int 
   if (act) atomicAdd(&hist[dig], 1);
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(BuildArgs a) {
-  const int kvh = blockIdx.y, b = blockIdx.z;
-  const int bh = b * a.Hkv + kvh;
+// Selection runs over blocks of kSelChunk consecutive scores per head, so a
+// head's long score list is spread over many CUs: four radix passes (8-bit
+// digits, most significant first) each add the block's digit histogram of
+// the scores still matching a threshold's prefix into the head's pass
+// histogram; every block of the next kernel replays the digit choices from
+// the completed histograms. Then the blocks count the scores above and equal
+// to each threshold, and finally each block places its scores: the earlier
+// blocks' counts give its output offsets and the tie ranks of its equal
+// scores (ties are taken lowest position first).
+
+// Digit of one threshold in one radix pass from its 256-bin histogram h of
+// the scores matching its prefix, krem = its rank among them: the digit d and
+// the count of scores in higher digits. Run by a whole wave (every lane gets
+// the values).
+__device__ __forceinline__ void radix_digit(const int* h, int krem, int lane, int& d, int& above) {
+  // each lane holds 4 bins in descending digit order; an inclusive scan over
+  // lanes gives the count of scores at or above each digit
+  int c[4], own = 0;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) { c[v] = h[255 - 4 * lane - v]; own += c[v]; }
+  int incl = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  int run = incl - own;  // scores above this lane's first digit
+  int hit_d = -1, hit_acc = 0;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    if (hit_d < 0 && run + c[v] >= krem) { hit_d = 255 - 4 * lane - v; hit_acc = run; }
+    run += c[v];
+  }
+  // the first lane (highest digits) that reaches krem owns the digit
+  const unsigned long long hit = __ballot(hit_d >= 0);
+  const int src = hit ? __ffsll((long long)hit) - 1 : 63;
+  d = __shfl(hit_d, src, 64);
+  above = __shfl(hit_acc, src, 64);
+  if (!hit) { d = 0; above = __shfl(incl, 63, 64) - h[0]; }
+}
+
+// Prefixes and remaining ranks of both thresholds (k1-th and k2-th largest)
+// after radix passes [0, npass), from the head's completed pass histograms
+// gh; while the two share their prefix one histogram (threshold 0's) served
+// both. Run by a whole wave.
+__device__ __forceinline__ void radix_replay(const int* gh, int npass, int k1, int k2, int lane, uint32_t (&pref)[2],
+                                             int (&krem)[2]) {
+  pref[0] = pref[1] = 0u;
+  krem[0] = k1;
+  krem[1] = k2;
+  for (int p = 0; p < npass; ++p) {
+    const int shift = 24 - 8 * p;
+    const bool shared = krem[0] > 0 && krem[1] > 0 && pref[0] == pref[1];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (krem[q] > 0) {  // wave-uniform
+        int d, above;
+        radix_digit(gh + (p * 2 + (shared ? 0 : q)) * 256, krem[q], lane, d, above);
+        pref[q] |= (uint32_t)d << shift;
+        krem[q] -= above;
+      }
+    }
+  }
+}
+
+// Setup shared by the selection kernels: the head, its chunk and the
+// threshold state after `npass` radix passes (replayed by wave 0, then read
+// by every thread). Returns false where the block has nothing to do.
+struct SelState {
+  int bh, n, i0;
+  int k1, k2;
+  uint32_t pref[2];
+  int krem[2];
+};
+__device__ __forceinline__ void sel_state(const BuildArgs& a, const HeadMeta& hm, int bh, int npass, SelState& st,
+                                          int* s_gh, uint32_t* s_pref, int* s_krem) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  st.bh = bh;
+  st.n = hm.n_sc;
+  st.i0 = blockIdx.x * kSelChunk;
+  st.k1 = hm.k_top;
+  st.k2 = hm.k_top + hm.r_eff;
+  // the completed pass histograms into LDS in one round trip, then replayed
+  const int* gh = a.sel_hist + (size_t)bh * kSelHist;
+  for (int x = threadIdx.x; x < npass * 512; x += blockDim.x) s_gh[x] = gh[x];
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t pf[2];
+    int kr[2];
+    radix_replay(s_gh, npass, st.k1, st.k2, lane, pf, kr);
+    if (lane == 0) {
+      s_pref[0] = pf[0]; s_pref[1] = pf[1];
+      s_krem[0] = kr[0]; s_krem[1] = kr[1];
+    }
+  }
+  __syncthreads();
+  st.pref[0] = s_pref[0]; st.pref[1] = s_pref[1];
+  st.krem[0] = s_krem[0]; st.krem[1] = s_krem[1];
+}
+
+// Radix pass `pass` over one block's scores: digit histograms of the scores
+// matching each threshold's prefix, added into the head's pass histogram
+// (zeroed by pool_scores).
+__global__ __launch_bounds__(kSelThreads) void select_hist(BuildArgs a, int pass) {
+  const int bh = blockIdx.z * a.Hkv + blockIdx.y;
   const HeadMeta hm = a.meta[bh];
+  if (hm.all_main || (int)blockIdx.x * kSelChunk >= hm.n_sc) return;  // block-uniform
+  __shared__ int s_hist[2][256];
+  __shared__ int s_gh[kSelHist];
+  __shared__ uint32_t s_pref[2];
+  __shared__ int s_krem[2];
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int i = tid; i < 512; i += kSelThreads) (&s_hist[0][0])[i] = 0;
+  SelState st;
+  sel_state(a, hm, bh, pass, st, s_gh, s_pref, s_krem);  // synchronises the block
+  if (st.krem[0] <= 0 && st.krem[1] <= 0) return;  // block-uniform
+  const bool shared = st.krem[0] > 0 && st.krem[1] > 0 && st.pref[0] == st.pref[1];
+  const int shift = 24 - 8 * pass;
+  const uint32_t mask = pass == 0 ? 0u : ~0u << (32 - 8 * pass);
+  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.score + (size_t)bh * a.S);
+  uint32_t u[kSelPer];
+#pragma unroll
+  for (int v = 0; v < kSelPer; ++v) {  // coalesced, all loads in flight together
+    const int i = st.i0 + v * kSelThreads + tid;
+    u[v] = i < st.n ? key[i] : 0u;
+  }
+#pragma unroll
+  for (int v = 0; v < kSelPer; ++v) {
+    const bool in = st.i0 + v * kSelThreads + tid < st.n;
+    const int dig = (u[v] >> shift) & 0xff;
+    wave_hist_add(s_hist[0], dig, in && st.krem[0] > 0 && (u[v] & mask) == st.pref[0], lane);
+    if (!shared) wave_hist_add(s_hist[1], dig, in && st.krem[1] > 0 && (u[v] & mask) == st.pref[1], lane);
+  }
+  __syncthreads();
+  int* gh = a.sel_hist + (size_t)bh * kSelHist + pass * 512;
+  for (int x = tid; x < 512; x += kSelThreads) {
+    const int c = (&s_hist[0][0])[x];
+    if (c) atomicAdd(&gh[x], c);
+  }
+}
+
+// Thresholds T_q = the final prefixes; krem[q] = how many scores equal to
+// T_q are taken (lowest positions first); a threshold with k = 0 takes none.
+// Per block: scores above and equal to each threshold.
+__global__ __launch_bounds__(kSelThreads) void select_count(BuildArgs a) {
+  const int bh = blockIdx.z * a.Hkv + blockIdx.y;
+  const HeadMeta hm = a.meta[bh];
+  if (hm.all_main || (int)blockIdx.x * kSelChunk >= hm.n_sc) return;  // block-uniform
+  __shared__ int s_gh[kSelHist];
+  __shared__ uint32_t s_pref[2];
+  __shared__ int s_krem[2];
+  SelState st;
+  sel_state(a, hm, bh, 4, st, s_gh, s_pref, s_krem);
   const int tid = threadIdx.x;
+  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.score + (size_t)bh * a.S);
+  int c[4] = {0, 0, 0, 0};  // above T1, equal T1, above T2, equal T2
+#pragma unroll
+  for (int v = 0; v < kSelPer; ++v) {
+    const int i = st.i0 + v * kSelThreads + tid;
+    if (i < st.n) {
+      const uint32_t u = key[i];
+      c[0] += u > st.pref[0]; c[1] += u == st.pref[0];
+      c[2] += u > st.pref[1]; c[3] += u == st.pref[1];
+    }
+  }
+  // block sums: across each wave, then the waves' partials in LDS
+  __shared__ int s_part[kSelThreads / 64][4];
+  const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c[q] += __shfl_xor(c[q], o, 64);
+  }
+  if (lane == 0)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s_part[wave][q] = c[q];
+  __syncthreads();
+  if (tid < 4) {
+    int t = 0;
+    for (int w = 0; w < kSelThreads / 64; ++w) t += s_part[w][tid];
+    a.sel_cnt[((size_t)bh * a.NSEL + blockIdx.x) * 4 + tid] = t;
+  }
+}
+
+// Placement: main_idx (top-scored, ascending, then the protected recent
+// window), elist (every other scored position, ascending) and seeds (ranks
+// k1 .. k2 - 1, ascending). Each thread owns kSelPer consecutive positions
+// of the block's chunk and ranks them; the block's three runs are gathered
+// in LDS and stored with consecutive lanes on consecutive entries.
+__global__ __launch_bounds__(kSelThreads) void select_write(BuildArgs a) {
+  const int bh = blockIdx.z * a.Hkv + blockIdx.y;
+  const HeadMeta hm = a.meta[bh];
+  const int tid = threadIdx.x, blk = blockIdx.x;
   int32_t* main_idx = a.main_idx + (size_t)bh * a.C;
-  if (tid == 0) {
+  if (blk == 0 && tid == 0) {
     a.res_len[bh] = hm.r;
     a.main_len[bh] = hm.main_len;
   }
   if (hm.all_main) {
-    for (int i = tid; i < hm.s; i += kSelThreads) main_idx[i] = i;
+    for (int i = blk * kSelChunk + tid; i < min(hm.s, (blk + 1) * kSelChunk); i += kSelThreads) main_idx[i] = i;
     return;
   }
-  const int n = hm.n_sc;
-  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.score + (size_t)bh * a.S);
-  __shared__ int s_hist[2][256];
-  __shared__ int s_tmp[kSelThreads / 64];
+  // the protected recent window follows the top-scored tokens
+  if (blk == 0)
+    for (int i = tid; i < hm.P; i += kSelThreads) main_idx[hm.k_top + i] = hm.n_sc + i;
+  if (blk * kSelChunk >= hm.n_sc) return;  // block-uniform
+  __shared__ int s_gh[kSelHist];
   __shared__ uint32_t s_pref[2];
   __shared__ int s_krem[2];
-  // select the k-th largest value for k1 = k_top and k2 = k_top + r_eff
-  const int kk[2] = {hm.k_top, hm.k_top + hm.r_eff};
-  uint32_t prefix[2] = {0u, 0u}, mask = 0u;
-  int krem[2] = {kk[0], kk[1]};
-  const int wave = tid >> 6, lane = tid & 63;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    // while both thresholds share their prefix (always in the first pass, and
-    // as long as they take the same digits) one histogram serves both
-    const bool shared = krem[0] > 0 && krem[1] > 0 && prefix[0] == prefix[1];  // block-uniform
-    for (int i = tid; i < 512; i += kSelThreads) (&s_hist[0][0])[i] = 0;
-    __syncthreads();
-    // coalesced, kHistBatch keys in flight per thread
-    constexpr int kHistBatch = 16;
-    for (int i0 = tid; i0 < n; i0 += kHistBatch * kSelThreads) {
-      uint32_t u[kHistBatch];
-#pragma unroll
-      for (int v = 0; v < kHistBatch; ++v) u[v] = i0 + v * kSelThreads < n ? key[i0 + v * kSelThreads] : 0u;
-#pragma unroll
-      for (int v = 0; v < kHistBatch; ++v) {
-        const int dig = (u[v] >> shift) & 0xff;
-        const bool in = i0 + v * kSelThreads < n;
-        wave_hist_add(s_hist[0], dig, in && krem[0] > 0 && (u[v] & mask) == prefix[0], lane);
-        if (!shared) wave_hist_add(s_hist[1], dig, in && krem[1] > 0 && (u[v] & mask) == prefix[1], lane);
-      }
-    }
-    __syncthreads();
-    // wave q finds the digit of threshold q: each lane holds 4 bins in
-    // descending digit order; an inclusive scan over lanes gives the count of
-    // keys at or above each digit
-    if (wave < 2) {
-      const int q = wave, hq = shared ? 0 : q;
-      if (krem[q] > 0) {
-        int c[4], own = 0;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) { c[v] = s_hist[hq][255 - 4 * lane - v]; own += c[v]; }
-        int incl = own;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(incl, o, 64);
-          if (lane >= o) incl += y;
-        }
-        int run = incl - own;  // keys above this lane's first digit
-        int hit_d = -1, hit_acc = 0;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          if (hit_d < 0 && run + c[v] >= krem[q]) { hit_d = 255 - 4 * lane - v; hit_acc = run; }
-          run += c[v];
-        }
-        // the first lane (highest digits) that reaches krem owns the digit
-        const unsigned long long hit = __ballot(hit_d >= 0);
-        const int src = hit ? __ffsll((long long)hit) - 1 : 63;
-        int d = __shfl(hit_d, src, 64), acc = __shfl(hit_acc, src, 64);
-        if (!hit) { d = 0; acc = __shfl(incl, 63, 64) - s_hist[hq][0]; }
-        if (lane == 0) {
-          s_pref[q] = prefix[q] | ((uint32_t)d << shift);
-          s_krem[q] = krem[q] - acc;
-        }
-      } else if (lane == 0) {
-        s_pref[q] = prefix[q];
-        s_krem[q] = krem[q];
-      }
-    }
-    __syncthreads();
-    prefix[0] = s_pref[0]; prefix[1] = s_pref[1];
-    krem[0] = s_krem[0]; krem[1] = s_krem[1];
-    mask |= 0xffu << shift;
-    __syncthreads();
+  __shared__ int s_tmp[kSelThreads / 64];
+  SelState st;
+  sel_state(a, hm, bh, 4, st, s_gh, s_pref, s_krem);
+  const uint32_t T1 = st.pref[0], T2 = st.pref[1];
+  const int need1 = st.krem[0], need2 = st.krem[1];
+  const bool on1 = st.k1 > 0, on2 = st.k2 > 0;
+  // offsets and tie ranks from the earlier blocks' counts (full chunks)
+  int base_e1 = 0, base_e2 = 0, base_top = 0, base_seed = 0;
+  const int32_t* cnt = a.sel_cnt + (size_t)bh * a.NSEL * 4;
+  for (int pb = 0; pb < blk; ++pb) {
+    const int gt1 = cnt[4 * pb], eq1 = cnt[4 * pb + 1], gt2 = cnt[4 * pb + 2], eq2 = cnt[4 * pb + 3];
+    const int top = on1 ? gt1 + min(max(need1 - base_e1, 0), eq1) : 0;
+    const int sel2 = on2 ? gt2 + min(max(need2 - base_e2, 0), eq2) : 0;
+    base_top += top;
+    base_seed += sel2 - top;  // the top scores are among the first k2
+    base_e1 += eq1;
+    base_e2 += eq2;
   }
-  // thresholds T_q = prefix[q]; krem[q] = how many keys equal to T_q to take
-  // (lowest positions first); kk[q] == 0 selects nothing
-  const uint32_t T1 = prefix[0], T2 = prefix[1];
-  const int need1 = krem[0], need2 = krem[1];
-  const bool on1 = kk[0] > 0, on2 = kk[1] > 0;
-  const int L = (n + kSelThreads - 1) / kSelThreads;
-  const int lo = min(n, tid * L), hi = min(n, lo + L);
-  // Each thread owns the consecutive keys [lo, hi); up to kSegKeys of them
-  // are held in registers across the three passes below (read once, all
-  // loads in flight together); longer segments are re-read per pass.
-  constexpr int kSegKeys = 32;
-  uint32_t seg[kSegKeys];
-  const bool in_regs = L <= kSegKeys;  // block-uniform
-  // longer segments: the keys of [lo, hi) in order, read kSegKeys at a time
-  // with every load of a batch in flight together
-  auto for_segment = [&](int lo_, int hi_, auto&& f) {
-    for (int i0 = lo_; i0 < hi_; i0 += kSegKeys) {
-      uint32_t b[kSegKeys];
+  const int base_ev = blk * kSelChunk - base_top;
+  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.score + (size_t)bh * a.S);
+  const int lo = st.i0 + tid * kSelPer;
+  uint32_t seg[kSelPer];
 #pragma unroll
-      for (int v = 0; v < kSegKeys; ++v) b[v] = i0 + v < hi_ ? key[i0 + v] : 0u;
-#pragma unroll
-      for (int v = 0; v < kSegKeys; ++v)
-        if (i0 + v < hi_) f(i0 + v, b[v]);
-    }
-  };
-  if (in_regs) {
-#pragma unroll
-    for (int v = 0; v < kSegKeys; ++v) seg[v] = lo + v < hi ? key[lo + v] : 0u;
-  }
-  // pass 1: equal-to-threshold counts per segment, scanned
+  for (int v = 0; v < kSelPer; ++v) seg[v] = lo + v < st.n ? key[lo + v] : 0u;
+  // equal-to-threshold counts per thread, scanned: the tie ranks
   int e1 = 0, e2 = 0;
-  if (in_regs) {
 #pragma unroll
-    for (int v = 0; v < kSegKeys; ++v)
-      if (lo + v < hi) { e1 += (seg[v] == T1); e2 += (seg[v] == T2); }
-  } else {
-    for_segment(lo, hi, [&](int, uint32_t u) {
-      e1 += (u == T1);
-      e2 += (u == T2);
-    });
-  }
+  for (int v = 0; v < kSelPer; ++v)
+    if (lo + v < st.n) { e1 += (seg[v] == T1); e2 += (seg[v] == T2); }
+  // both counts in one scan (each block total is at most kSelChunk < 2^16)
   int tot;
-  int eb1 = block_excl_scan<kSelThreads>(e1, s_tmp, tot);
-  int eb2 = block_excl_scan<kSelThreads>(e2, s_tmp, tot);
-  // pass 2: classify, count main / evicted / seed per segment
-  int c_top = 0, c_ev = 0, c_seed = 0;
+  const int eb12 = block_excl_scan<kSelThreads>(e1 | (e2 << 16), s_tmp, tot);
+  const int eb1 = base_e1 + (eb12 & 0xffff), eb2 = base_e2 + (eb12 >> 16);
   auto classify = [&](uint32_t u, int& r1, int& r2, bool& top, bool& sel2) {
     top = on1 && (u > T1 || (u == T1 && r1 < need1));
     sel2 = on2 && (u > T2 || (u == T2 && r2 < need2));
     r1 += (u == T1);
     r2 += (u == T2);
   };
+  int c_top = 0, c_seed = 0;
   {
     int r1 = eb1, r2 = eb2;
-    if (in_regs) {
 #pragma unroll
-      for (int v = 0; v < kSegKeys; ++v) {
-        if (lo + v < hi) {
-          bool top, sel2;
-          classify(seg[v], r1, r2, top, sel2);
-          c_top += top;
-          c_ev += !top;
-          c_seed += (sel2 && !top);
-        }
-      }
-    } else {
-      for_segment(lo, hi, [&](int, uint32_t u) {
+    for (int v = 0; v < kSelPer; ++v) {
+      if (lo + v < st.n) {
         bool top, sel2;
-        classify(u, r1, r2, top, sel2);
+        classify(seg[v], r1, r2, top, sel2);
         c_top += top;
-        c_ev += !top;
         c_seed += (sel2 && !top);
-      });
+      }
     }
   }
-  int ob_top = block_excl_scan<kSelThreads>(c_top, s_tmp, tot);
-  int ob_ev = block_excl_scan<kSelThreads>(c_ev, s_tmp, tot);
-  int ob_seed = block_excl_scan<kSelThreads>(c_seed, s_tmp, tot);
-  // pass 3: write
+  // block-local run offsets: top-scored from the front of s_run, evicted
+  // after them (the two partition the chunk), seeds in their own buffer
+  // (the evicted count of the threads before this one is their positions
+  // minus their top-scored ones: every earlier thread holds kSelPer)
+  int nts;
+  const int ots = block_excl_scan<kSelThreads>(c_top | (c_seed << 16), s_tmp, nts);
+  const int n_top = nts & 0xffff, n_seed = nts >> 16;
+  const int n_valid = min(kSelChunk, st.n - st.i0);
+  const int n_ev = n_valid - n_top;
+  int ob_top = ots & 0xffff;
+  int ob_seed = ots >> 16;
+  int ob_ev = n_top + min(tid * kSelPer, n_valid) - ob_top;
+  __shared__ int s_run[kSelChunk];
+  __shared__ int s_seed[kSelChunk];
+  int r1 = eb1, r2 = eb2;
+#pragma unroll
+  for (int v = 0; v < kSelPer; ++v) {
+    if (lo + v < st.n) {
+      bool top, sel2;
+      classify(seg[v], r1, r2, top, sel2);
+      if (top) s_run[ob_top++] = lo + v;
+      else s_run[ob_ev++] = lo + v;
+      if (sel2 && !top) s_seed[ob_seed++] = lo + v;
+    }
+  }
+  __syncthreads();
   int32_t* elist = a.elist + (size_t)bh * a.S;
   int32_t* seeds = a.seeds + (size_t)bh * a.Rcap;
-  {
-    int r1 = eb1, r2 = eb2;
-    auto emit = [&](int i, uint32_t u) {
-      bool top, sel2;
-      classify(u, r1, r2, top, sel2);
-      if (top) main_idx[ob_top++] = i;
-      else elist[ob_ev++] = i;
-      if (sel2 && !top) seeds[ob_seed++] = i;
-    };
-    if (in_regs) {
-#pragma unroll
-      for (int v = 0; v < kSegKeys; ++v)
-        if (lo + v < hi) emit(lo + v, seg[v]);
-    } else {
-      for_segment(lo, hi, emit);
-    }
+  for (int i = tid; i < n_top + n_ev; i += kSelThreads) {
+    if (i < n_top) main_idx[base_top + i] = s_run[i];
+    else elist[base_ev + i - n_top] = s_run[i];
   }
-  // the protected recent window follows the top-scored tokens
-  for (int i = tid; i < hm.P; i += kSelThreads) main_idx[hm.k_top + i] = hm.n_sc + i;
+  for (int i = tid; i < n_seed; i += kSelThreads) seeds[base_seed + i] = s_seed[i];
 }
 
 // ------------------------------------- AdaKV cross-head budget allocation
@@ -1424,6 +1538,9 @@ BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const voi
   a.cstart = reinterpret_cast<int32_t*>(ws + pl.off_cstart);
   a.ccount = reinterpret_cast<int32_t*>(ws + pl.off_ccount);
   a.order = reinterpret_cast<int32_t*>(ws + pl.off_order);
+  a.sel_hist = reinterpret_cast<int32_t*>(ws + pl.off_selh);
+  a.sel_cnt = reinterpret_cast<int32_t*>(ws + pl.off_selc);
+  a.NSEL = pl.NSEL;
   a.B = pl.B; a.Hq = pl.Hq; a.Hkv = pl.Hkv; a.G = pl.G; a.C = pl.C; a.Rcap = pl.Rcap; a.S = pl.S; a.w = pl.w;
   a.wr = pl.wr; a.pool_half = pl.pool_half; a.R = pl.R; a.LG = pl.LG; a.NCH = pl.NCH; a.NBLK = pl.NBLK; a.T = pl.T;
   a.cap_slots = pl.C;
@@ -1468,7 +1585,12 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
     hipLaunchKernelGGL(adakv_alloc, dim3(pl.B), dim3(kAdaThreads), 0, st, a, alloc_meta, safeguard);
     RESKV_CHECK();
   }
-  hipLaunchKernelGGL(select_kernel, bhg, dim3(kSelThreads), 0, st, a); RESKV_CHECK();
+  for (int pass = 0; pass < 4; ++pass) {
+    hipLaunchKernelGGL(select_hist, grid(pl.NSEL), dim3(kSelThreads), 0, st, a, pass);
+    RESKV_CHECK();
+  }
+  hipLaunchKernelGGL(select_count, grid(pl.NSEL), dim3(kSelThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(select_write, grid(pl.NSEL), dim3(kSelThreads), 0, st, a); RESKV_CHECK();
   const int rows = pl.max_main + pl.Rcap;
   const int gblocks = (rows * (D * (int)sizeof(T) / 16) + kThreads - 1) / kThreads;
   hipLaunchKernelGGL((gather_init<T, D>), grid(gblocks < 64 ? gblocks : 64), dim3(kThreads), 0, st, a);
@@ -1559,6 +1681,8 @@ bool layout_build_plan(BuildPlan* plan) {
   pl.NSC = (pl.max_s + kKeyChunk - 1) / kKeyChunk;
   pl.NBLK = (pl.max_E + kTokBlock - 1) / kTokBlock;
   if (pl.NBLK < 1) pl.NBLK = 1;
+  pl.NSEL = (pl.max_s + kSelChunk - 1) / kSelChunk;
+  if (pl.NSEL < 1) pl.NSEL = 1;
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align_up(off + bytes, 256); return o; };
   pl.off_meta = take(BH * sizeof(HeadMeta));
@@ -1577,6 +1701,8 @@ bool layout_build_plan(BuildPlan* plan) {
   pl.off_cstart = take(BH * pl.Rcap * sizeof(int32_t));
   pl.off_ccount = take(BH * pl.Rcap * sizeof(int32_t));
   pl.off_order = take(BH * pl.S * sizeof(int32_t));
+  pl.off_selh = take(BH * kSelHist * sizeof(int32_t));
+  pl.off_selc = take(BH * pl.NSEL * 4 * sizeof(int32_t));
   pl.bytes = off;
   return true;
 }

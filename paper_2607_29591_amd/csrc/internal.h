@@ -85,9 +85,10 @@ struct BuildPlan {
   int NCH;    // lse key chunks (256 * LG keys) of the longest sequence
   int NSC;    // score-pass key chunks of the longest sequence
   int NBLK;   // 256-token blocks of the largest evicted set
+  int NSEL;   // selection blocks (8192 scores each) of the longest sequence
   int max_s, max_main, max_reff, max_E;
   size_t off_meta, off_lsep, off_lse, off_raw, off_score, off_elist, off_seeds, off_cent, off_chi,
-      off_clo, off_cnorm, off_assign, off_hist, off_cstart, off_ccount, off_order, bytes;
+      off_clo, off_cnorm, off_assign, off_hist, off_cstart, off_ccount, off_order, off_selh, off_selc, bytes;
 };
 
 // Device buffers one construction writes.

@@ -71,6 +71,21 @@ def test_build_ties_take_lowest_positions():
         assert got["main_idx"][0, h, :32].tolist() == list(range(2, 26)) + list(range(192, 200))
 
 
+def test_build_ties_across_selection_blocks():
+    """All scores equal over 20000 positions (three 8192-score selection
+    blocks): the tie ranks run across the blocks, so the top-scored tokens
+    are the lowest interior positions and the seeds the next ones."""
+    wl, x = small(3, dtype="bf16", d=64, s=20000, budget=600, res=(64, 32))
+    x["K"][:] = 1.0
+    x["q_obs"][:] = 0.5
+    host_copies(x)
+    got = run_build(wl, x)
+    for h in range(wl.hkv):
+        check_head(wl, x, got, 0, h)
+        k_top = 600 - wl.res[0, 0, h] - wl.window
+        assert got["main_idx"][0, h, :k_top].tolist() == list(range(2, 2 + k_top))
+
+
 def test_build_workload0_and_decode():
     """The fp32 toy workload end to end: construction parity, then decode of
     the 8 queries over the GPU-built cache."""
