@@ -123,7 +123,8 @@ def traffic_from_profile(src_hash, name=PROFILES[2]["decode"]):
         rec = json.load(f)
     if rec.get("decode_source_sha256_16") != src_hash:
         return None
-    return rec.get("bytes_per_call") / rec.get("algorithmic_bytes_per_call")
+    num, den = rec.get("bytes_per_call"), rec.get("algorithmic_bytes_per_call")
+    return num / den if num and den else None
 
 
 def construction_mfma_from_profile(src_hash, name=PROFILES[2]["construction"]):
@@ -532,6 +533,8 @@ def main():
     for l in range(L):
         x = synth.gen_layer_device(wl, l, dev)
         layers.append(x)
+        if l == 0 or l == L - 1 or args.mode == "decode":
+            progress(f"input of layer {l} generated")
     q_stage = torch.stack([x["q_dec"] for x in layers])      # [L, steps, B, Hq, d]
     kn_stage = torch.stack([x["k_new"] for x in layers])
     vn_stage = torch.stack([x["v_new"] for x in layers])
@@ -619,6 +622,8 @@ def main():
             rk.reskv_build_cache(shape, params, x["K"], x["V"], x["seq_len"], x["q_obs"], x["budget"],
                                  res_layers[l].reshape(-1), c["kc"], c["vc"], c["logc"], c["main_idx"],
                                  c["res_len"], c["main_len"], build_ws)
+            torch.cuda.synchronize()
+            progress(f"layer {l} built")
         for t in range(args.steps):
             for l in range(L):
                 c = caches[l]
