@@ -488,11 +488,11 @@ __device__ __forceinline__ void radix_replay(const int* gh, int npass, int k1, i
   }
 }
 
-// Setup shared by the selection kernels: the head, its chunk and the
-// threshold state after `npass` radix passes (replayed by wave 0, then read
-// by every thread). Returns false where the block has nothing to do.
+// Setup shared by the selection kernels: the head's scored length, the
+// block's first score and the threshold state after `npass` radix passes
+// (replayed by wave 0, then read by every thread; synchronises the block).
 struct SelState {
-  int bh, n, i0;
+  int n, i0;
   int k1, k2;
   uint32_t pref[2];
   int krem[2];
@@ -500,7 +500,6 @@ struct SelState {
 __device__ __forceinline__ void sel_state(const BuildArgs& a, const HeadMeta& hm, int bh, int npass, SelState& st,
                                           int* s_gh, uint32_t* s_pref, int* s_krem) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  st.bh = bh;
   st.n = hm.n_sc;
   st.i0 = blockIdx.x * kSelChunk;
   st.k1 = hm.k_top;
