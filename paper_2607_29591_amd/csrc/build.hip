@@ -1301,25 +1301,24 @@ __global__ __launch_bounds__(kTokBlock) void lloyd_scatter(BuildArgs a) {
   a.order[(size_t)bh * a.S + dst] = src;
 }
 
-// New centre of group j = fp64 mean of its members' keys, summed in a fixed
-// order; an empty group keeps its centre. The last round also writes the
-// entry: mean key and mean value in the cache dtype, and log c_j.
-// kPacked (bf16): rows stay packed until they are added, which keeps the
-// kernel at 64 registers and eight blocks per CU, the better shape when the
-// groups are of similar size (rounds after the first). The first round's
-// groups, grown around single seed keys, are very uneven; there the wider
-// variant (rows converted as they land, about 100 registers, four blocks per
-// CU) keeps more of a long group's rows in flight and finishes sooner.
-// kKV (last round, bf16): each member's key and value rows are read in the
-// same loop, twice the rows in flight of two passes one after the other.
 // Member indices q, q + NG, q + 2NG, q + 3NG of a group's sorted list.
 __device__ __forceinline__ void load_ids(int (&id)[4], const int32_t* mem, int q, int NG) {
 #pragma unroll
   for (int u = 0; u < 4; ++u) id[u] = mem[q + u * NG];
 }
 
-template <typename T, int D, bool kPacked, bool kKV = false>
-__global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && sizeof(T) == 2 ? 8 : 4)) void lloyd_update(BuildArgs a, int last, int rev) {
+// New centre of group j = fp64 mean of its members' keys, summed in a fixed
+// order; an empty group keeps its centre. The last round also writes the
+// entry: mean key and mean value in the cache dtype, and log c_j. Each
+// thread keeps four member rows in flight and requests the next four
+// members' indices right behind them, so a long group (the first round's
+// groups, grown around single seed keys, run from a few rows to thousands)
+// waits one memory round trip per step. bf16 rows stay packed until they are
+// added (68 registers, seven blocks per CU).
+// kKV (last round, bf16): each member's key and value rows are read in the
+// same loop, twice the rows in flight of two passes one after the other.
+template <typename T, int D, bool kKV = false>
+__global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : sizeof(T) == 2 ? 7 : 4)) void lloyd_update(BuildArgs a, int last, int rev) {
   const int j = blockIdx.x;
   int b, kvh, bh;
   block_head(a, rev, b, kvh, bh);
@@ -1403,15 +1402,15 @@ __global__ __launch_bounds__(kThreads, (kKV && sizeof(T) == 2 ? 4 : kPacked && s
     // members g, g + NG, g + 2NG, ... in order; four 16-byte row loads in
     // flight, and (wider variant) the next four members' indices requested
     // behind them; the packed variant has no registers to spare for them
-    constexpr bool kPacked16 = kPacked && sizeof(T) == 2;
     int q = g;
     int id[4];
-    if (!kPacked16 && q + 3 * NG < cnt) load_ids(id, mem, q, NG);
+    if (q + 3 * NG < cnt) load_ids(id, mem, q, NG);
     for (; q + 3 * NG < cnt; q += 4 * NG) {
-      if constexpr (kPacked16) {  // rows stay packed until added: 4 registers each
+      if constexpr (sizeof(T) == 2) {  // rows stay packed until added: 4 registers each
         uint4 w[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) w[u] = *reinterpret_cast<const uint4*>(X + (size_t)mem[q + u * NG] * D + 8 * c);
+        for (int u = 0; u < 4; ++u) w[u] = *reinterpret_cast<const uint4*>(X + (size_t)id[u] * D + 8 * c);
+        if (q + 7 * NG < cnt) load_ids(id, mem, q + 4 * NG, NG);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const uint32_t pw[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
@@ -1617,12 +1616,10 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
       // the update walks the heads in reverse of the assignment before and
       // after it, so each starts on the keys the other read last
       const int last = it == pl.T - 1 ? 1 : 0;
-      if (it == 0)
-        hipLaunchKernelGGL((lloyd_update<T, D, false>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
-      else if (last)
-        hipLaunchKernelGGL((lloyd_update<T, D, true, true>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
-      else
+      if (last)
         hipLaunchKernelGGL((lloyd_update<T, D, true>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
+      else
+        hipLaunchKernelGGL((lloyd_update<T, D>), grid(pl.max_reff), dim3(kThreads), 0, st, a, last, 1);
       RESKV_CHECK();
     }
   }
