@@ -71,11 +71,13 @@ def test_build_ties_take_lowest_positions():
         assert got["main_idx"][0, h, :32].tolist() == list(range(2, 26)) + list(range(192, 200))
 
 
-def test_build_ties_across_selection_blocks():
+@pytest.mark.parametrize("s", [20000, 16392])
+def test_build_ties_across_selection_blocks(s):
     """All scores equal over 20000 positions (three 8192-score selection
-    blocks): the tie ranks run across the blocks, so the top-scored tokens
-    are the lowest interior positions and the seeds the next ones."""
-    wl, x = small(3, dtype="bf16", d=64, s=20000, budget=600, res=(64, 32))
+    blocks, the last partial) or over exactly two full blocks (16384 scored
+    positions): the tie ranks run across the blocks, so the top-scored
+    tokens are the lowest interior positions and the seeds the next ones."""
+    wl, x = small(3, dtype="bf16", d=64, s=s, budget=600, res=(64, 32))
     x["K"][:] = 1.0
     x["q_obs"][:] = 0.5
     host_copies(x)
