@@ -367,9 +367,10 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
     const int nvalid = min(kUnit, end - s0);
     load_unit_k<T, D>(u, kc, s0, end - 1, hd, g, app_row, kn);
     if (is_res) load_unit_lc<T, D>(u, logc, s0, nvalid, g);
+    // the value rows are requested before the logits wait on the keys
+    load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, app_row, vn);
     float sc[kTiles][4];
     unit_logits<T, D>(u, q, a.qk_scale, sc);
-    load_unit_v<T, D>(u, vc, s0, nvalid, hd, g, app_row, vn);
     softmax_pv<T, D>(st, u, sc, 0, nvalid, is_res, a.beta_log2, g);
     if (app_row >= s0 && app_row < s0 + nvalid) {  // wave-uniform: the new rows into the cache
       constexpr int kPieces = D * (int)sizeof(T) / 16;
@@ -409,34 +410,59 @@ __global__ __launch_bounds__(kThreads) void decode_split(DecodeArgs a) {
 
 // Merge the records of one (b, kv head), evaluate the gate and write the G
 // outputs. Record p < PR is residual chunk p, record PR + q is main chunk q;
-// only chunks that hold slots were written.
+// only chunks that hold slots were written. The loads that do not depend on
+// the cache lengths are issued before those arrive: the (max, sum) of the
+// first 16 kML records of this thread's query head and the accumulators of
+// the first kPF records of its outputs. Records of chunks without slots hold
+// stale values; they are masked once the lengths are known.
 template <int D, int GP>
 __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
   extern __shared__ float s_w[];  // [GP][P] weights of the records
   const int kvh = blockIdx.x, b = blockIdx.y;
   const int bh = b * a.Hkv + kvh;
+  const int tid = threadIdx.x, lane16 = tid & 15, h = tid >> 4;
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml) + (size_t)bh * a.P * GP;
+  const float* pacc = a.part_acc + (size_t)bh * a.P * GP * D;
+  constexpr int kML = 4;
+  constexpr int kOut = (GP * D + kThreads - 1) / kThreads;
+  constexpr int kPF = kOut >= 8 ? 8 : 16;
+  const bool hv = h < a.G;
+  float2 mlv[kML];
+#pragma unroll
+  for (int k = 0; k < kML; ++k) {
+    const int q = lane16 + 16 * k;
+    mlv[k] = hv && q < a.P ? ml[q * GP + h] : make_float2(kNegInf, 0.f);
+  }
+  float pv[kOut][kPF];
+#pragma unroll
+  for (int k = 0; k < kOut; ++k) {
+    const int idx = min(tid + k * kThreads, a.G * D - 1), hh = idx / D, d = idx % D;
+#pragma unroll
+    for (int j = 0; j < kPF; ++j) pv[k][j] = j < a.P ? pacc[(j * GP + hh) * D + d] : 0.f;
+  }
   int r, n;
   cache_lengths(a.res_len, a.main_len, bh, a.C, a.Rcap, r, n);
   const bool app = a.k_new != nullptr && r + n < a.C;  // as in decode_split
   if (app) n += 1;
   const int nRC = (r + kChunk - 1) / kChunk, nMC = (n + kChunk - 1) / kChunk;
-  const float* ml = a.part_ml + (size_t)bh * a.P * GP * 2;
-  const float* pacc = a.part_acc + (size_t)bh * a.P * GP * D;
-  const int tid = threadIdx.x, lane16 = tid & 15, h = tid >> 4;
-  if (h < a.G) {
+  auto valid = [&](int p) { return p < nRC || (p >= a.PR && p < a.PR + nMC); };
+  if (hv) {
+    auto rec = [&](int k, int p) { return k < kML ? mlv[k] : ml[p * GP + h]; };
     float mM = kNegInf, mR = kNegInf;
-    for (int q = lane16; q < nMC; q += 16) mM = fmaxf(mM, ml[((a.PR + q) * GP + h) * 2]);
-    for (int q = lane16; q < nRC; q += 16) mR = fmaxf(mR, ml[(q * GP + h) * 2]);
+    for (int k = 0, p = lane16; p < a.P; ++k, p += 16) {
+      if (!valid(p)) continue;
+      const float m = rec(k, p).x;
+      if (p >= a.PR) mM = fmaxf(mM, m);
+      else mR = fmaxf(mR, m);
+    }
 #pragma unroll
     for (int msk = 1; msk < 16; msk <<= 1) { mM = wave_xor_max(mM, msk); mR = wave_xor_max(mR, msk); }
     float lM = 0.f, lR = 0.f;
-    for (int q = lane16; q < nMC; q += 16) {
-      const float* e = ml + ((a.PR + q) * GP + h) * 2;
-      if (e[0] != kNegInf) lM = fmaf(e[1], exp2f(e[0] - mM), lM);
-    }
-    for (int q = lane16; q < nRC; q += 16) {
-      const float* e = ml + (q * GP + h) * 2;
-      if (e[0] != kNegInf) lR = fmaf(e[1], exp2f(e[0] - mR), lR);
+    for (int k = 0, p = lane16; p < a.P; ++k, p += 16) {
+      const float2 e = rec(k, p);
+      if (!valid(p) || e.x == kNegInf) continue;
+      if (p >= a.PR) lM = fmaf(e.y, exp2f(e.x - mM), lM);
+      else lR = fmaf(e.y, exp2f(e.x - mR), lR);
     }
 #pragma unroll
     for (int msk = 1; msk < 16; msk <<= 1) { lM = wave_xor_add(lM, msk); lR = wave_xor_add(lR, msk); }
@@ -452,13 +478,14 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
     if (mM != kNegInf) den += lM * exp2f(mM - Mx);
     if (mRg != kNegInf) den += lR * exp2f(mRg - Mx);
     const float inv = den > 0.f ? 1.f / den : 0.f;
-    for (int q = lane16; q < nMC; q += 16) {
-      const float m = ml[((a.PR + q) * GP + h) * 2];
-      s_w[h * a.P + a.PR + q] = m != kNegInf ? exp2f(m - Mx) * inv : 0.f;
-    }
-    for (int q = lane16; q < nRC; q += 16) {
-      const float m = ml[(q * GP + h) * 2];
-      s_w[h * a.P + q] = (m != kNegInf && mRg != kNegInf) ? exp2f(m + lg2g - Mx) * inv : 0.f;
+    for (int k = 0, p = lane16; p < a.P; ++k, p += 16) {
+      const float m = rec(k, p).x;
+      float w = 0.f;
+      if (valid(p) && m != kNegInf) {
+        if (p >= a.PR) w = exp2f(m - Mx) * inv;
+        else if (mRg != kNegInf) w = exp2f(m + lg2g - Mx) * inv;
+      }
+      s_w[h * a.P + p] = w;
     }
     if (lane16 == 0) {
       if (a.dbg_lse_main) a.dbg_lse_main[qh] = lM > 0.f ? (mM + log2f(lM)) * kLn2 : kNegInf;
@@ -467,23 +494,19 @@ __global__ __launch_bounds__(kThreads) void decode_combine(DecodeArgs a) {
     }
   }
   __syncthreads();
-  for (int idx = tid; idx < a.G * D; idx += kThreads) {
+#pragma unroll
+  for (int k = 0; k < kOut; ++k) {
+    const int idx = tid + k * kThreads;
+    if (idx >= a.G * D) continue;
     const int hh = idx / D, d = idx % D;
     const float* w = s_w + hh * a.P;
-    float o0 = 0.f, o1 = 0.f;
-    int q = 0;
-    for (; q + 1 < nRC; q += 2) {
-      o0 = fmaf(w[q], pacc[(q * GP + hh) * D + d], o0);
-      o1 = fmaf(w[q + 1], pacc[((q + 1) * GP + hh) * D + d], o1);
-    }
-    if (q < nRC) o0 = fmaf(w[q], pacc[(q * GP + hh) * D + d], o0);
-    for (q = 0; q + 1 < nMC; q += 2) {
-      const int pp = a.PR + q;
-      o0 = fmaf(w[pp], pacc[(pp * GP + hh) * D + d], o0);
-      o1 = fmaf(w[pp + 1], pacc[((pp + 1) * GP + hh) * D + d], o1);
-    }
-    if (q < nMC) o0 = fmaf(w[a.PR + q], pacc[((a.PR + q) * GP + hh) * D + d], o0);
-    a.out[((size_t)b * a.Hq + kvh * a.G + hh) * D + d] = o0 + o1;
+    float o = 0.f;
+#pragma unroll
+    for (int j = 0; j < kPF; ++j)
+      if (j < a.P && valid(j)) o = fmaf(w[j], pv[k][j], o);
+    for (int j = kPF; j < a.P; ++j)
+      if (valid(j)) o = fmaf(w[j], pacc[(j * GP + hh) * D + d], o);
+    a.out[((size_t)b * a.Hq + kvh * a.G + hh) * D + d] = o;
   }
   // the appended token is in the cache: advance main_len (one block per
   // head, and every thread of it read the length above)
