@@ -625,12 +625,15 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   T* vc = static_cast<T*>(const_cast<void*>(a.vc)) + (size_t)bh * a.C * D;
   const float* logc = a.logc + (size_t)bh * a.Rcap;
 
-  // Units: residual slots [0, r) in 64-slot chunks, then main slots [r, r+n)
-  // in 64-slot chunks, dealt round-robin to the waves so that every wave
-  // streams about the same number of slots whatever the split between the
-  // kinds. A wave's first unit is slots [64 wave, 64 wave + 64) unless it is a
-  // main unit and r is not a multiple of 64, so its keys are requested before
-  // the cache lengths are read (and requested again in that case).
+  // Units: the head's r + n slots (residual slots [0, r), then main slots) in
+  // 64-slot blocks [64 u, 64 u + 64), each of one kind: the block holding
+  // slot r, when r is not a multiple of 64, is unit u = UR - 1 for its
+  // residual slots and one extra unit u = NB, dealt last, for its main slots.
+  // Units go round-robin to the waves, so every wave streams about the same
+  // number of slots whatever the split between the kinds, and a wave meets
+  // its residual units before its main ones. A wave's first unit is slots
+  // [64 wave, 64 wave + 64) (unless it is the extra unit), so its keys are
+  // requested before the cache lengths are read.
   UnitRegs<T, D> ur0;
   load_unit_k<T, D>(ur0, kc, kUnit * wave, a.C - 1, hd, g, -1, nullptr);
   int r, n;
@@ -667,11 +670,20 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   if (hd < a.G) q.load(static_cast<const T*>(a.q) + ((size_t)b * a.Hq + (size_t)kvh * a.G + hd) * D, g);
   else q.zero();
 
-  const int UR = (r + kUnit - 1) / kUnit, U = UR + (n + kUnit - 1) / kUnit;
+  const int total = r + n;
+  const int UR = (r + kUnit - 1) / kUnit, NB = (total + kUnit - 1) / kUnit;
+  const bool straddle = r % kUnit != 0 && total > r;
+  const int U = NB + (straddle ? 1 : 0);
   auto unit_range = [&](int u, bool& is_res, int& s0, int& end) {
-    is_res = u < UR;
-    s0 = is_res ? u * kUnit : r + (u - UR) * kUnit;
-    end = is_res ? r : r + n;
+    if (u < NB) {
+      is_res = u < UR;
+      s0 = u * kUnit;
+      end = is_res ? r : total;
+    } else {  // the main slots of block UR - 1
+      is_res = false;
+      s0 = r;
+      end = min(UR * kUnit, total);
+    }
   };
   WaveState<D> st;
   st.reset();

@@ -244,6 +244,49 @@ def test_decode_whole_head_wide_groups(dtype, d, G):
     check(dtype, shape, q, kc, vc, logc, res, main, heads=heads, tau=tau)
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_decode_whole_head_residual_boundary_inside_a_block(dtype, d):
+    """256 (b, kv head) pairs whose residual count r is not a multiple of the
+    64-slot unit: the block holding slot r is streamed as its residual part
+    and its main part (dealt last), with this step's token appended before,
+    at or after the end of that block, and heads short enough that the main
+    part is a wave's first unit. Every query head is checked, and the
+    appended rows and lengths bit for bit."""
+    B, Hkv, G = 64, 4, 4
+    rng = np.random.default_rng(70 + d)
+    C, Rcap = 640, 200
+    res = rng.choice([1, 37, 63, 64, 65, 127, 130, 191], size=(B, Hkv))
+    ur = (res + 63) // 64
+    # main lengths: inside the boundary block, exactly filling it, or past it
+    pick = rng.integers(0, 3, size=(B, Hkv))
+    main = np.where(pick == 0, np.maximum(1, 64 * ur - res - 1 - rng.integers(0, 8, size=(B, Hkv))),
+                    np.where(pick == 1, np.maximum(1, 64 * ur - res), rng.integers(1, C - 200, size=(B, Hkv))))
+    main = np.minimum(main, C - res - 1)
+    shape, q, kc, vc, logc = cache_case(80 + d, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main)
+    kn = rng.normal(size=(B, Hkv, d))
+    vn = rng.normal(size=(B, Hkv, d))
+    knd, vnd = to_dev(kn, dtype), to_dev(vn, dtype)
+    kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
+    lcd = torch.as_tensor(logc.astype(np.float32)).cuda()
+    rl = torch.as_tensor(res.astype(np.int32).reshape(-1)).cuda()
+    ml = torch.as_tensor(main.astype(np.int32).reshape(-1)).cuda()
+    out = torch.empty((B, G * Hkv, d), device="cuda")
+    ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    rk.reskv_decode_attn(shape, rk.make_gate(), to_dev(q, dtype), kcd, vcd, lcd, rl, ml, out, ws,
+                         k_new=knd, v_new=vnd)
+    torch.cuda.synchronize()
+    kc2, vc2, main2 = kc.copy(), vc.copy(), main + 1
+    for b in range(B):
+        for h in range(Hkv):
+            kc2[b, h, res[b, h] + main[b, h]] = knd[b, h].double().cpu().numpy()
+            vc2[b, h, res[b, h] + main[b, h]] = vnd[b, h].double().cpu().numpy()
+    np.testing.assert_array_equal(ml.cpu().numpy().reshape(B, Hkv), main2)
+    np.testing.assert_array_equal(kcd.double().cpu().numpy(), kc2)
+    np.testing.assert_array_equal(vcd.double().cpu().numpy(), vc2)
+    ref, *_ = orc.decode(q, kc2, vc2, logc, res, main2, 0.25, 12.0, 0.0, 1.0)
+    assert rel_err_rows(out.double().cpu().numpy(), ref).max() <= TOL[dtype]
+
+
 def test_prepared_decode_call_matches_direct_call():
     """prepare_decode_attn marshals the arguments once; issuing it twice
     (each call appends a token) gives the same caches, lengths and outputs,
