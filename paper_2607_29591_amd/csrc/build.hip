@@ -357,25 +357,44 @@ __global__ __launch_bounds__(kThreads, (RC > kRowChunk ? 2 : sizeof(T) == 2 ? 4 
 }
 
 // Centred (2 * pool_half + 1)-tap sum with zero padding over the scored
-// positions (5 taps for the SnapKV rule, 1 for H2O and TOVA).
+// positions (5 taps for the SnapKV rule, 1 for H2O and TOVA). A thread pools
+// kPoolPer consecutive positions from one window of raw scores held in
+// registers (zeros outside [0, n)), adding the taps in ascending position
+// order as the one-position form does.
+constexpr int kPoolPer = 4;
+constexpr int kPoolHalfMax = 15;  // pool_half <= 15 (pool_kernel <= 31)
 __global__ __launch_bounds__(kThreads) void pool_scores(BuildArgs a) {
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int bh = b * a.Hkv + kvh;
   const HeadMeta hm = a.meta[bh];
   if (blockIdx.x == 0)  // the selection's pass histograms start from zero
     for (int i = threadIdx.x; i < kSelHist; i += kThreads) a.sel_hist[(size_t)bh * kSelHist + i] = 0;
-  const int p = blockIdx.x * kThreads + threadIdx.x;
-  if (p >= a.S) return;
+  const int p0 = (blockIdx.x * kThreads + threadIdx.x) * kPoolPer;
+  if (p0 >= a.S) return;
   const int n = hm.all_main ? 0 : hm.n_sc;
+  const int ph = a.pool_half;
   const float* raw = a.raw + (size_t)bh * a.S;
-  float v = -1.f;
-  if (p < n) {
-    v = 0.f;
-    const int lo = max(p - a.pool_half, 0), hi = min(p + a.pool_half, n - 1);
-    for (int q = lo; q <= hi; ++q) v += raw[q];
-    a.score[(size_t)bh * a.S + p] = v;
+  float w[kPoolPer + 2 * kPoolHalfMax];  // raw[p0 - kPoolHalfMax + i]
+#pragma unroll
+  for (int i = 0; i < kPoolPer + 2 * kPoolHalfMax; ++i) {
+    const int q = p0 - kPoolHalfMax + i;
+    const bool tap = q >= p0 - ph && q < p0 + kPoolPer + ph;
+    w[i] = tap && q >= 0 && q < n ? raw[q] : 0.f;
   }
-  if (a.dbg_scores) a.dbg_scores[(size_t)bh * a.S + p] = v;
+#pragma unroll
+  for (int k = 0; k < kPoolPer; ++k) {
+    const int p = p0 + k;
+    if (p >= a.S) break;
+    float v = -1.f;
+    if (p < n) {
+      v = 0.f;
+#pragma unroll
+      for (int j = -kPoolHalfMax; j <= kPoolHalfMax; ++j)
+        if (j >= -ph && j <= ph) v += w[k + kPoolHalfMax + j];
+      a.score[(size_t)bh * a.S + p] = v;
+    }
+    if (a.dbg_scores) a.dbg_scores[(size_t)bh * a.S + p] = v;
+  }
 }
 
 // -------------------------------------------------------------- selection
@@ -1548,22 +1567,26 @@ BuildArgs make_args(const BuildPlan& pl, const void* k, const void* v, const voi
 
 #define RESKV_CHECK() do { e = hipGetLastError(); if (e != hipSuccess) return e; } while (0)
 
-// Raw window scores of every scored position (lse, then weights summed).
-template <typename T, int D>
-hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
+// The two scoring passes with RC window rows per chunk.
+template <typename T, int D, int RC>
+hipError_t launch_score_passes(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
   auto grid = [&](int x) { return dim3(x < 1 ? 1 : x, pl.Hkv, pl.B); };
   hipError_t e;
-  // the wide chunk at bf16 rows (fp32 rows of 128 would hold one block per CU)
-  const bool wide = pl.R > kRowChunk && (sizeof(T) == 2 || D == 64);
-  if (wide) hipLaunchKernelGGL((lse_partial<T, D, kRowChunkWide>), grid(pl.NCH), dim3(kThreads), 0, st, a);
-  else hipLaunchKernelGGL((lse_partial<T, D, kRowChunk>), grid(pl.NCH), dim3(kThreads), 0, st, a);
-  RESKV_CHECK();
+  hipLaunchKernelGGL((lse_partial<T, D, RC>), grid(pl.NCH), dim3(kThreads), 0, st, a); RESKV_CHECK();
   hipLaunchKernelGGL(lse_final, grid((pl.R + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
   // the second pass over the keys walks the heads in reverse (cache reuse)
-  if (wide) hipLaunchKernelGGL((score_accum<T, D, kRowChunkWide>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1);
-  else hipLaunchKernelGGL((score_accum<T, D, kRowChunk>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1);
-  RESKV_CHECK();
+  hipLaunchKernelGGL((score_accum<T, D, RC>), grid(pl.NSC), dim3(kThreads), 0, st, a, 1); RESKV_CHECK();
   return hipSuccess;
+}
+
+// Raw window scores of every scored position (lse, then weights summed).
+// The wide chunk only at bf16 rows or rows of 64 (fp32 rows of 128 would
+// hold one block per CU).
+template <typename T, int D>
+hipError_t launch_scores_typed(const BuildPlan& pl, const BuildArgs& a, hipStream_t st) {
+  if constexpr (sizeof(T) == 2 || D == 64)
+    if (pl.R > kRowChunk) return launch_score_passes<T, D, kRowChunkWide>(pl, a, st);
+  return launch_score_passes<T, D, kRowChunk>(pl, a, st);
 }
 
 // Pooling, selection, gather and the Lloyd rounds of one candidate.
@@ -1578,7 +1601,9 @@ hipError_t launch_candidate_typed(const BuildPlan& pl, const BuildArgs& a, hipSt
                        (size_t)pl.T * pl.B * pl.Hkv * pl.S, -1);
     RESKV_CHECK();
   }
-  hipLaunchKernelGGL(pool_scores, grid((pl.S + kThreads - 1) / kThreads), dim3(kThreads), 0, st, a); RESKV_CHECK();
+  hipLaunchKernelGGL(pool_scores, grid((pl.S + kThreads * kPoolPer - 1) / (kThreads * kPoolPer)), dim3(kThreads), 0,
+                     st, a);
+  RESKV_CHECK();
   if (alloc_meta) {
     hipLaunchKernelGGL(adakv_alloc, dim3(pl.B), dim3(kAdaThreads), 0, st, a, alloc_meta, safeguard);
     RESKV_CHECK();

@@ -141,13 +141,15 @@ def test_build_is_deterministic():
         np.testing.assert_array_equal(a[k], b[k])
 
 
-@pytest.mark.parametrize("scorer", ["h2o", "tova", "pool3"])
+@pytest.mark.parametrize("scorer", ["h2o", "tova", "pool3", "pool9", "pool31"])
 def test_build_alternative_scorers(scorer):
     """The compared scorers of App. B.2.2 through the same selection and
     residual path: H2O (accumulated window attention, no pooling, 64 recent
     tokens), TOVA (last-token window w = 1, no pooling, 1 recent token), and
-    a 3-tap pooling; ragged lengths, G = 4, bf16, d = 128."""
-    window, recent, pool = {"h2o": (8, 64, 1), "tova": (1, 1, 1), "pool3": (8, 8, 3)}[scorer]
+    3-, 9- and 31-tap (the largest accepted) pooling; ragged lengths, G = 4,
+    bf16, d = 128."""
+    window, recent, pool = {"h2o": (8, 64, 1), "tova": (1, 1, 1), "pool3": (8, 8, 3), "pool9": (8, 8, 9),
+                            "pool31": (8, 8, 31)}[scorer]
     wl = synth.tiny_workload(s=900, d=128, hq=8, hkv=2, budget=160, res=0, window=window, dtype="bf16", batch=2,
                              n_heavy=6)
     wl.ctx = [900, 517]
