@@ -5,8 +5,11 @@ Parity contract for construction (scores, selection, Lloyd, entries):
   * selection from the GPU's own fp32 scores is exact: the oracle's selection
     run on those scores reproduces main_idx bit for bit;
   * main_idx equals the oracle's own fp64 selection except where the oracle's
-    scores at the k_top boundary are closer than the score tolerance
-    (certified near-ties, counted and returned);
+    scores at the k_top boundary are closer than twice the score tolerance,
+    absolute floor included (certified near-ties, counted and returned): a
+    window row's probabilities below fp32's normal range are zero in the
+    kernel, so where fewer than k_top positions score above the floor the
+    kernel's choice among its zero scores is the lowest positions;
   * Lloyd replay: in every round each evicted token's GPU group is an
     eps-argmin of the fp64 distances to the centres the oracle recomputes from
     the GPU's previous round (the first round uses the seeds the oracle selects
@@ -26,6 +29,7 @@ from oracle import reskv_oracle as orc
 from paper_2607_29591_amd import reskv as rk
 
 SCORE_RTOL = 1e-4
+SCORE_ATOL = 1e-30  # scores below fp32's normal range carry no relative precision
 
 
 def to_dev(x, dtype):
@@ -198,7 +202,7 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
         raw = orc.window_raw_scores(K, Qw, fit)
         ref = orc.pool(raw[:n], pool)
         err = np.abs(gs - ref)
-        assert (err <= SCORE_RTOL * np.abs(ref) + 1e-30).all(), \
+        assert (err <= SCORE_RTOL * np.abs(ref) + SCORE_ATOL).all(), \
             f"score err {(err / np.maximum(np.abs(ref), 1e-30)).max():.2e}"
     # (i) exact selection on the GPU's own scores
     main_g, ev_g, seeds_g = orc.select_top(gs, s, n, kt, r)
@@ -210,7 +214,8 @@ def check_head(wl, x, got, b, h, recent=None, iters=None, full_oracle=True, repl
         if not np.array_equal(main_o, main_g):
             srt = np.sort(ref)[::-1]
             gap = abs(srt[kt - 1] - srt[kt]) if 0 < kt < n else 0.0
-            assert gap <= 2 * SCORE_RTOL * srt[max(kt - 1, 0)], "selection differs outside a near-tie"
+            assert gap <= 2 * (SCORE_RTOL * srt[max(kt - 1, 0)] + SCORE_ATOL), \
+                "selection differs outside a near-tie"
             rep["near_ties"] += 1
     # cache main rows are exact copies
     np.testing.assert_array_equal(got["kc"][b, h, r:r + ml], K[midx])
