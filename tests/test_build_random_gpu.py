@@ -34,7 +34,7 @@ def draw_case(seed):
     return rng, dtype, d, G, hkv, batch, window, pool, ctx, budget, n_heavy, res
 
 
-@pytest.mark.parametrize("seed", list(range(10)))
+@pytest.mark.parametrize("seed", list(range(30)))
 def test_build_random_geometry(seed):
     rng, dtype, d, G, hkv, batch, window, pool, ctx, budget, n_heavy, res = draw_case(seed)
     wl = synth.tiny_workload(s=max(ctx), d=d, hq=G * hkv, hkv=hkv, budget=max(budget), res=0, window=window,

@@ -1,13 +1,17 @@
-"""GPU parity of reskv_decode_attn on seeded random shapes (Sec. 5.4
+"""GPU parity of the decode entry points on seeded random shapes (Sec. 5.4
 shared-softmax decode, Sec. 5.5.2 gate, App. D Algorithm 2).
 
 Each seed draws a cache geometry (group size, head dim, storage type, slot
 capacity, residual capacity, per-head residual and main lengths), a gate, a
 per-query or scalar threshold, and whether this step's token is appended in
-the call; every query head is compared with the oracle decoding the same
-cache (after the append), to the bar of the other decode tests. About half
-of the seeds have 256 (b, kv head) pairs (the one-block-per-head kernel),
-the others a few pairs (the split kernels).
+the call. reskv_decode_attn, reskv_decode_attn_ragged (where its plan
+applies: groups up to 8, bf16 or rows of 64) and reskv_decode_attn_static
+(where the split records fit its 16 MiB) each run on fresh copies of the
+same inputs; for each, every query head is compared with the oracle
+decoding the same cache (after the append), to the bar of the other decode
+tests, and the appended rows and lengths bit for bit. About half of the
+seeds have 256 (b, kv head) pairs (the one-block-per-head kernel), the
+others a few pairs (the split kernels).
 """
 
 import numpy as np
@@ -19,6 +23,8 @@ from paper_2607_29591_amd import reskv as rk
 from tests.helpers import TOL, random_cache, rel_err_rows, to_dev
 
 pytestmark = pytest.mark.gpu
+
+STATIC_SCRATCH_BYTES = 16 << 20
 
 
 def draw_case(seed):
@@ -46,7 +52,7 @@ def draw_case(seed):
     return rng, dtype, d, G, B, Hkv, C, Rcap, res, main, gate, per_query_tau, append
 
 
-@pytest.mark.parametrize("seed", list(range(16)))
+@pytest.mark.parametrize("seed", list(range(40)))
 def test_decode_random_shape(seed):
     rng, dtype, d, G, B, Hkv, C, Rcap, res, main, gate, per_query_tau, append = draw_case(seed)
     Hq = G * Hkv
@@ -56,47 +62,63 @@ def test_decode_random_shape(seed):
         q.astype(np.float32).astype(np.float64)
     tau = rng.normal(0.3, 0.2, size=(B, Hq)) if per_query_tau else None
     shape = rk.make_shape(B, Hq, Hkv, d, dtype, C, Rcap)
-
-    kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
-    lcd = torch.as_tensor(logc.astype(np.float32)).cuda()
-    rl = torch.as_tensor(res.astype(np.int32).reshape(-1)).cuda()
-    ml = torch.as_tensor(main.astype(np.int32).reshape(-1)).cuda()
-    out = torch.full((B, Hq, d), float("nan"), device="cuda")
-    lm = torch.empty(B * Hq, device="cuda")
-    lr = torch.empty(B * Hq, device="cuda")
-    gt = torch.empty(B * Hq, device="cuda")
-    taud = None if tau is None else torch.as_tensor(tau.astype(np.float32).reshape(-1)).cuda()
-    ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
-    kn = vn = knd = vnd = None
+    kn = vn = None
     if append:
         kn, vn = rng.normal(size=(B, Hkv, d)), rng.normal(size=(B, Hkv, d))
-        knd, vnd = to_dev(kn, dtype), to_dev(vn, dtype)
-    rk.reskv_decode_attn(shape, rk.make_gate(tau=taud, **gate), to_dev(q, dtype), kcd, vcd, lcd, rl, ml, out, ws,
-                         lm, lr, gt, k_new=knd, v_new=vnd)
-    torch.cuda.synchronize()
 
-    main2 = main.copy()
+    # the expected caches and lengths after the call, and the oracle's outputs
+    kc2, vc2, main2 = kc.copy(), vc.copy(), main.copy()
     if append:  # the token becomes main slot r + n wherever the cache has room
+        knr = to_dev(kn, dtype).double().cpu().numpy()
+        vnr = to_dev(vn, dtype).double().cpu().numpy()
         for b in range(B):
             for h in range(Hkv):
                 slot = res[b, h] + main[b, h]
                 if slot < C:
-                    kc[b, h, slot] = knd[b, h].double().cpu().numpy()
-                    vc[b, h, slot] = vnd[b, h].double().cpu().numpy()
+                    kc2[b, h, slot], vc2[b, h, slot] = knr[b, h], vnr[b, h]
                     main2[b, h] += 1
-        np.testing.assert_array_equal(kcd.double().cpu().numpy(), kc)
-        np.testing.assert_array_equal(vcd.double().cpu().numpy(), vc)
-    np.testing.assert_array_equal(ml.cpu().numpy().reshape(B, Hkv), main2)
-
     t = gate["tau_scalar"] if tau is None else tau.astype(np.float32).astype(np.float64)
-    ref, lse_m, lse_r, g = orc.decode(q, kc, vc, logc, res, main2, t, gate["alpha"], gate["g_min"], gate["beta"])
-    got = out.double().cpu().numpy()
-    assert np.isfinite(got).all()
-    err = rel_err_rows(got, ref)
-    assert err.max() <= TOL[dtype], f"max rel err {err.max():.3e}"
-    np.testing.assert_allclose(gt.double().cpu().numpy().reshape(B, Hq), g, rtol=1e-5, atol=1e-6)
-    np.testing.assert_allclose(lm.double().cpu().numpy().reshape(B, Hq), lse_m, rtol=1e-5, atol=1e-5)
-    got_lr = lr.double().cpu().numpy().reshape(B, Hq)
+    ref, lse_m, lse_r, g = orc.decode(q, kc2, vc2, logc, res, main2, t, gate["alpha"], gate["g_min"], gate["beta"])
     fin = np.isfinite(lse_r)
-    assert (np.isfinite(got_lr) == fin).all()
-    np.testing.assert_allclose(got_lr[fin], lse_r[fin], rtol=1e-5, atol=1e-5)
+
+    entries = ["workspace"]
+    if rk.reskv_decode_ragged_workspace_size(shape) > 0:
+        entries.append("ragged")
+    if rk.reskv_decode_workspace_size(shape) <= STATIC_SCRATCH_BYTES:
+        entries.append("static")
+    for entry in entries:
+        kcd, vcd = to_dev(kc, dtype), to_dev(vc, dtype)
+        lcd = torch.as_tensor(logc.astype(np.float32)).cuda()
+        rl = torch.as_tensor(res.astype(np.int32).reshape(-1)).cuda()
+        ml = torch.as_tensor(main.astype(np.int32).reshape(-1)).cuda()
+        out = torch.full((B, Hq, d), float("nan"), device="cuda")
+        lm = torch.empty(B * Hq, device="cuda")
+        lr = torch.empty(B * Hq, device="cuda")
+        gt = torch.empty(B * Hq, device="cuda")
+        taud = None if tau is None else torch.as_tensor(tau.astype(np.float32).reshape(-1)).cuda()
+        knd = to_dev(kn, dtype) if append else None
+        vnd = to_dev(vn, dtype) if append else None
+        args = (shape, rk.make_gate(tau=taud, **gate), to_dev(q, dtype), kcd, vcd, lcd, rl, ml, out)
+        if entry == "workspace":
+            ws = torch.zeros(rk.reskv_decode_workspace_size(shape), dtype=torch.uint8, device="cuda")
+            rk.reskv_decode_attn(*args, ws, lm, lr, gt, k_new=knd, v_new=vnd)
+        elif entry == "ragged":
+            ws = torch.zeros(rk.reskv_decode_ragged_workspace_size(shape), dtype=torch.uint8, device="cuda")
+            rk.reskv_decode_attn_ragged(*args, ws, lm, lr, gt, k_new=knd, v_new=vnd)
+        else:
+            rk.reskv_decode_attn_static(*args, lm, lr, gt, k_new=knd, v_new=vnd)
+        torch.cuda.synchronize()
+
+        np.testing.assert_array_equal(ml.cpu().numpy().reshape(B, Hkv), main2, err_msg=entry)
+        np.testing.assert_array_equal(kcd.double().cpu().numpy(), kc2, err_msg=entry)
+        np.testing.assert_array_equal(vcd.double().cpu().numpy(), vc2, err_msg=entry)
+        got = out.double().cpu().numpy()
+        assert np.isfinite(got).all(), entry
+        err = rel_err_rows(got, ref)
+        assert err.max() <= TOL[dtype], f"{entry}: max rel err {err.max():.3e}"
+        np.testing.assert_allclose(gt.double().cpu().numpy().reshape(B, Hq), g, rtol=1e-5, atol=1e-6, err_msg=entry)
+        np.testing.assert_allclose(lm.double().cpu().numpy().reshape(B, Hq), lse_m, rtol=1e-5, atol=1e-5,
+                                   err_msg=entry)
+        got_lr = lr.double().cpu().numpy().reshape(B, Hq)
+        assert (np.isfinite(got_lr) == fin).all(), entry
+        np.testing.assert_allclose(got_lr[fin], lse_r[fin], rtol=1e-5, atol=1e-5, err_msg=entry)
