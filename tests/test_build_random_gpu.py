@@ -46,3 +46,32 @@ def test_build_random_geometry(seed):
     for b in range(batch):
         for h in range(hkv):
             check_head(wl, x, got, b, h, pool=pool if pool > 0 else 5, lloyd_info=False)
+
+
+def draw_long_case(seed):
+    rng = np.random.default_rng(3000 + seed)
+    dtype = ["bf16", "f32"][seed % 2]
+    d = [128, 64][(seed // 2) % 2]
+    G = int(rng.choice([1, 4, 7]))
+    hkv = int(rng.choice([1, 2]))
+    window = int(rng.choice([4, 8, 32]))
+    ctx = [int(rng.integers(8193, 40000))]
+    budget = [int(rng.integers(64, 1100))]
+    n_heavy = [int(rng.integers(4, 64))]
+    res = np.array([[[int(rng.integers(0, 65)) for _ in range(hkv)]]])
+    return dtype, d, G, hkv, window, ctx, budget, n_heavy, res
+
+
+@pytest.mark.parametrize("seed", list(range(8)))
+def test_build_random_long_context(seed):
+    """Contexts of 8K-40K tokens: the top-k selection spans several 8192-score
+    blocks with thresholds wherever the draw puts them."""
+    dtype, d, G, hkv, window, ctx, budget, n_heavy, res = draw_long_case(seed)
+    wl = synth.tiny_workload(s=ctx[0], d=d, hq=G * hkv, hkv=hkv, budget=budget[0], res=0, window=window,
+                             dtype=dtype, batch=1)
+    wl.n_heavy, wl.res = n_heavy, res
+    x = synth.gen_layer(wl, 0, seed=60 + seed, n_decode=1)
+    x["K_host"], x["V_host"], x["q_host"] = x["K"], x["V"], x["q_obs"]
+    got = run_build(wl, x)
+    for h in range(hkv):
+        check_head(wl, x, got, 0, h, lloyd_info=False)
