@@ -925,9 +925,8 @@ __global__ __launch_bounds__(kHeadThreads) void decode_ragged(DecodeArgs a) {
   // blocks
   const int NB = max(1, min(max(a.rag_blocks, (U + kRagUnits - 1) / kRagUnits), U / a.rag_min_units));
   const int blk = blockIdx.x;
-  if (blk == 0) {  // the plan the combine kernel reads: prefix, U, NB, block starts
+  if (blk == 0) {  // the plan the combine kernel reads: prefix, U, NB
     for (int h = tid; h < BH; h += kHeadThreads) a.plan[h] = s_pre[h];
-    for (int b = tid; b <= NB; b += kHeadThreads) a.plan[BH + 2 + b] = rag_lo(b, U, NB);
     if (tid == 0) { a.plan[BH] = U; a.plan[BH + 1] = NB; }
   }
   if (blk >= NB) return;  // block-uniform
@@ -1054,42 +1053,68 @@ __global__ __launch_bounds__(kHeadThreads) void decode_ragged(DecodeArgs a) {
 
 // Heads shared by several blocks: merge their records (ascending block
 // order), apply the gate and write the outputs; then advance every head's
-// main_len by the appended token. One block per (b, kv head).
+// main_len by the appended token. One block per (b, kv head). The blocks
+// that share a head follow from the plan's unit count and block count alone
+// (block b starts at unit b U / NB), so after the lengths and the plan the
+// records' (max, sum) and the first kPF records' accumulator rows are all
+// requested at once.
 template <int D, int GP>
 __global__ __launch_bounds__(kThreads) void decode_ragged_combine(DecodeArgs a) {
-  __shared__ int s_idx[kRagMaxRec];
+  __shared__ int s_idx[kRagMaxRec];         // record of slot i: (block, edge), -1 if the block streamed nothing
   __shared__ float s_w[kRagMaxRec][2][GP];  // record max, then its weight e^{m - M}
   __shared__ float s_lr[kRagMaxRec][2][GP]; // record sum
   __shared__ float s_lw[2][GP];             // merged sums
   __shared__ float s_mx[2][GP];             // merged maxima
-  __shared__ int s_nrec;
   const int bh = blockIdx.x, tid = threadIdx.x;
   int r, n, ur, um;
   bool app;
   rag_units(a, bh, r, n, ur, um, app);
   const int U = a.plan[a.BH], NB = a.plan[a.BH + 1];
-  const int* blo = a.plan + a.BH + 2;  // block starts
   const int P0 = a.plan[bh];
   const int b0 = rag_block(P0, U, NB), b1 = rag_block(P0 + ur + um - 1, U, NB);
   const bool shared = ur + um > 0 && b0 != b1;
   constexpr int kRec = GP * (D + 2);  // floats per (block, edge, kind) record
+  constexpr int kOut = (GP * D + kThreads - 1) / kThreads;
+  constexpr int kPF = 8;  // records whose accumulator rows are requested together
   if (shared) {
-    // the head's records: blocks with an empty range left none; the head's
-    // first block holds it as its last head unless the block starts with it
-    if (tid == 0) {
-      int c = 0;
-      for (int bb = b0; bb <= b1 && c < kRagMaxRec; ++bb)
-        if (blo[bb] < blo[bb + 1]) s_idx[c++] = bb * 2 + (blo[bb] >= P0 ? 0 : 1);
-      s_nrec = c;
+    const int nrec = min(b1 - b0 + 1, kRagMaxRec);
+    // slot i = block b0 + i; the head's first block holds it as its last
+    // head unless the block starts with it; a block with an empty range left
+    // no record
+    for (int i = tid; i < nrec; i += kThreads) {
+      const int bb = b0 + i;
+      const int lo = rag_lo(bb, U, NB), hi = rag_lo(bb + 1, U, NB);
+      s_idx[i] = lo < hi ? bb * 2 + (lo >= P0 ? 0 : 1) : -1;
     }
     __syncthreads();
-    const int nrec = s_nrec;
-    // every record's (max, sum) per kind and query head, loaded at once
+    // every record's (max, sum) per kind and query head, and the first kPF
+    // records' accumulator rows of this thread's outputs, requested together
     for (int x = tid; x < nrec * 2 * GP; x += kThreads) {
       const int i = x / (2 * GP), kind = (x / GP) % 2, h = x % GP;
-      const float* rc = a.rec + ((size_t)s_idx[i] * 2 + kind) * kRec;
-      s_w[i][kind][h] = rc[GP * D + h];
-      s_lr[i][kind][h] = rc[GP * D + GP + h];
+      float m = kNegInf, l = 0.f;
+      if (s_idx[i] >= 0) {
+        const float* rc = a.rec + ((size_t)s_idx[i] * 2 + kind) * kRec;
+        m = rc[GP * D + h];
+        l = rc[GP * D + GP + h];
+      }
+      s_w[i][kind][h] = m;
+      s_lr[i][kind][h] = l;
+    }
+    // accumulator row of slot i, kind, output (h, d): slots past nrec or of
+    // blocks without a record read slot 0's record (the head's first block
+    // always streamed some of it) and get weight 0
+    auto acc_at = [&](int i, int kind, int h, int d) {
+      const int ri = i < nrec && s_idx[i] >= 0 ? s_idx[i] : s_idx[0];
+      return a.rec[((size_t)ri * 2 + kind) * kRec + h * D + d];
+    };
+    float pv[kOut][kPF][2];
+#pragma unroll
+    for (int k = 0; k < kOut; ++k) {
+      const int idx = min(tid + k * kThreads, a.G * D - 1), h = idx / D, d = idx % D;
+#pragma unroll
+      for (int i = 0; i < kPF; ++i)
+#pragma unroll
+        for (int kind = 0; kind < 2; ++kind) pv[k][i][kind] = acc_at(i, kind, h, d);
     }
     __syncthreads();
     if (tid < 2 * GP) {
@@ -1098,7 +1123,7 @@ __global__ __launch_bounds__(kThreads) void decode_ragged_combine(DecodeArgs a) 
       for (int i = 0; i < nrec; ++i) M = fmaxf(M, s_w[i][kind][h]);
       float L = 0.f;
       for (int i = 0; i < nrec; ++i) {
-        const float w = M != kNegInf ? exp2f(s_w[i][kind][h] - M) : 0.f;
+        const float w = M != kNegInf && s_w[i][kind][h] != kNegInf ? exp2f(s_w[i][kind][h] - M) : 0.f;
         s_w[i][kind][h] = w;
         L = fmaf(w, s_lr[i][kind][h], L);
       }
@@ -1107,13 +1132,29 @@ __global__ __launch_bounds__(kThreads) void decode_ragged_combine(DecodeArgs a) 
     }
     __syncthreads();
     const int b = bh / a.Hkv, kvh = bh - b * a.Hkv;
-    for (int idx = tid; idx < a.G * D; idx += kThreads) {
+#pragma unroll
+    for (int k = 0; k < kOut; ++k) {
+      const int idx = tid + k * kThreads;
+      if (idx >= a.G * D) continue;
       const int h = idx / D, d = idx % D;
       float Ok[2] = {0.f, 0.f};
 #pragma unroll
-      for (int kind = 0; kind < 2; ++kind)
-        for (int i = 0; i < nrec; ++i)
-          Ok[kind] = fmaf(s_w[i][kind][h], a.rec[((size_t)s_idx[i] * 2 + kind) * kRec + h * D + d], Ok[kind]);
+      for (int i = 0; i < kPF; ++i)
+#pragma unroll
+        for (int kind = 0; kind < 2; ++kind)
+          if (i < nrec) Ok[kind] = fmaf(s_w[i][kind][h], pv[k][i][kind], Ok[kind]);
+      for (int i0 = kPF; i0 < nrec; i0 += kPF) {  // further records, kPF at a time
+        float v[kPF][2];
+#pragma unroll
+        for (int i = 0; i < kPF; ++i)
+#pragma unroll
+          for (int kind = 0; kind < 2; ++kind) v[i][kind] = acc_at(i0 + i, kind, h, d);
+#pragma unroll
+        for (int i = 0; i < kPF; ++i)
+#pragma unroll
+          for (int kind = 0; kind < 2; ++kind)
+            if (i0 + i < nrec) Ok[kind] = fmaf(s_w[i0 + i][kind][h], v[i][kind], Ok[kind]);
+      }
       const int qh = b * a.Hq + kvh * a.G + h;
       float gg;
       const float Mm = s_mx[1][h], Lm = s_lw[1][h], Mr = s_mx[0][h], Lr = s_lw[0][h];
@@ -1242,7 +1283,7 @@ bool make_ragged_plan(const reskv_shape_t& s, RaggedPlan* plan) {
   const long long nb = (umax + kRagUnits - 1) / kRagUnits;
   p.blocks = (int)(nb > kRagMinBlocks ? nb : kRagMinBlocks);
   p.plan_off = 0;
-  p.rec_off = align_up((size_t)(p.BH + 3 + p.blocks) * sizeof(int32_t), 256);
+  p.rec_off = align_up((size_t)(p.BH + 2) * sizeof(int32_t), 256);
   p.bytes = p.rec_off + align_up((size_t)p.blocks * 4 * p.GP * (s.head_dim + 2) * sizeof(float), 256);
   return true;
 }
