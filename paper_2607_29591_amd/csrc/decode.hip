@@ -972,9 +972,10 @@ __global__ __launch_bounds__(kHeadThreads) void decode_ragged(DecodeArgs a) {
       cur_bh = bh;
     }
     if (is_res) load_unit_lc<T, D>(ur_, a.logc + (size_t)bh * a.Rcap, s0, nvalid, g);
+    // the value rows are requested before the logits wait on the keys
+    load_unit_v<T, D>(ur_, vc, s0, nvalid, hd, g, app_row, vn);
     float sc[kTiles][4];
     unit_logits<T, D>(ur_, q, a.qk_scale, sc);
-    load_unit_v<T, D>(ur_, vc, s0, nvalid, hd, g, app_row, vn);
     softmax_pv<T, D>(st, ur_, sc, 0, nvalid, is_res, a.beta_log2, g);
     if (app_row >= s0 && app_row < s0 + nvalid) {  // wave-uniform: the new rows into the cache
       constexpr int kPieces = D * (int)sizeof(T) / 16;
