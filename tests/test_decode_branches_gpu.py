@@ -101,3 +101,21 @@ def test_branches_whole_head_shape():
     res = rng.choice([0, 64, 128], size=(B, Hkv))
     main = rng.integers(100, 384, size=(B, Hkv))
     run_case(6, B, G * Hkv, Hkv, 128, "bf16", 512, 128, res, main)
+
+
+@pytest.mark.parametrize("seed", list(range(12)))
+def test_branches_random_shapes(seed):
+    """Seeded random geometries: group size, head dim, storage type, slot and
+    residual capacities, per-head lengths, threshold kind and gate floor."""
+    rng = np.random.default_rng(6000 + seed)
+    dtype = ["bf16", "f32"][seed % 2]
+    d = [64, 128][(seed // 2) % 2]
+    G = int(rng.choice([1, 2, 3, 4, 7, 8, 16]))
+    Hkv = int(rng.choice([1, 2, 3]))
+    B = int(rng.integers(1, 5))
+    C = int(rng.integers(8, 1200))
+    Rcap = int(rng.integers(1, 400))
+    res = rng.integers(0, min(Rcap, C - 1) + 1, size=(B, Hkv))
+    main = np.array([[int(rng.integers(1, C - r + 1)) for r in row] for row in res])
+    run_case(7000 + seed, B, G * Hkv, Hkv, d, dtype, C, Rcap, res, main,
+             tau_kind=str(rng.choice(["scalar", "normal"])), g_min=float(rng.choice([0.0, 0.3])))
