@@ -677,6 +677,9 @@ def main():
         graph_check = "bitwise equal to eager calls" if torch.equal(out, out_graph) else "MISMATCH with eager calls"
     build_ms = sum(a.elapsed_time(b) for a, b, _ in phase) / args.steps
     decode_ms = sum(b.elapsed_time(c) for _, b, c in phase) / args.steps
+    # spread over the timed jobs: per-job decode time and whole-job GPU time
+    dec_job_ms = [b.elapsed_time(c) for _, b, c in phase]
+    job_ms = [a.elapsed_time(c) for a, _, c in phase]
 
     # algorithmic bytes
     build_bytes = sum(build_call_bytes(wl, elem, res_layers[l]) for l in range(L))
@@ -731,7 +734,9 @@ def main():
                                 "reskv_decode_attn (per layer-step: decode_split over 256-slot blocks with the "
                                 "append fused, decode_combine with the gate)"),
                      "bytes_per_call": avg_bytes, "us_per_call": avg_ms * 1e3,
+                     "us_per_call_range": [min(dec_job_ms) / calls * 1e3, max(dec_job_ms) / calls * 1e3],
                      "calls_timed": calls * args.steps},
+        "job_ms_range": [min(job_ms), max(job_ms)],
         "setup_s": t_setup,
         "decode_launch": decode_launch,
         "decode_graph_check": graph_check,
