@@ -614,6 +614,10 @@ __global__ __launch_bounds__(kThreads) void merge_branches_kernel(const float* o
 // to scratch and ran 1.5-3x slower.
 constexpr int kHeadWaves = 8;
 constexpr int kHeadThreads = 64 * kHeadWaves;
+// Head-dependent start of the main-only blocks past the first round:
+// (kStaggerMul * bh) mod kStaggerMod blocks, taken modulo their count.
+constexpr int kStaggerMod = 24;
+constexpr int kStaggerMul = 5;
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
@@ -629,11 +633,17 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
   // 64-slot blocks [64 u, 64 u + 64), each of one kind: the block holding
   // slot r, when r is not a multiple of 64, is unit u = UR - 1 for its
   // residual slots and one extra unit u = NB, dealt last, for its main slots.
-  // Units go round-robin to the waves, so every wave streams about the same
-  // number of slots whatever the split between the kinds, and a wave meets
-  // its residual units before its main ones. A wave's first unit is slots
-  // [64 wave, 64 wave + 64) (unless it is the extra unit), so its keys are
-  // requested before the cache lengths are read.
+  // Units go round-robin to the waves in processing order p = wave, wave + 8,
+  // ..., so every wave streams about the same number of slots whatever the
+  // split between the kinds, and a wave meets its residual units before its
+  // main ones. The first round (p < 8) and the residual units take the
+  // natural order, so a wave's first unit is slots [64 wave, 64 wave + 64)
+  // (unless it is the extra unit) and its keys are requested before the
+  // cache lengths are read. The main-only blocks after them start at a
+  // head-dependent block and wrap around: with every head streamed from
+  // slot 0 in step, some head strides put the concurrent streams of many
+  // heads on the same memory channels (a 2064-slot capacity ran nearly 30%
+  // slower than a 2080-slot one); staggering the heads spreads them.
   UnitRegs<T, D> ur0;
   load_unit_k<T, D>(ur0, kc, kUnit * wave, a.C - 1, hd, g, -1, nullptr);
   int r, n;
@@ -721,10 +731,19 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
             ur.v[4 * T4 + uu].store(vc + (size_t)app_row * D + VPiece<T, D>::kElems * hd);
     }
   };
+  // processing order -> unit: blocks [lo, NB) start at block lo + ro
+  const int lo = max(kHeadWaves, UR);
+  const int nM = NB - lo;
+  const int ro = nM > 0 ? (bh * kStaggerMul) % kStaggerMod % nM : 0;
+  auto unit_of = [&](int p) {
+    if (p < lo || p >= NB) return p;
+    const int q = p - lo + ro;
+    return lo + (q < nM ? q : q - nM);
+  };
   if (wave < U) {
     bool is_res;
     int s0, end;
-    unit_range(wave, is_res, s0, end);
+    unit_range(unit_of(wave), is_res, s0, end);
     if (s0 != kUnit * wave) {
       load_unit_k<T, D>(ur0, kc, s0, end - 1, hd, g, app_row, kn);
     } else if (app_row >= s0 && app_row < s0 + kUnit) {
@@ -732,9 +751,10 @@ __global__ __launch_bounds__(kHeadThreads) void decode_head(DecodeArgs a) {
       for (int t = 0; t < kTiles; ++t)
         if (min(s0 + 16 * t + hd, a.C - 1) == app_row) ur0.k[t].load(kn, g);
     }
-    run_unit(wave, ur0);
+    run_unit(unit_of(wave), ur0);
   }
-  for (int u = wave + kHeadWaves; u < U; u += kHeadWaves) {
+  for (int p = wave + kHeadWaves; p < U; p += kHeadWaves) {
+    const int u = unit_of(p);
     bool is_res;
     int s0, end;
     unit_range(u, is_res, s0, end);

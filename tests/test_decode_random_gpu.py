@@ -11,7 +11,11 @@ same inputs; for each, every query head is compared with the oracle
 decoding the same cache (after the append), to the bar of the other decode
 tests, and the appended rows and lengths bit for bit. About half of the
 seeds have 256 (b, kv head) pairs (the one-block-per-head kernel), the
-others a few pairs (the split kernels).
+others a few pairs (the split kernels). Ten more seeds draw 256 pairs of
+520-1400-slot caches with up to 800 residual entries, so the one-block-per-
+head kernel streams main blocks past its first round in its staggered
+order, residual units run past the first round, and the block holding slot
+r is split between the kinds.
 """
 
 import numpy as np
@@ -27,13 +31,19 @@ pytestmark = pytest.mark.gpu
 STATIC_SCRATCH_BYTES = 16 << 20
 
 
-def draw_case(seed):
-    rng = np.random.default_rng(1000 + seed)
+def draw_case(seed, long_heads=False):
+    rng = np.random.default_rng(1000 + seed + (500 if long_heads else 0))
     dtype = ["bf16", "f32"][seed % 2]
     d = [64, 128][(seed // 2) % 2]
     G = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 12, 16]))
-    whole = (seed // 4) % 2 == 0 and (dtype == "bf16" or d == 64)
-    if whole:
+    whole = long_heads or ((seed // 4) % 2 == 0 and (dtype == "bf16" or d == 64))
+    if long_heads:  # heads past the first round of eight 64-slot blocks
+        dtype = "bf16" if d == 128 else dtype
+        Hkv = int(rng.choice([1, 2, 4, 8]))
+        B = 256 // Hkv
+        C = int(rng.integers(520, 1400))
+        Rcap = int(rng.integers(1, 800))
+    elif whole:
         Hkv = int(rng.choice([1, 2, 4, 8]))
         B = 256 // Hkv
         C = int(rng.integers(8, 360))
@@ -52,9 +62,9 @@ def draw_case(seed):
     return rng, dtype, d, G, B, Hkv, C, Rcap, res, main, gate, per_query_tau, append
 
 
-@pytest.mark.parametrize("seed", list(range(40)))
-def test_decode_random_shape(seed):
-    rng, dtype, d, G, B, Hkv, C, Rcap, res, main, gate, per_query_tau, append = draw_case(seed)
+@pytest.mark.parametrize("long_heads,seed", [(False, s) for s in range(40)] + [(True, s) for s in range(10)])
+def test_decode_random_shape(long_heads, seed):
+    rng, dtype, d, G, B, Hkv, C, Rcap, res, main, gate, per_query_tau, append = draw_case(seed, long_heads)
     Hq = G * Hkv
     kc, vc, logc = random_cache(rng, B, Hkv, C, Rcap, d, dtype, res, main)
     q = rng.normal(size=(B, Hq, d)) * 1.5
