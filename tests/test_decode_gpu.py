@@ -74,6 +74,32 @@ def test_decode_gate_variants(dtype):
     check(dtype, shape, q, kc, vc, logc, res, main, tau=tau)
     check(dtype, shape, q, kc, vc, logc, res, main, gate=dict(tau_scalar=0.25, alpha=12.0, g_min=1.0, beta=1.0))
     check(dtype, shape, q, kc, vc, logc, res, main, gate=dict(tau_scalar=0.9, alpha=3.0, g_min=0.2, beta=0.5))
+    for gate in GATE_EDGES:
+        check(dtype, shape, q, kc, vc, logc, res, main, gate=gate)
+
+
+# Degenerate gate settings (Sec. 5.5.2; beta weights log c_j in the residual
+# logits): no count weighting, a constant gate of 1/2 (alpha = 0), the gate
+# pinned at 1 by g_min, a threshold far below every p_max (the sigmoid
+# underflows: gate 0 in fp32, ~1e-262 in the fp64 oracle, the residual
+# entries switched off either way) and far above it (gate 1).
+GATE_EDGES = [dict(tau_scalar=0.25, alpha=12.0, g_min=0.0, beta=0.0),
+              dict(tau_scalar=0.25, alpha=0.0, g_min=0.0, beta=1.0),
+              dict(tau_scalar=0.25, alpha=0.0, g_min=1.0, beta=0.0),
+              dict(tau_scalar=-50.0, alpha=12.0, g_min=0.0, beta=1.0),
+              dict(tau_scalar=50.0, alpha=12.0, g_min=0.0, beta=1.0)]
+
+
+def test_decode_gate_edges_one_block_per_head():
+    """The gate edge settings on the one-block-per-head kernel (256 (b, kv
+    head) pairs), whose epilogue evaluates the gate and shared denominator."""
+    B, Hkv, G, d, C, Rcap = 64, 4, 4, 128, 300, 64
+    rng = np.random.default_rng(8)
+    res = rng.integers(0, Rcap + 1, size=(B, Hkv))
+    main = np.array([[int(rng.integers(1, C - r + 1)) for r in row] for row in res])
+    shape, q, kc, vc, logc = cache_case(9, B, Hkv * G, Hkv, d, "bf16", C, Rcap, res, main)
+    for gate in GATE_EDGES:
+        check("bf16", shape, q, kc, vc, logc, res, main, gate=gate)
 
 
 def test_decode_all_residual_entries_empty():
