@@ -57,6 +57,28 @@ def test_build_ragged_batch_gqa7_and_edge_cases():
             check_head(wl, x, got2, b, h, recent=70)
 
 
+@pytest.mark.parametrize("recent", [None, 4])
+def test_build_window_covers_the_sequence(recent):
+    """s = w, the largest window the boundary accepts: every position is a
+    window query position and the scored range [0, s - |P|) shrinks with the
+    protected window. With the default protected window (|P| = min(w, m, s)
+    = m) every main slot is protected and no top-k is taken; with |P| = 4
+    the top-k runs on [0, s - 4). A 4-token sequence (w = s = 4, budget 2,
+    r = 1) sits beside a 40-token one."""
+    wl = synth.tiny_workload(s=40, d=64, hq=8, hkv=2, budget=24, res=0, window=40, dtype="f32", batch=1, n_heavy=2)
+    wl.res = np.array([[[8, 0]]])
+    x = host_copies(synth.gen_layer(wl, 0, seed=21, n_decode=1))
+    got = run_build(wl, x, recent=recent)
+    for h in range(2):
+        check_head(wl, x, got, 0, h, recent=recent)
+    wl = synth.tiny_workload(s=4, d=64, hq=8, hkv=2, budget=2, res=0, window=4, dtype="f32", batch=1, n_heavy=1)
+    wl.res = np.array([[[1, 0]]])
+    x = host_copies(synth.gen_layer(wl, 0, seed=22, n_decode=1))
+    got = run_build(wl, x, recent=None if recent is None else 1)
+    for h in range(2):
+        check_head(wl, x, got, 0, h, recent=None if recent is None else 1)
+
+
 def test_build_ties_take_lowest_positions():
     """Identical keys and queries give identical window scores; zero-padded
     pooling lowers the two positions at each end of the scored range, so the
