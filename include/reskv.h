@@ -317,9 +317,8 @@ size_t reskv_build_proxy_workspace_size(const reskv_shape_t* shape,
  * on) every head is streamed at once, and a few strides put many heads on
  * the same HBM channels: at 256 heads of 2048 live slots, d = 128, bf16, a
  * call took 48-51 us at most capacities between 2056 and 2552 slots and up
- * to 57 us at the worst one measured (2064). A capacity of budget + decode
- * steps rounded up to a multiple of 8 slots is a reasonable choice; the
- * kernels accept any C.
+ * to 57 us at the worst one measured (2064). The kernels accept any C; a
+ * caller tuning for speed can time a few capacities at its own shape.
  */
 reskv_status_t reskv_decode_attn(const reskv_shape_t* shape,
                                  const reskv_gate_t* gate,
