@@ -33,12 +33,14 @@ def clone(state):
     return {k: v.clone() for k, v in state.items()}
 
 
-@pytest.mark.parametrize("B,Hkv,G", [(64, 4, 4), (2, 2, 7)])
-def test_decode_step_graph_replays_match_eager(B, Hkv, G):
-    """(64, 4, 4): one block per (sequence, KV head) with the append fused;
-    (2, 2, 7): the split-K path (partial blocks with the append fused, then
-    the combine, which advances the main lengths)."""
-    d, C, Rcap = 128, 320, 64
+@pytest.mark.parametrize("B,Hkv,G,C", [(64, 4, 4, 320), (64, 4, 8, 1500), (2, 2, 7, 320)])
+def test_decode_step_graph_replays_match_eager(B, Hkv, G, C):
+    """(64, 4, 4, 320): one block per (sequence, KV head) with the append
+    fused; (64, 4, 8, 1500): the same kernel on caches long enough for the
+    staggered order of the main blocks past the first round; (2, 2, 7, 320):
+    the split-K path (partial blocks with the append fused, then the
+    combine, which advances the main lengths)."""
+    d, Rcap = 128, 64
     shape = rk.make_shape(B, G * Hkv, Hkv, d, "bf16", C, Rcap)
     rng, base = decode_state(B, Hkv, G, d, C, Rcap, 5 + G)
     eager, graphed = clone(base), clone(base)
